@@ -1,0 +1,153 @@
+/*
+ * KV-COBRA oracle, exact integer part: per-token encode and the packed layout.
+ *
+ * Test infrastructure only. Nothing in the product path may link or load
+ * this file; it shares no code with the GPU library.
+ *
+ * Passages followed: calibration/inference table, steps 7-8 (a token's code is
+ * quantize(P x) with the Hadamard rotation folded into P; codes are cached and
+ * dequantized on read); Section 3.4 (one uniform b-bit quantizer per head).
+ *
+ * Definition computed (readings stated in oracle/quant.py and oracle/layout.py):
+ *   y_i = sum_j P_ij x_j, exactly (P and x are fp16, so every product is an
+ *         integer multiple of 2^-48 and the sum fits a 128-bit integer);
+ *   k_i = clamp(floor(y_i / step) + 2^(b-1), 0, 2^b - 1), exactly.
+ * The packed layout is the one documented in oracle/layout.py.
+ *
+ * Build: gcc -O2 -ffp-contract=off -fPIC -shared (no fast-math).
+ */
+#include <stdint.h>
+#include <string.h>
+
+typedef __int128 i128;
+
+/* fp16 bits -> signed integer mantissa and power-of-two exponent. Returns -1 for inf/nan. */
+static int half_parts(uint16_t h, int64_t *m, int *e) {
+    int s = h >> 15, ex = (h >> 10) & 31, fr = h & 1023;
+    if (ex == 31) return -1;
+    if (ex == 0) { *m = fr; *e = -24; }
+    else { *m = 1024 + fr; *e = ex - 25; }
+    if (s) *m = -*m;
+    return 0;
+}
+
+/* step as an exact integer multiple of 2^-48; returns -1 if out of the supported range. */
+static int step_units(float step, i128 *D) {
+    uint32_t u;
+    memcpy(&u, &step, 4);
+    int ex = (u >> 23) & 255;
+    if ((u >> 31) || ex == 0 || ex == 255) return -1;  /* positive normal only */
+    int64_t m = 0x800000 | (u & 0x7fffff);
+    int e = ex - 150;           /* step = m * 2^e */
+    int s = e + 48;
+    if (s < 0 || s > 60) return -1;
+    *D = ((i128)m) << s;
+    return 0;
+}
+
+/* Exact codes: codes[t*r + i] for tokens t < n. Returns 0, or -1 on a non-finite input / bad step. */
+int oracle_encode_codes(const uint16_t *P, int r, int d, float step, int b,
+                        const uint16_t *x, int n, uint8_t *codes) {
+    i128 D;
+    if (step_units(step, &D)) return -1;
+    const int64_t h = (int64_t)1 << (b - 1);
+    const int64_t kmax = ((int64_t)1 << b) - 1;
+    for (int t = 0; t < n; ++t) {
+        const uint16_t *xt = x + (int64_t)t * d;
+        for (int i = 0; i < r; ++i) {
+            const uint16_t *Pi = P + (int64_t)i * d;
+            i128 N = 0;
+            for (int j = 0; j < d; ++j) {
+                int64_t mp, mx; int ep, exx;
+                if (half_parts(Pi[j], &mp, &ep) || half_parts(xt[j], &mx, &exx)) return -1;
+                int s = ep + exx + 48;              /* 0 .. 58 */
+                N += (i128)(mp * mx) * ((i128)1 << s);  /* exact, no overflow */
+            }
+            i128 q = N / D;
+            if ((N % D) != 0 && N < 0) q -= 1;      /* floor division (D > 0) */
+            i128 k = q + h;
+            if (k < 0) k = 0;
+            if (k > kmax) k = kmax;
+            codes[(int64_t)t * r + i] = (uint8_t)k;
+        }
+    }
+    return 0;
+}
+
+static int n_planes(int b, int *w) {
+    if (b == 8) { w[0] = 8; return 1; }
+    int n = 0;
+    if (b & 4) w[n++] = 4;
+    if (b & 2) w[n++] = 2;
+    if (b & 1) w[n++] = 1;
+    return n;
+}
+
+static int slot_of(int side, int t, int i, int r) {
+    if (side == 0) return t * r + i;
+    int a = t / 16, c = (t / 4) % 4, e = t % 4;
+    return i * 64 + 16 * c + 4 * a + e;
+}
+
+/* codes[t*r+i] (t < n) -> stream of ceil(n/64) tiles (zero-filled by this function). */
+void oracle_pack(const uint8_t *codes, int n, int r, int b, int side, uint8_t *out) {
+    int w[3];
+    int np = n_planes(b, w);
+    int n_tiles = (n + 63) / 64;
+    int64_t tb = 8LL * r * b;
+    memset(out, 0, (size_t)(n_tiles * tb));
+    for (int tile = 0; tile < n_tiles; ++tile) {
+        uint8_t *base = out + tile * tb;
+        int64_t plane_off = 0;
+        for (int k = 0; k < np; ++k) {
+            int p = w[k];
+            int sh = 0;
+            for (int k2 = k + 1; k2 < np; ++k2) sh += w[k2];
+            int per_word = 32 / p;
+            for (int t = 0; t < 64; ++t) {
+                int tok = tile * 64 + t;
+                if (tok >= n) continue;
+                for (int i = 0; i < r; ++i) {
+                    uint32_t v = (codes[(int64_t)tok * r + i] >> sh) & ((1u << p) - 1);
+                    int phi = slot_of(side, t, i, r);
+                    int word = phi / per_word, iota = phi % per_word;
+                    int bit = 8 * (iota % 4) + p * (iota / 4);
+                    uint8_t *wp = base + plane_off + 4 * word;
+                    uint32_t cur = (uint32_t)wp[0] | ((uint32_t)wp[1] << 8) | ((uint32_t)wp[2] << 16) | ((uint32_t)wp[3] << 24);
+                    cur |= v << bit;
+                    wp[0] = cur & 255; wp[1] = (cur >> 8) & 255; wp[2] = (cur >> 16) & 255; wp[3] = cur >> 24;
+                }
+            }
+            plane_off += 8LL * r * p;
+        }
+    }
+}
+
+/* stream -> codes[t*r+i] for tokens t < n. */
+void oracle_unpack(const uint8_t *stream, int n, int r, int b, int side, uint8_t *codes) {
+    int w[3];
+    int np = n_planes(b, w);
+    int64_t tb = 8LL * r * b;
+    for (int tok = 0; tok < n; ++tok) {
+        int tile = tok / 64, t = tok % 64;
+        const uint8_t *base = stream + tile * tb;
+        for (int i = 0; i < r; ++i) {
+            uint32_t c = 0;
+            int64_t plane_off = 0;
+            for (int k = 0; k < np; ++k) {
+                int p = w[k];
+                int sh = 0;
+                for (int k2 = k + 1; k2 < np; ++k2) sh += w[k2];
+                int per_word = 32 / p;
+                int phi = slot_of(side, t, i, r);
+                int word = phi / per_word, iota = phi % per_word;
+                int bit = 8 * (iota % 4) + p * (iota / 4);
+                const uint8_t *wp = base + plane_off + 4 * word;
+                uint32_t cur = (uint32_t)wp[0] | ((uint32_t)wp[1] << 8) | ((uint32_t)wp[2] << 16) | ((uint32_t)wp[3] << 24);
+                c |= ((cur >> bit) & ((1u << p) - 1)) << sh;
+                plane_off += 8LL * r * p;
+            }
+            codes[(int64_t)tok * r + i] = (uint8_t)c;
+        }
+    }
+}

@@ -1,0 +1,230 @@
+"""Pins of the oracle's exact encode, packed layout, reconstruction and decode
+attention (CPU only): exact rational arithmetic, hand-derived bit positions,
+round trips, Lemma lem:head-dist and dense softmax attention."""
+import math
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+from oracle import attention as oatt
+from oracle import basis as ob
+from oracle import layout as ol
+from oracle import native as onat
+from oracle import quant as oq
+
+
+def half_fraction(bits: int) -> Fraction:
+    return Fraction(float(np.array([bits], dtype=np.uint16).view(np.float16)[0]))
+
+
+def encode_fraction(P_bits, step, b, x_bits):
+    r, d = P_bits.shape
+    out = np.zeros((x_bits.shape[0], r), dtype=np.uint8)
+    st = Fraction(float(np.float32(step)))
+    for t in range(x_bits.shape[0]):
+        xs = [half_fraction(int(v)) for v in x_bits[t]]
+        for i in range(r):
+            y = sum(half_fraction(int(P_bits[i, j])) * xs[j] for j in range(d))
+            out[t, i] = oq.code_exact(y, st, b)
+    return out
+
+
+def rand_half_bits(rng, shape, scale=1.0, subnormal_frac=0.05):
+    v = (rng.standard_normal(shape) * scale).astype(np.float16).view(np.uint16)
+    mask = rng.uniform(size=shape) < subnormal_frac
+    v[mask] = rng.integers(0, 1024, size=mask.sum()) | (rng.integers(0, 2, size=mask.sum()) << 15)
+    return v
+
+
+@pytest.mark.parametrize("b", [1, 2, 3, 5, 8])
+def test_c_exact_encode_matches_rationals(b):
+    rng = np.random.default_rng(b)
+    r, d = 6, 16
+    P = rand_half_bits(rng, (r, d), 0.3)
+    x = rand_half_bits(rng, (20, d), 2.0)
+    step = np.float32(0.37 / (1 << (b - 1)))
+    assert np.array_equal(onat.encode_codes(P, step, b, x), encode_fraction(P, step, b, x))
+
+
+def test_c_exact_encode_on_exact_thresholds():
+    # y lands exactly on multiples of the step: codes must follow floor exactly
+    d, b = 8, 4
+    P = np.zeros((2, d), dtype=np.float16)
+    P[0, 0] = 1.0
+    P[1, :2] = [0.5, -0.25]
+    step = np.float32(0.125)
+    xs = []
+    for j in range(-9, 10):
+        x = np.zeros(d, dtype=np.float16)
+        x[0] = np.float16(j * 0.125)
+        x[1] = np.float16(j * 0.25 * 0.5)
+        xs.append(x)
+    x = np.stack(xs)
+    got = onat.encode_codes(P.view(np.uint16), step, b, x.view(np.uint16))
+    exp = encode_fraction(P.view(np.uint16), step, b, x.view(np.uint16))
+    assert np.array_equal(got, exp)
+    # hand check: y0 = j/8 exactly -> floor = j -> code j + 8 clamped to [0, 15]
+    assert list(got[:, 0]) == [max(0, min(15, j + 8)) for j in range(-9, 10)]
+
+
+def test_layout_hand_derived_bit_positions():
+    # K side, r = 2, b = 1: slot(t=0, i=1) = 1 -> word 0, bit 8 * 1 + 1 * 0 = 8
+    c = np.zeros((64, 2), dtype=np.uint8)
+    c[0, 1] = 1
+    s = onat.pack(c, 2, 1, ol.SIDE_K)
+    assert s.size == 16 and list(np.nonzero(s)[0]) == [1] and s[1] == 1
+    # K side, r = 2, b = 1: slot(t=2, i=0) = 4 -> iota 4 -> bit 8 * 0 + 1 * 1 = 1
+    c[:] = 0
+    c[2, 0] = 1
+    s = onat.pack(c, 2, 1, ol.SIDE_K)
+    assert list(np.nonzero(s)[0]) == [0] and s[0] == 2
+    # V side, r = 2, b = 1: coord 1, token 0 -> slot 64 -> word 2, bit 0 -> byte 8
+    c[:] = 0
+    c[0, 1] = 1
+    s = onat.pack(c, 2, 1, ol.SIDE_V)
+    assert list(np.nonzero(s)[0]) == [8] and s[8] == 1
+    # V side: token 5 = 16*0 + 4*1 + 1 -> psi = 16*1 + 4*0 + 1 = 17 -> iota 17 -> bit 8*1 + 4 = 12 -> byte 1, bit 4
+    c[:] = 0
+    c[5, 0] = 1
+    s = onat.pack(c, 2, 1, ol.SIDE_V)
+    assert list(np.nonzero(s)[0]) == [1] and s[1] == 16
+    # b = 8 on the K side is plain bytes in token-major order
+    c = np.arange(64 * 2, dtype=np.uint8).reshape(64, 2)
+    s = onat.pack(c, 2, 8, ol.SIDE_K)
+    assert np.array_equal(s, np.arange(128, dtype=np.uint8))
+    # b = 3 = planes (2, 1): the 2-bit plane holds the high bits, then the 1-bit plane
+    c = np.zeros((64, 2), dtype=np.uint8)
+    c[0, 0] = 0b110
+    s = onat.pack(c, 2, 3, ol.SIDE_K)
+    assert s.size == 48 and s[0] == 0b11 and np.count_nonzero(s) == 1
+
+
+@pytest.mark.parametrize("side", [ol.SIDE_K, ol.SIDE_V])
+@pytest.mark.parametrize("b", range(1, 9))
+def test_pack_c_matches_python_and_round_trips(side, b):
+    rng = np.random.default_rng(10 * b + side)
+    for r, n in [(2, 64), (6, 70), (16, 5), (50, 130)]:
+        codes = rng.integers(0, 1 << b, size=(n, r)).astype(np.uint8)
+        s = onat.pack(codes, r, b, side)
+        assert s.size == ol.stream_bytes(n, r, b) == ((n + 63) // 64) * 8 * r * b
+        assert bytes(s) == ol.pack(codes.tolist(), r, b, side)
+        assert np.array_equal(onat.unpack(s, n, r, b, side), codes)
+        assert np.array_equal(np.array(ol.unpack(bytes(s), n, r, b, side), dtype=np.uint8), codes)
+
+
+def test_storage_is_exactly_rb_over_d_bits_per_dimension():
+    # Appendix G: r*b/d bits per dimension, no per-token metadata (whole tiles)
+    for r in (2, 16, 100, 128):
+        for b in range(1, 9):
+            n = 64 * 7
+            assert ol.stream_bytes(n, r, b) * 8 / (n * 128) == r * b / 128
+
+
+def _head(rng, d=128, alpha=1.2):
+    Q, R = np.linalg.qr(rng.standard_normal((d, d)))
+    Q = Q * np.sign(np.diag(R))
+    lam = np.arange(1, d + 1, dtype=np.float64) ** (-alpha)
+    return Q, lam
+
+
+def test_orthogonal_decomposition_per_token():
+    # Lemma lem:head-dist step 1: ||x - x_hat||^2 = ||xi_1||^2 + ||xi_2||^2, deterministically
+    rng = np.random.default_rng(21)
+    U, lam = _head(rng)
+    r, b = 40, 3
+    sign = rng.integers(0, 2, 128) * 2 - 1
+    Pbits, step = ob.make_basis(U, np.arange(128), lam, r, b, sign)
+    x = ((rng.standard_normal((50, 128)) * np.sqrt(lam)) @ U.T).astype(np.float16)
+    codes = onat.encode_codes(Pbits, step, b, x.view(np.uint16))
+    xh = oatt.reconstruct(codes, Pbits, step, b)
+    P = oatt.fp16_to_f64(Pbits)
+    xf = x.astype(np.float64)
+    # with the fp16-rounded basis the projector is P^T P (rows not exactly orthonormal): use its range
+    Q, _ = np.linalg.qr(P.T)
+    xi1 = xf - (Q @ (Q.T @ xf.T)).T
+    xi2 = (xf - xh) - xi1
+    tot = np.sum((xf - xh) ** 2, axis=1)
+    assert np.allclose(tot, np.sum(xi1 ** 2, axis=1) + np.sum(xi2 ** 2, axis=1), rtol=1e-10)
+
+
+@pytest.mark.parametrize("r,b", [(32, 3), (64, 4), (128, 5), (96, 6)])
+def test_head_distortion_matches_lemma_with_actual_quantizer(r, b):
+    # Lemma lem:head-dist: E||x - x_hat||^2 = sum_{i>r} lam + sum_i E[eps_i^2]; after the rotation every
+    # channel is ~N(0, sigma_bar^2) so E[eps_i^2] = sigma_bar^2 * mse(delta_b) (Gaussian closed form)
+    rng = np.random.default_rng(r + b)
+    U, lam = _head(rng, alpha=1.0)
+    sign = rng.integers(0, 2, 128) * 2 - 1
+    Pbits, step = ob.make_basis(U, np.arange(128), lam, r, b, sign)
+    n = 4000
+    x = ((rng.standard_normal((n, 128)) * np.sqrt(lam)) @ U.T).astype(np.float16)
+    codes = onat.encode_codes(Pbits, step, b, x.view(np.uint16))
+    err = np.mean(np.sum((x.astype(np.float64) - oatt.reconstruct(codes, Pbits, step, b)) ** 2, axis=1))
+    sigma2 = lam[:r].mean()
+    model = lam[r:].sum() + r * sigma2 * oq.gaussian_midrise_mse(oq.delta_b(b), b)
+    assert abs(err - model) < 0.08 * model, (err, model)
+
+
+def test_full_rank_high_bits_reconstructs_within_step():
+    rng = np.random.default_rng(5)
+    U, lam = _head(rng, alpha=0.6)
+    sign = rng.integers(0, 2, 128) * 2 - 1
+    Pbits, step = ob.make_basis(U, np.arange(128), lam, 128, 8, sign)
+    x = ((rng.standard_normal((200, 128)) * np.sqrt(lam)) @ U.T).astype(np.float16)
+    codes = onat.encode_codes(Pbits, step, 8, x.view(np.uint16))
+    y = x.astype(np.float64) @ oatt.fp16_to_f64(Pbits).T
+    zh = oatt.dequantize(codes, step, 8)
+    inside = np.abs(y) < 127 * float(step)
+    assert np.all(np.abs(y - zh)[inside] <= float(step) / 2 * (1 + 1e-12))
+    xh = oatt.reconstruct(codes, Pbits, step, 8)
+    # sqrt(d) * step / 2 from quantisation plus the fp16 rounding of the basis
+    bound = math.sqrt(128) * float(step) / 2 + 2e-3 * np.linalg.norm(x.astype(np.float64), axis=1)
+    ok = np.all(inside, axis=1)            # tokens with no clipped coordinate
+    assert ok.sum() > 150
+    assert np.all((np.linalg.norm(x.astype(np.float64) - xh, axis=1) <= bound)[ok])
+
+
+def test_brute_force_attention_closed_forms():
+    rng = np.random.default_rng(1)
+    V = rng.standard_normal((7, 16))
+    K = rng.standard_normal((7, 16))
+    assert np.allclose(oatt.brute_force_attention(np.zeros((1, 16)), K, V), V.mean(axis=0))
+    assert np.allclose(oatt.brute_force_attention(rng.standard_normal((2, 16)), K[:1], V[:1]), V[:1])
+    q = np.zeros((1, 16))
+    q[0, 3] = 1e4
+    K2 = np.zeros((7, 16))
+    K2[4, 3] = 1.0
+    assert np.allclose(oatt.brute_force_attention(q, K2, V), V[4])
+
+
+def test_rank_space_attention_equals_dense_on_identity_basis():
+    # codes -> z_hat with P = I and every value representable: equals softmax(q K^T / sqrt(d)) V
+    rng = np.random.default_rng(3)
+    d, T, b = 128, 300, 8
+    step = np.float32(0.0625)
+    ck = rng.integers(0, 256, (T, d)).astype(np.uint8)
+    cv = rng.integers(0, 256, (T, d)).astype(np.uint8)
+    I = np.eye(d, dtype=np.float16).view(np.uint16)
+    q = (rng.standard_normal((4, d)) * 0.5).astype(np.float16)
+    out = oatt.decode_attention(ck, cv, I, I, step, step, b, b, q.view(np.uint16), T)
+    K = oatt.dequantize(ck, step, b)
+    V = oatt.dequantize(cv, step, b)
+    ref = oatt.brute_force_attention(q.astype(np.float64), K, V)
+    assert np.allclose(out, ref, rtol=1e-12, atol=1e-13)
+
+
+def test_rank_space_attention_equals_dense_on_reconstruction():
+    rng = np.random.default_rng(4)
+    U, lam = _head(rng)
+    sk = rng.integers(0, 2, 128) * 2 - 1
+    Pk, stk = ob.make_basis(U, np.arange(128), lam, 48, 3, sk)
+    Pv, stv = ob.make_basis(U, np.arange(128), lam, 100, 2, sk)
+    T = 500
+    ck = rng.integers(0, 8, (T, 48)).astype(np.uint8)
+    cv = rng.integers(0, 4, (T, 100)).astype(np.uint8)
+    q = (rng.standard_normal((4, 128)) * 3).astype(np.float16)
+    out = oatt.decode_attention(ck, cv, Pk, Pv, stk, stv, 3, 2, q.view(np.uint16), 321)
+    Kh = oatt.reconstruct(ck, Pk, stk, 3)[:321]
+    Vh = oatt.reconstruct(cv, Pv, stv, 2)[:321]
+    ref = oatt.brute_force_attention(q.astype(np.float64), Kh, Vh)
+    assert np.allclose(out, ref, rtol=1e-10, atol=1e-12)
