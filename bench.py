@@ -1,0 +1,244 @@
+#!/usr/bin/env python3
+"""Benchmark of the KV-COBRA hot path on one MI355X.
+
+Workload (default): Llama-3-8B-shaped compressed cache, 32 layers x 8 KV heads
+x batch 8, 32 768 cached tokens per sequence, 4 query heads per KV head,
+head_dim 128, joint K+V at 2 bits per dimension (K: attention-KL weights with
+C1 + C2; V: MSE weights, C1 only), synthetic power-law KV.
+
+A step is one serving decode step: append the new token's K and V to every
+unit's compressed stream (encode) and run decode attention over all 32 769
+tokens of every unit. `value` is the step's algorithmic HBM bytes divided by
+the step time. Separately timed: the bulk prefill encode of the whole cache
+(encode tokens/s), and the decode-attention call alone (roofline entry).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "decode-attn HBM GB/s + encode tokens/s, 8B-shape KV @32k ctx, 2 bpd"
+HBM_PEAK_GBS = 8000.0
+
+
+def log(msg):
+    print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
+
+
+def decode_alg_bytes(cache, n_tok: int) -> int:
+    """Code bytes actually needed (r*b/8 per token), bases once per (layer, head, side), q and out."""
+    w = cache.w
+    K, V = cache.K, cache.V
+    per_tok = int(np.sum(K.r_h.astype(np.int64) * K.b_h + V.r_h.astype(np.int64) * V.b_h))  # bits per token
+    codes = per_tok * n_tok // 8
+    basis = sum(p.size * 2 for p in cache.k_tab.P) + sum(p.size * 2 for p in cache.v_tab.P)
+    qo = w.n_units * w.group * w.d * (2 + 4)
+    return codes + basis + qo
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in ("kvc_kernels.hip", "kvc_device.h"):
+        with open(os.path.join(ROOT, "paper_2609_24298_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(per_launch_alg: int):
+    """HBM bytes per decode call from the committed rocprofv3 counter summary, if it is current."""
+    path = os.path.join(ROOT, "profiles", "decode_attn_llama8b_b8_t32k_2bpd_traffic.json")
+    try:
+        with open(path) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel_source_sha") != kernel_source_hash():
+        return None
+    return t.get("hbm_bytes_per_call")
+
+
+def cpu_baseline(w, stats, seed: int, units, n_tok: int):
+    """The oracle, untuned, on a bounded sample: its own tables, bases and exact codes for `units`,
+    then its fp64 decode attention timed over those units."""
+    import torch
+    from threadpoolctl import threadpool_info
+
+    from oracle import alloc as oa
+    from oracle import attention as oatt
+    from oracle import basis as ob
+    from oracle import native as onat
+    from paper_2609_24298_amd import kvc, pipeline
+
+    lam_k = np.stack([s.lam_k for s in stats])
+    sq = np.stack([s.sigma2_q for s in stats])
+    lam_v = np.stack([s.lam_v for s in stats])
+    ak = oa.allocate(lam_k, sq, oa.AllocOpts(bpd=w.bpd))
+    av = oa.allocate(lam_v, None, oa.AllocOpts(bpd=w.bpd, solver=oa.SOLVER_C1_ONLY))
+    prepared = []
+    code_bytes = 0
+    t_enc = 0.0
+    n_vec = 0
+    for u in units:
+        h = w.head_of_unit(u)
+        s = stats[h]
+        rk, bk, rv, bv = int(ak["r"][h]), int(ak["b"][h]), int(av["r"][h]), int(av["b"][h])
+        Pk, dk = ob.make_basis(s.U_k, ak["order"][h], s.lam_k, rk, bk, s.sign_k)
+        Pv, dv = ob.make_basis(s.U_v, av["order"][h], s.lam_v, rv, bv, s.sign_v)
+        xk = pipeline.draw_unit_tokens(w, stats, kvc.SIDE_K, n_tok, seed, "cuda", units=[u])[0]
+        xv = pipeline.draw_unit_tokens(w, stats, kvc.SIDE_V, n_tok, seed, "cuda", units=[u])[0]
+        xkb = xk.view(torch.int16).cpu().numpy().view(np.uint16)
+        xvb = xv.view(torch.int16).cpu().numpy().view(np.uint16)
+        t = time.perf_counter()
+        ck = onat.encode_codes(Pk, dk, bk, xkb)
+        cv = onat.encode_codes(Pv, dv, bv, xvb)
+        t_enc += time.perf_counter() - t
+        n_vec += 2 * n_tok
+        sk = onat.pack(ck, rk, bk, kvc.SIDE_K)
+        sv = onat.pack(cv, rv, bv, kvc.SIDE_V)
+        q = pipeline.draw_queries(w, stats, seed + 1, "cpu")[u].view(torch.int16).numpy().view(np.uint16)
+        prepared.append((sk, sv, rk, bk, rv, bv, Pk, Pv, dk, dv, q))
+        code_bytes += (rk * bk + rv * bv) * n_tok // 8
+    reps = 0
+    t0 = time.perf_counter()
+    while True:
+        for sk, sv, rk, bk, rv, bv, Pk, Pv, dk, dv, q in prepared:
+            ck = onat.unpack(sk, n_tok, rk, bk, kvc.SIDE_K)
+            cv = onat.unpack(sv, n_tok, rv, bv, kvc.SIDE_V)
+            oatt.decode_attention(ck, cv, Pk, Pv, dk, dv, bk, bv, q, n_tok)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el > 8.0 or reps >= 50:
+            break
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    return {
+        "value": round(code_bytes * reps / el / 1e9, 4), "unit": "GB/s", "cores": int(threads), "kind": "oracle",
+        "sample": f"{len(units)} units x {n_tok} tokens of the workload, fp64 decode from packed codes, "
+                  f"{reps} reps in {el:.1f} s; exact encode of the same sample {n_vec / t_enc:.0f} vectors/s",
+        "encode_vectors_per_s": round(n_vec / t_enc, 1),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="llama8b_b8_t32k_2bpd")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on exactly one GPU (asked for {args.gpus}); the multi-GPU path is not part of "
+              "this build", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2609_24298_amd import kvc, pipeline, synth
+
+    w = synth.WORKLOADS[args.workload]
+    T = w.tokens
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    log(f"workload {w}")
+    t_setup = time.perf_counter()
+    cache = pipeline.Cache(w, seed=args.seed, device=dev, capacity=T + kvc.TILE)
+    log(f"tables + bases in {time.perf_counter() - t_setup:.1f} s; "
+        f"K (r,b) spread {len(set(zip(cache.k_tab.r.tolist(), cache.k_tab.b.tolist())))} pairs")
+
+    # ---- bulk prefill encode of the whole cache
+    xk = pipeline.draw_unit_tokens(w, cache.stats, kvc.SIDE_K, T, args.seed, dev)
+    xv = pipeline.draw_unit_tokens(w, cache.stats, kvc.SIDE_V, T, args.seed, dev)
+    torch.cuda.synchronize()
+    log(f"drew {2 * w.n_units * T} fp16 vectors")
+    enc_times = []
+    for rep in range(2):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        cache.encode(xk, xv, 0, T)
+        e1.record()
+        torch.cuda.synchronize()
+        enc_times.append(e0.elapsed_time(e1) / 1e3)
+        log(f"bulk encode rep {rep}: {enc_times[-1] * 1e3:.2f} ms")
+    t_enc = min(enc_times)
+    enc_vectors = 2 * w.n_units * T
+    enc_read = enc_vectors * w.d * 2
+    del xk, xv
+    torch.cuda.empty_cache()
+
+    # ---- decode step: append one token per unit, attend over T + 1 tokens
+    xk1 = pipeline.draw_unit_tokens(w, cache.stats, kvc.SIDE_K, 1, args.seed + 100, dev)
+    xv1 = pipeline.draw_unit_tokens(w, cache.stats, kvc.SIDE_V, 1, args.seed + 100, dev)
+    q = pipeline.draw_queries(w, cache.stats, args.seed + 1, dev)
+    n_att = T + 1
+    seq = torch.full((w.n_units,), n_att, dtype=torch.int32, device=dev)
+    ws, out = cache.decode_buffers(n_att)
+
+    def step():
+        cache.encode(xk1, xv1, T, 1)
+        cache.decode(q, seq, n_att, out, ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s0.record()
+    for _ in range(args.steps):
+        step()
+    s1.record()
+    torch.cuda.synchronize()
+    ms_step = s0.elapsed_time(s1) / args.steps
+    log(f"{args.steps} steps: {ms_step:.3f} ms/step")
+
+    # decode call alone, events on the launch stream, for the roofline entry
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    for a, b in evs:
+        a.record()
+        cache.decode(q, seq, n_att, out, ws)
+        b.record()
+    torch.cuda.synchronize()
+    t_dec = float(np.mean([a.elapsed_time(b) for a, b in evs])) / 1e3
+    assert torch.isfinite(out).all().item()
+
+    dec_bytes = decode_alg_bytes(cache, n_att)
+    # append: read the new token's fp16 K and V, write r*b bits per unit and side
+    append_bytes = 2 * w.n_units * w.d * 2 + int(np.sum(cache.K.r_h.astype(np.int64) * cache.K.b_h
+                                                        + cache.V.r_h.astype(np.int64) * cache.V.b_h)) // 8
+    step_bytes = dec_bytes + append_bytes
+    value = step_bytes / (ms_step / 1e3) / 1e9
+    achieved = dec_bytes / t_dec / 1e9
+    log(f"decode call {t_dec * 1e3:.3f} ms, {achieved:.1f} GB/s algorithmic ({dec_bytes / 1e9:.3f} GB)")
+
+    res = {
+        "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": w.name, "layers": w.layers, "kv_heads": w.kv_heads, "q_per_kv": w.group,
+                   "batch": w.batch, "context": T, "bpd_per_side": w.bpd, "head_dim": w.d},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(dec_bytes),
+                     "kernel": "kvc_decode_attn (qproj + decode_partial + combine)",
+                     "alg_bytes_per_launch": dec_bytes, "avg_launch_ms": round(t_dec * 1e3, 4)},
+        "encode": {"vectors_per_s": round(enc_vectors / t_enc, 1), "model_tokens_per_s": round(w.batch * T / t_enc, 1),
+                   "ms": round(t_enc * 1e3, 3), "hbm_read_GBs": round(enc_read / t_enc / 1e9, 2)},
+    }
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle) ...")
+        try:
+            res["cpu_baseline"] = cpu_baseline(w, cache.stats, args.seed, [0, w.n_units // 2 + 3], T)
+        except Exception as e:  # the baseline is context, never a reason to lose the GPU line
+            res["cpu_baseline"] = {"error": repr(e)}
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

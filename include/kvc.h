@@ -1,0 +1,233 @@
+/*
+ * kvc.h - C ABI of the KV-COBRA hot path on AMD Instinct MI355X (gfx950).
+ *
+ * KV-COBRA compresses each attention head's keys and values by projecting
+ * them onto a per-head truncated eigenbasis with a folded Walsh-Hadamard
+ * rotation, quantizing the r retained coordinates to b bits and bit-packing
+ * them; the per-head (r, b) comes from a rate-distortion allocator. Decode
+ * attention reads the packed codes directly.
+ *
+ * Conventions for every entry point
+ *  - Return value: KVC_OK (0) or a positive KVC_E* code; on error a message is
+ *    available from kvc_last_error() (thread-local), and no output has been
+ *    written by a kernel (validation happens on the host before any launch).
+ *  - "device" pointers are HIP device memory (e.g. torch tensors on cuda:0);
+ *    "host" pointers are ordinary CPU memory. The library never allocates,
+ *    frees or keeps any caller array; the caller owns every buffer.
+ *  - Asynchronous calls enqueue kernels on `stream` (a hipStream_t; NULL is
+ *    the null stream) and return without synchronising. Faults inside a
+ *    kernel surface at the caller's next synchronisation.
+ *  - d (head dimension) is 128; r is even in [2, d]; b is in [1, 8].
+ *  - Every floating-point input must be finite.
+ *
+ * Packed code stream of one (unit, side), defined by this library (the
+ * paper fixes only its size: exactly r*b bits per token, no metadata):
+ *  - tiles of 64 tokens, tile t at byte code_off + t * 8*r*b;
+ *  - a b-bit code is split into planes (b = 8: one 8-bit plane; otherwise the
+ *    binary expansion of b, widest first, widest = most significant bits);
+ *    the plane of width p is 8*r*p bytes = 2*r*p little-endian 32-bit words,
+ *    planes in that order;
+ *  - slot phi of a plane lies in word phi / (32/p) at bit
+ *    8*(iota % 4) + p*(iota / 4), iota = phi % (32/p);
+ *  - slot of (token t in the tile, coordinate i):
+ *      K side: phi = t*r + i;
+ *      V side: phi = i*64 + psi(t), psi(16a + 4c + e) = 16c + 4a + e;
+ *  - kvc_encode writes only the slots of the tokens it encodes; slots of
+ *    tokens never encoded keep the arena's contents (zero if the caller
+ *    zeroed the arena, which the reference packing assumes).
+ */
+#ifndef KVC_H
+#define KVC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define KVC_OK 0
+#define KVC_EINVAL 1        /* null pointer, bad size, inconsistent arguments */
+#define KVC_EUNSUPPORTED 2  /* odd r, r > d, b outside 1..8, d != 128, step out of range */
+#define KVC_ENOSPACE 3      /* token range beyond capacity, arena or workspace too small */
+#define KVC_EDEVICE 4       /* a HIP runtime call failed */
+
+#define KVC_SIDE_K 0
+#define KVC_SIDE_V 1
+
+#define KVC_SOLVER_DAMPED 0   /* C1 + damped C2 (the paper's default) */
+#define KVC_SOLVER_DP 1       /* C1 + exact integer DP over per-head budgets */
+#define KVC_SOLVER_C1_ONLY 2  /* C1 at the uniform budget bpd*d (V side; "w/o C2" ablation) */
+
+#define KVC_TILE_TOKENS 64
+#define KVC_HEAD_DIM 128
+
+/* Allocator options (Sections 3.2-3.3; Appendices B-D, F). */
+typedef struct kvc_alloc_opts {
+    int32_t d;        /* head dimension (128) */
+    int32_t r_min;    /* smallest rank on the grid (2) */
+    int32_t r_step;   /* rank grid step (2) */
+    int32_t b_min;    /* smallest bit width (1) */
+    int32_t b_max;    /* largest bit width (8) */
+    int32_t solver;   /* KVC_SOLVER_* */
+    int32_t rounds;   /* C2 rounds (5) */
+    int32_t reorder;  /* 1: sort directions by weight, descending (stable) */
+    double bpd;       /* target bits per dimension of this side */
+    double eta;       /* C2 damping (0.3) */
+    double B_min;     /* per-head budget floor in bits (r_min * b_min) */
+    double B_max;     /* per-head budget cap for the DP (d * b_max) */
+} kvc_alloc_opts;
+
+/* Per-head result of the allocator. */
+typedef struct kvc_head_alloc {
+    int32_t r;   /* retained rank */
+    int32_t b;   /* bits per retained coordinate */
+    double B;    /* final per-head budget in bits (real for C2, integer for DP) */
+    double D;    /* modelled distortion D(r, b) */
+} kvc_head_alloc;
+
+/* One side (K or V) of a compressed cache: n_units streams plus their bases.
+ * A unit is one (layer, sequence, KV head). Units may share a basis. */
+typedef struct kvc_stream_desc {
+    int32_t n_units;
+    int32_t d;              /* 128 */
+    int32_t capacity;       /* tokens each unit's stream can hold */
+    int32_t side;           /* KVC_SIDE_K or KVC_SIDE_V */
+    /* host mirrors, used for validation and launch planning */
+    const int32_t* r_host;         /* [n_units] */
+    const int32_t* b_host;         /* [n_units] */
+    const int64_t* code_off_host;  /* [n_units] byte offset of the stream, multiple of 16 */
+    const int64_t* basis_off_host; /* [n_units] element offset of the unit's basis */
+    const float* delta_host;       /* [n_units] quantizer step, in [2^-24, 2^24] */
+    /* device copies of the same tables */
+    const int32_t* r;
+    const int32_t* b;
+    const int64_t* code_off;
+    const int64_t* basis_off;      /* [n_units] element offset of the unit's r x d fp16 basis */
+    const float* delta;
+    /* device arenas */
+    uint8_t* codes;                /* code arena */
+    int64_t codes_bytes;           /* its size */
+    const uint16_t* basis;         /* fp16 basis arena */
+    int64_t basis_elems;           /* its size in elements */
+} kvc_stream_desc;
+
+/* Defaults listed above with the given bits per dimension. Host only. */
+int kvc_alloc_opts_default(kvc_alloc_opts* o, double bpd);
+
+/*
+ * kvc_allocate - per-head rank and bit width under a total bit budget.
+ * Paper: global problem Eq. (eq:global); table steps 2-4; C1 Section 3.2 and
+ * Appendix B; C2 damped update Eq. (eq:c2-update), Appendix C; exact DP
+ * Appendix D; V side C1 only, Appendix F.
+ *
+ *  lambda     host, [n_heads][d]: eigenvalues of each head's covariance in
+ *             descending order (eigen index order).
+ *  sigma2_q   host, [n_heads][d] or NULL: query variance along each
+ *             eigendirection. Non-NULL selects the attention-KL weights
+ *             w = sigma2_q * lambda (Proposition prop:kl-bound); NULL selects
+ *             the MSE weights w = lambda.
+ *  out        host, [n_heads]: result per head.
+ *  order      host, [n_heads][d] or NULL: importance order (eigen indices
+ *             sorted by w descending, ties in eigen order; identity when
+ *             o->reorder == 0). The first r entries are the retained directions.
+ * Budget B_tot = bpd * n_heads * d. fp64 throughout, deterministic; C1 ties
+ * keep the smallest r; an infeasible budget (below r_min*b_min) yields
+ * (r_min, b_min). Synchronous, host only, reentrant.
+ */
+int kvc_allocate(const double* lambda, const double* sigma2_q, int32_t n_heads,
+                 const kvc_alloc_opts* o, kvc_head_alloc* out, int32_t* order);
+
+/*
+ * kvc_make_basis - the stored per-head record: fused basis and quantizer step.
+ * Paper: Section 3.4 and table steps 5-6 (P = H_r diag(s) U_r^T), Appendix A.1
+ * (after the rotation every channel has the mean retained variance).
+ *
+ *  U        host, [d][d] row-major; column k is the eigenvector of eigen index k.
+ *  order    host, [>= r]: importance order; order[0..r) are the retained directions.
+ *  lambda   host, [d]: eigenvalues by eigen index (variances, not KL weights).
+ *  sign     host, [r]: +1/-1 per importance position (the random sign flip).
+ *  P        host out, [r][d]: fp16 bits of P = blockdiag(H_n/sqrt(n)) diag(sign) U_r^T.
+ *           H_n are Sylvester-Hadamard blocks over the binary expansion of r,
+ *           largest first; position i goes to the block with the largest
+ *           remaining quota (i+1)*n_j - r*count_j (ties: larger block). For
+ *           r = 2^k this is the r x r Walsh-Hadamard matrix of the paper.
+ *           Entries are accumulated in fp64 over block columns in order, scaled
+ *           by 1/sqrt(n) and rounded to nearest even fp16.
+ *  delta    host out: f32(sqrt(mean(lambda[order[0..r)])) * delta_b), delta_b the
+ *           MSE-optimal step of the 2^b-level uniform mid-rise quantizer of a
+ *           unit Gaussian, to four significant digits.
+ * Returns KVC_EUNSUPPORTED if the step falls outside [2^-24, 2^24].
+ */
+int kvc_make_basis(const double* U, const int32_t* order, const double* lambda, int32_t d,
+                   int32_t r, int32_t b, const int8_t* sign, uint16_t* P, float* delta);
+
+/*
+ * kvc_encode - compress tokens [t0, t0 + n_tok) of every unit into its stream.
+ * Paper: table step 7 (quantize(P k_t, b): projection and rotation in one
+ * multiply), step 8 (cache the codes).
+ *
+ *  x            device fp16 [n_units][...]: unit u's tokens start at
+ *               x + u * x_unit_stride elements, n_tok rows of d.
+ *  Code of coordinate i: k = clamp(floor(y_i / delta) + 2^(b-1), 0, 2^b - 1)
+ *  with y_i = sum_j P_ij x_j taken exactly (the GPU computes y in fp32 with a
+ *  rigorous error bound and settles every undecided element with exact
+ *  integer arithmetic), so the stream is bit-identical to the definition.
+ *  Codes of tokens of the same tiles outside [t0, t0 + n_tok) are preserved
+ *  (read-modify-write of the partial tiles), so a cache grows by appending.
+ *  Requires t0 >= 0, n_tok >= 0, t0 + n_tok <= capacity; x must be 16-byte
+ *  aligned and x_unit_stride a multiple of 8 elements, >= n_tok * d.
+ *  Async on `stream`. Calls on one stream are ordered; concurrent calls that
+ *  touch the same tiles race.
+ */
+int kvc_encode(const kvc_stream_desc* s, const uint16_t* x, int64_t x_unit_stride,
+               int32_t t0, int32_t n_tok, void* stream);
+
+/*
+ * kvc_decode_attn - one decode step of attention over the compressed cache.
+ * Paper: table step 8 (dequantize on read); Section 4 (logits <q,k>/sqrt(d),
+ * softmax); Appendix H "Wall-clock at the primitive level" (dequantize and
+ * undo the rotation in one fused pass).
+ *
+ *  k, v         descriptors of the K and V sides; same n_units, unit u pairs.
+ *  q            device fp16 [n_units][G][d]: the G query heads sharing unit
+ *               u's KV head.
+ *  seq_len      device int32 [n_units]: tokens attended per unit (each in
+ *               [1, max_seq_len]).
+ *  max_seq_len  host: upper bound of seq_len, <= both capacities.
+ *  out          device f32 [n_units][G][d]:
+ *               out[u][g] = P_V^T sum_t p_t z_V,t,
+ *               p = softmax_t((P_K q_g) . z_K,t / sqrt(d)),
+ *               z = (k - 2^(b-1) + 1/2) * delta (dequantized codes).
+ *  ws           device workspace of >= kvc_decode_attn_workspace(...) bytes,
+ *               256-byte aligned; contents on entry are ignored.
+ * Split over the context (flash-decoding): each (unit, chunk) writes a
+ * partial (max, sum, rank-space accumulator); a second kernel merges them and
+ * applies the V basis. No atomics: results are deterministic. Async.
+ */
+int kvc_decode_attn(const kvc_stream_desc* k, const kvc_stream_desc* v, const uint16_t* q,
+                    int32_t G, const int32_t* seq_len, int32_t max_seq_len, float* out,
+                    void* ws, size_t ws_bytes, void* stream);
+
+/* Workspace bytes kvc_decode_attn needs for these descriptors (host only). */
+size_t kvc_decode_attn_workspace(const kvc_stream_desc* k, const kvc_stream_desc* v,
+                                 int32_t G, int32_t max_seq_len);
+
+/*
+ * kvc_reconstruct - x_hat_t = P^T z_t for tokens [t0, t0 + n_tok) of every unit.
+ * Paper: Appendix A, Lemma lem:head-dist (x_hat = U_r H_r^T Q(H_r U_r^T x)).
+ *  out   device f32 [n_units][n_tok][d]. Async.
+ */
+int kvc_reconstruct(const kvc_stream_desc* s, int32_t t0, int32_t n_tok, float* out, void* stream);
+
+/* Message of the last failing call on this thread ("" if none). */
+const char* kvc_last_error(void);
+
+/* Library version, for the binding's load check. */
+int32_t kvc_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KVC_H */

@@ -101,20 +101,42 @@ def distortion(w, r: int, b: int) -> float:
     return tail_sum(w, r) + q_model(b) * head_sum(w, r)
 
 
+class HeadSums:
+    """All head sums S[r] and tail sums T[r] of one head, built with the same
+    additions, in the same order, as head_sum / tail_sum."""
+
+    def __init__(self, w):
+        d = len(w)
+        self.S = [0.0] * (d + 1)
+        self.T = [0.0] * (d + 1)
+        for k in range(d):
+            self.S[k + 1] = self.S[k] + float(w[k])
+        for k in range(d - 1, -1, -1):
+            self.T[k] = self.T[k + 1] + float(w[k])
+        self.d = d
+
+    def __len__(self):
+        return self.d
+
+    def distortion(self, r: int, b: int) -> float:
+        return self.T[r] + q_model(b) * self.S[r]
+
+
 def c1(w, B: float, o: AllocOpts):
-    """Per-head optimum (r, b, D) at real budget B."""
-    d = len(w)
+    """Per-head optimum (r, b, D) at real budget B (w: weights or their HeadSums)."""
+    hs = w if isinstance(w, HeadSums) else HeadSums(w)
+    d = len(hs)
     r_hi = min(d, math.floor(B / o.b_min))
     best = None
     r = o.r_min
     while r <= r_hi:
         b = min(o.b_max, math.floor(B / r))
-        D = distortion(w, r, b)
+        D = hs.distortion(r, b)
         if best is None or D < best[2]:
             best = (r, b, D)
         r += o.r_step
     if best is None:
-        best = (o.r_min, o.b_min, distortion(w, o.r_min, o.b_min))
+        best = (o.r_min, o.b_min, hs.distortion(o.r_min, o.b_min))
     return best
 
 
@@ -138,6 +160,7 @@ def c2_damped(W, o: AllocOpts):
     B_tot = o.bpd * float(N * d)
     B_bar = B_tot / N
     step = o.eta * B_bar
+    W = [HeadSums(w) for w in W]
     B = [o.bpd * float(d) for _ in range(N)]
     for _ in range(o.rounds):
         allocs = [c1(W[h], B[h], o) for h in range(N)]
@@ -164,6 +187,7 @@ def dp_exact(W, o: AllocOpts):
     cap = math.floor(B_tot)
     lo = math.ceil(o.bmin())
     hi = math.floor(o.bmax())
+    W = [HeadSums(w) for w in W]
     dstar = [[None] * (hi + 1) for _ in range(N)]
     for h in range(N):
         for beta in range(lo, hi + 1):
@@ -240,7 +264,7 @@ def allocate(lam, sigma2_q, o: AllocOpts):
         orders.append(order)
     if o.solver == SOLVER_C1_ONLY:
         B = [o.bpd * float(o.d) for _ in range(N)]
-        allocs = [c1(W[h], B[h], o) for h in range(N)]
+        allocs = [c1(HeadSums(W[h]), B[h], o) for h in range(N)]
     elif o.solver == SOLVER_DAMPED:
         B, allocs = c2_damped(W, o)
     elif o.solver == SOLVER_DP:

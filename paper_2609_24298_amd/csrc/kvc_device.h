@@ -1,0 +1,61 @@
+// Device-side helpers of libkvc shared by the HIP kernels: the packed-stream
+// layout (see include/kvc.h) and fp16 bit decoding. CDNA4 / gfx950 only.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace kvc {
+
+// Per-side tables passed to kernels by value.
+struct DevSide {
+    const int32_t* r;
+    const int32_t* b;
+    const int64_t* code_off;
+    const int64_t* basis_off;
+    const float* delta;
+    uint8_t* codes;
+    const uint16_t* basis;
+};
+
+// Slot of (token t in tile, coordinate i): token-major for K, coordinate-major
+// with the 4x4 (a, c) transpose of the token index for V.
+__device__ __forceinline__ int slot_k(int t, int i, int r) { return t * r + i; }
+__device__ __forceinline__ int psi(int t) { return (t & 0x03) | ((t & 0x0c) << 2) | ((t & 0x30) >> 2); }
+__device__ __forceinline__ int slot_v(int t, int i) { return i * 64 + psi(t); }
+
+// Code stored in slot phi of the tile starting at `tile` (planes widest first).
+__device__ __forceinline__ uint32_t load_code(const uint8_t* __restrict__ tile, int r, int b, int phi) {
+    if (b == 8) return tile[phi];
+    uint32_t c = 0;
+    int rem = b;
+    int off = 0;
+#pragma unroll
+    for (int p = 4; p >= 1; p >>= 1) {
+        if (b & p) {
+            const int per_word = 32 / p;
+            const int w = phi / per_word, iota = phi % per_word;
+            const int bit = 8 * (iota & 3) + p * (iota >> 2);
+            const uint32_t word = reinterpret_cast<const uint32_t*>(tile + off)[w];
+            rem -= p;
+            c |= ((word >> bit) & ((1u << p) - 1u)) << rem;
+            off += 8 * r * p;
+        }
+    }
+    return c;
+}
+
+// fp16 bits -> fp32 (exact).
+__device__ __forceinline__ float h2f(uint16_t h) { return (float)__builtin_bit_cast(_Float16, h); }
+
+// fp16 bits -> signed integer mantissa m and exponent e with value m * 2^e
+// (finite inputs; e in [-24, 5]).
+__device__ __forceinline__ void half_parts(uint16_t h, int32_t& m, int& e) {
+    const int ex = (h >> 10) & 31, fr = h & 1023;
+    if (ex == 0) { m = fr; e = -24; }
+    else { m = 1024 + fr; e = ex - 25; }
+    if (h & 0x8000) m = -m;
+}
+
+}  // namespace kvc

@@ -1,0 +1,492 @@
+// Device half of libkvc: HIP kernels for CDNA4 (gfx950) and their C-ABI
+// launchers (encode, reconstruct, decode attention).
+//
+// Kernels
+//  encode_kernel        one (unit, 64-token tile) per 256-thread block: the
+//                       fp16 basis is staged in LDS as fp32, each thread
+//                       projects one token onto a quarter of the coordinates
+//                       in fp32 with a rigorous error bound, undecided codes
+//                       are settled exactly in 128-bit integers, and the tile
+//                       is bit-packed from LDS with one thread per output word.
+//  reconstruct_kernel   x_hat = P^T z for a 64-token block of one unit.
+//  qproj_kernel         q~ = P_K q per unit and query head, pre-scaled by
+//                       step_K * log2(e) / sqrt(d) (rank-space logits).
+//  decode_partial_kernel  one (unit, context chunk) per wavefront: logits in
+//                       rank space from the K codes, online softmax, and the
+//                       probability-weighted sum of centred V codes.
+//  combine_kernel       merges the chunk partials of a unit and applies the
+//                       V step and basis: out = P_V^T (step_V (a / l + 1/2)).
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+
+#include "kvc_device.h"
+#include "kvc_internal.h"
+
+namespace kvc {
+
+constexpr int kD = KVC_HEAD_DIM;
+constexpr int kTile = KVC_TILE_TOKENS;
+constexpr int kMaxG = 16;
+constexpr int kPartStride = 132;  // floats per (item, query head): m, l, pad, pad, acc[128]
+
+// ---------------------------------------------------------------- encode
+
+// Exact code: y = sum_j P_ij x_j as an integer multiple of 2^-48 (|y| < 2^88),
+// k = clamp(floor(y / step) + 2^(b-1), 0, 2^b - 1) with floor division in
+// 128-bit integers. Used only for elements the fp32 path cannot decide.
+__device__ __noinline__ uint32_t exact_code(const uint16_t* __restrict__ Prow, const uint16_t* __restrict__ xrow,
+                                            float step, int b) {
+    __int128 N = 0;
+    for (int j = 0; j < kD; ++j) {
+        int32_t mp, mx;
+        int ep, ex;
+        half_parts(Prow[j], mp, ep);
+        half_parts(xrow[j], mx, ex);
+        N += (__int128)((int64_t)mp * mx) * ((__int128)1 << (ep + ex + 48));
+    }
+    const uint32_t u = __float_as_uint(step);
+    const int64_t m = 0x800000 | (u & 0x7fffff);
+    const int sD = (int)((u >> 23) & 255) - 150 + 48;  // >= 1 for step >= 2^-24
+    const __int128 D = (__int128)m << sD;
+    __int128 q = N / D;
+    if (N % D != 0 && N < 0) q -= 1;
+    const __int128 k = q + (1 << (b - 1));
+    const __int128 kmax = (1 << b) - 1;
+    return (uint32_t)(k < 0 ? 0 : (k > kmax ? kmax : k));
+}
+
+// Code from the fp32 projection `acc` whose error is at most `err`
+// (|acc - y| <= err). Falls back to exact_code when a quantizer threshold
+// j * step, j in [1 - 2^(b-1), 2^(b-1) - 1], is not clearly separated.
+__device__ __forceinline__ uint32_t decide_code(float acc, float err, float step, int b,
+                                                const uint16_t* Prow, const uint16_t* xrow) {
+    const int h = 1 << (b - 1);
+    const double st = step, yd = acc, ed = err;
+    const double t = yd / st;
+    bool amb = !(ed < 0.25 * st);
+    if (!amb) {
+        const double jn = rint(t);
+        if (jn >= 1 - h && jn <= h - 1) amb = !(fabs(yd - jn * st) > ed + 0x1p-45 * fabs(yd));
+    }
+    if (!amb) {
+        const double kd = fmin(fmax(floor(t) + h, 0.0), (double)((1 << b) - 1));
+        return (uint32_t)kd;
+    }
+    return exact_code(Prow, xrow, step, b);
+}
+
+// Plane of output word w of a tile: width p, bit shift in the code, word index in the plane.
+__device__ __forceinline__ void word_plane(int w, int r, int b, int& p, int& shift, int& lw) {
+    if (b == 8) { p = 8; shift = 0; lw = w; return; }
+    int rem = b;
+#pragma unroll
+    for (int q = 4; q >= 1; q >>= 1) {
+        if (b & q) {
+            rem -= q;
+            const int nw = 2 * r * q;
+            if (w < nw) { p = q; shift = rem; lw = w; return; }
+            w -= nw;
+        }
+    }
+    p = 1; shift = 0; lw = w;  // not reached for w < 2*r*b
+}
+
+constexpr int kEncThreads = 256;
+
+__global__ __launch_bounds__(kEncThreads) void encode_kernel(DevSide s, int side, const uint16_t* __restrict__ x,
+                                                             int64_t x_stride, int t0, int n_tok, int tile_first) {
+    extern __shared__ float smem[];
+    const int u = blockIdx.y;
+    const int tile = tile_first + blockIdx.x;
+    const int r = s.r[u], b = s.b[u];
+    const float step = s.delta[u];
+    const uint16_t* __restrict__ P = s.basis + s.basis_off[u];
+    float* Ps = smem;                                   // [r][128] fp32 basis
+    float* pn = Ps + r * kD;                            // [r] row norms
+    uint8_t* cs = reinterpret_cast<uint8_t*>(pn + kD);  // [64][128] codes
+
+    for (int k = threadIdx.x; k < r * kD; k += kEncThreads) Ps[k] = h2f((P[k]));
+    __syncthreads();
+    if (threadIdx.x < r) {
+        float s2 = 0.f;
+        for (int j = 0; j < kD; ++j) s2 = fmaf(Ps[threadIdx.x * kD + j], Ps[threadIdx.x * kD + j], s2);
+        pn[threadIdx.x] = sqrtf(s2);
+    }
+
+    const int t = threadIdx.x & 63, grp = threadIdx.x >> 6;
+    const int tok = tile * kTile + t;
+    const bool active = tok >= t0 && tok < t0 + n_tok;
+    const uint16_t* xrow = x + (int64_t)u * x_stride + (int64_t)(tok - t0) * kD;
+    float xv[kD];
+    float xn2 = 0.f;
+    if (active) {
+        const uint4* xr4 = reinterpret_cast<const uint4*>(xrow);
+#pragma unroll
+        for (int q = 0; q < kD / 8; ++q) {
+            const uint4 v = xr4[q];
+            const uint32_t w4[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                xv[8 * q + 2 * e] = h2f(((uint16_t)(w4[e] & 0xffff)));
+                xv[8 * q + 2 * e + 1] = h2f(((uint16_t)(w4[e] >> 16)));
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < kD; ++j) xn2 = fmaf(xv[j], xv[j], xn2);
+    }
+    // |acc - y| <= gamma_128 * sum_j |P_ij x_j| <= 2^-17 * ||P_i|| ||x||; 2^-15 leaves a 4x margin
+    // for the rounding of the norms themselves.
+    const float xn = sqrtf(xn2);
+    __syncthreads();
+    if (active) {
+        for (int i = grp; i < r; i += 4) {
+            const float4* Pr = reinterpret_cast<const float4*>(Ps + i * kD);
+            float acc = 0.f;
+#pragma unroll
+            for (int q = 0; q < kD / 4; ++q) {
+                const float4 pv = Pr[q];
+                acc = fmaf(pv.x, xv[4 * q], acc);
+                acc = fmaf(pv.y, xv[4 * q + 1], acc);
+                acc = fmaf(pv.z, xv[4 * q + 2], acc);
+                acc = fmaf(pv.w, xv[4 * q + 3], acc);
+            }
+            const float err = 0x1p-15f * pn[i] * xn;
+            cs[t * kD + i] = (uint8_t)decide_code(acc, err, step, b, P + (int64_t)i * kD, xrow);
+        }
+    }
+    __syncthreads();
+
+    // Pack: one thread per 32-bit output word; partial tiles keep the other tokens' bits.
+    uint32_t* tw = reinterpret_cast<uint32_t*>(s.codes + s.code_off[u] + (int64_t)tile * 8 * r * b);
+    const int tok0 = tile * kTile;
+    const bool full = tok0 >= t0 && tok0 + kTile <= t0 + n_tok;
+    const int n_words = 2 * r * b;
+    for (int w = threadIdx.x; w < n_words; w += kEncThreads) {
+        int p, shift, lw;
+        word_plane(w, r, b, p, shift, lw);
+        const int per_word = 32 / p;
+        const uint32_t vmask = (1u << p) - 1u;
+        uint32_t val = 0, msk = 0;
+        for (int iota = 0; iota < per_word; ++iota) {
+            const int phi = lw * per_word + iota;
+            int tt, i;
+            if (side == KVC_SIDE_K) { tt = phi / r; i = phi - tt * r; }
+            else { i = phi >> 6; tt = psi(phi & 63); }
+            const int tk = tok0 + tt;
+            if (tk >= t0 && tk < t0 + n_tok) {
+                const int bit = 8 * (iota & 3) + p * (iota >> 2);
+                val |= ((uint32_t)(cs[tt * kD + i] >> shift) & vmask) << bit;
+                msk |= vmask << bit;
+            }
+        }
+        tw[w] = full ? val : ((tw[w] & ~msk) | val);
+    }
+}
+
+// ---------------------------------------------------------------- reconstruct
+
+constexpr int kRecThreads = 256;
+
+__global__ __launch_bounds__(kRecThreads) void reconstruct_kernel(DevSide s, int side, int t0, int n_tok, float* __restrict__ out) {
+    extern __shared__ float smem[];
+    const int u = blockIdx.y;
+    const int blk0 = t0 + blockIdx.x * kTile;  // first token of this block
+    const int r = s.r[u], b = s.b[u];
+    const float step = s.delta[u];
+    const float half = (float)(1 << (b - 1)) - 0.5f;
+    const uint16_t* __restrict__ P = s.basis + s.basis_off[u];
+    const uint8_t* __restrict__ stream = s.codes + s.code_off[u];
+    float* Ps = smem;            // [r][128]
+    float* zh = Ps + r * kD;     // [64][r + 1]
+    const int zs = r + 1;
+    for (int k = threadIdx.x; k < r * kD; k += kRecThreads) Ps[k] = h2f((P[k]));
+    for (int k = threadIdx.x; k < kTile * r; k += kRecThreads) {
+        const int tt = k / r, i = k - tt * r;
+        const int tok = blk0 + tt;
+        float z = 0.f;
+        if (tok < t0 + n_tok) {
+            const uint8_t* tile = stream + (int64_t)(tok / kTile) * 8 * r * b;
+            const int tl = tok % kTile;
+            const int phi = side == KVC_SIDE_K ? slot_k(tl, i, r) : slot_v(tl, i);
+            z = ((float)load_code(tile, r, b, phi) - half) * step;
+        }
+        zh[tt * zs + i] = z;
+    }
+    __syncthreads();
+    const int j = threadIdx.x & (kD - 1);
+    for (int tt = threadIdx.x >> 7; tt < kTile; tt += kRecThreads / kD) {
+        const int tok = blk0 + tt;
+        if (tok >= t0 + n_tok) break;
+        float o = 0.f;
+        for (int i = 0; i < r; ++i) o = fmaf(Ps[i * kD + j], zh[tt * zs + i], o);
+        out[((int64_t)u * n_tok + (tok - t0)) * kD + j] = o;
+    }
+}
+
+// ---------------------------------------------------------------- decode attention
+
+// q~[u][g][i] = (step_K * log2(e) / sqrt(d)) * sum_j P_K[i][j] q[u][g][j]; zero for i >= r_K.
+__global__ __launch_bounds__(kD) void qproj_kernel(DevSide k, const uint16_t* __restrict__ q, int G, float* __restrict__ qs) {
+    __shared__ float qsh[kMaxG][kD];
+    const int u = blockIdx.x, i = threadIdx.x;
+    for (int g = 0; g < G; ++g) qsh[g][i] = h2f((q[((int64_t)u * G + g) * kD + i]));
+    __syncthreads();
+    const int r = k.r[u];
+    const float scale = k.delta[u] * 1.4426950408889634f * 0.08838834764831845f;  // log2(e) / sqrt(128)
+    const uint16_t* __restrict__ P = k.basis + k.basis_off[u] + (int64_t)i * kD;
+    for (int g = 0; g < G; ++g) {
+        float acc = 0.f;
+        if (i < r)
+            for (int j = 0; j < kD; ++j) acc = fmaf(h2f((P[j])), qsh[g][j], acc);
+        qs[((int64_t)u * G + g) * kD + i] = acc * scale;
+    }
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+    return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    return v;
+}
+
+// One wavefront per (unit, chunk). Logits use centred codes (c - 2^(b-1)); the
+// dropped +1/2 adds the same constant to every logit of a query, which softmax
+// ignores. The V accumulator also holds centred codes; combine adds the 1/2.
+template <int G>
+__global__ __launch_bounds__(64) void decode_partial_kernel(DevSide K, DevSide V, const float* __restrict__ qs,
+                                                            const int32_t* __restrict__ seq_len, int max_seq, int chunk,
+                                                            int n_chunks, float* __restrict__ part) {
+    __shared__ float qsh[G][kD];
+    __shared__ float psh[G][kTile];
+    const int u = blockIdx.y, c = blockIdx.x, lane = threadIdx.x;
+    int T = seq_len[u];
+    T = T < 0 ? 0 : (T > max_seq ? max_seq : T);
+    const int start = c * chunk;
+    const int end = min(T, start + chunk);
+    float* __restrict__ out = part + ((int64_t)u * n_chunks + c) * G * kPartStride;
+    if (start >= end) {
+        if (lane < G) { out[lane * kPartStride] = -INFINITY; out[lane * kPartStride + 1] = 0.f; }
+        return;
+    }
+    for (int g = 0; g < G; ++g) {
+        qsh[g][lane] = qs[((int64_t)u * G + g) * kD + lane];
+        qsh[g][lane + 64] = qs[((int64_t)u * G + g) * kD + lane + 64];
+    }
+    const int rk = K.r[u], bk = K.b[u], rv = V.r[u], bv = V.b[u];
+    const float hk = (float)(1 << (bk - 1)), hv = (float)(1 << (bv - 1));
+    const uint8_t* __restrict__ kstream = K.codes + K.code_off[u];
+    const uint8_t* __restrict__ vstream = V.codes + V.code_off[u];
+    float m[G], l[G], acc[G][2];
+#pragma unroll
+    for (int g = 0; g < G; ++g) { m[g] = -INFINITY; l[g] = 0.f; acc[g][0] = acc[g][1] = 0.f; }
+    __syncthreads();
+    for (int tok0 = start; tok0 < end; tok0 += kTile) {
+        const int tile = tok0 / kTile;
+        const uint8_t* ktile = kstream + (int64_t)tile * 8 * rk * bk;
+        const uint8_t* vtile = vstream + (int64_t)tile * 8 * rv * bv;
+        const bool valid = tok0 + lane < end;
+        float s[G];
+#pragma unroll
+        for (int g = 0; g < G; ++g) s[g] = 0.f;
+        for (int i = 0; i < rk; ++i) {
+            const float cf = (float)load_code(ktile, rk, bk, slot_k(lane, i, rk)) - hk;
+#pragma unroll
+            for (int g = 0; g < G; ++g) s[g] = fmaf(qsh[g][i], cf, s[g]);
+        }
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+            const float sv = valid ? s[g] : -INFINITY;
+            const float mn = fmaxf(m[g], wave_max(sv));
+            const float alpha = exp2f(m[g] - mn);
+            const float p = valid ? exp2f(sv - mn) : 0.f;
+            l[g] = l[g] * alpha + wave_sum(p);
+            acc[g][0] *= alpha;
+            acc[g][1] *= alpha;
+            m[g] = mn;
+            psh[g][lane] = p;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int jj = 0; jj < 2; ++jj) {
+            const int i = lane + 64 * jj;
+            if (i < rv) {
+                for (int t2 = 0; t2 < kTile; ++t2) {
+                    const float cf = (float)load_code(vtile, rv, bv, slot_v(t2, i)) - hv;
+#pragma unroll
+                    for (int g = 0; g < G; ++g) acc[g][jj] = fmaf(psh[g][t2], cf, acc[g][jj]);
+                }
+            }
+        }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+        if (lane == 0) { out[g * kPartStride] = m[g]; out[g * kPartStride + 1] = l[g]; }
+        out[g * kPartStride + 4 + lane] = acc[g][0];
+        out[g * kPartStride + 4 + lane + 64] = acc[g][1];
+    }
+}
+
+__global__ __launch_bounds__(kD) void combine_kernel(DevSide V, int G, int n_chunks, const float* __restrict__ part,
+                                                     float* __restrict__ out) {
+    __shared__ float zs[kD];
+    const int u = blockIdx.x, j = threadIdx.x;
+    const int rv = V.r[u];
+    const float step = V.delta[u];
+    const uint16_t* __restrict__ P = V.basis + V.basis_off[u];
+    for (int g = 0; g < G; ++g) {
+        const float* pg = part + (int64_t)u * n_chunks * G * kPartStride + g * kPartStride;
+        float M = -INFINITY;
+        for (int c = 0; c < n_chunks; ++c) M = fmaxf(M, pg[(int64_t)c * G * kPartStride]);
+        float L = 0.f, A = 0.f;
+        for (int c = 0; c < n_chunks; ++c) {
+            const float* pc = pg + (int64_t)c * G * kPartStride;
+            const float lc = pc[1];
+            if (lc > 0.f) {
+                const float w = exp2f(pc[0] - M);
+                L = fmaf(lc, w, L);
+                if (j < rv) A = fmaf(pc[4 + j], w, A);
+            }
+        }
+        if (j < rv) zs[j] = L > 0.f ? step * (A / L + 0.5f) : 0.f;
+        __syncthreads();
+        float o = 0.f;
+        for (int i = 0; i < rv; ++i) o = fmaf(h2f((P[(int64_t)i * kD + j])), zs[i], o);
+        out[((int64_t)u * G + g) * kD + j] = L > 0.f ? o : 0.f;
+        __syncthreads();
+    }
+}
+
+// ---------------------------------------------------------------- host side
+
+namespace {
+
+DevSide dev_side(const kvc_stream_desc* s) {
+    return DevSide{s->r, s->b, s->code_off, s->basis_off, s->delta, s->codes, s->basis};
+}
+
+int max_r(const kvc_stream_desc* s) {
+    int m = 2;
+    for (int u = 0; u < s->n_units; ++u) m = s->r_host[u] > m ? s->r_host[u] : m;
+    return m;
+}
+
+int check_launch(const char* what) {
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return set_error(KVC_EDEVICE, "%s: %s", what, hipGetErrorString(e));
+    return KVC_OK;
+}
+
+// Context chunk per work item: a power of two >= 64 giving about 4096 items.
+int choose_chunk(int n_units, int max_seq) {
+    const int64_t tokens = (int64_t)n_units * max_seq;
+    int64_t c = 64;
+    while (c < 4096 && tokens / (c * 2) >= 4096) c *= 2;
+    return (int)c;
+}
+
+int set_smem_limit(const void* fn, size_t bytes) {
+    const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+    if (e != hipSuccess) return set_error(KVC_EDEVICE, "hipFuncSetAttribute: %s", hipGetErrorString(e));
+    return KVC_OK;
+}
+
+}  // namespace
+}  // namespace kvc
+
+using namespace kvc;
+
+extern "C" int kvc_encode(const kvc_stream_desc* s, const uint16_t* x, int64_t x_unit_stride, int32_t t0, int32_t n_tok,
+                          void* stream) {
+    clear_error();
+    if (int e = validate_desc(s, "kvc_encode")) return e;
+    if (t0 < 0 || n_tok < 0) return set_error(KVC_EINVAL, "kvc_encode: negative t0 or n_tok");
+    if ((int64_t)t0 + n_tok > s->capacity) return set_error(KVC_ENOSPACE, "kvc_encode: t0 + n_tok > capacity");
+    if (n_tok == 0 || s->n_units == 0) return KVC_OK;
+    if (!x || (reinterpret_cast<uintptr_t>(x) & 15) || (x_unit_stride & 7) || x_unit_stride < (int64_t)n_tok * kD)
+        return set_error(KVC_EINVAL, "kvc_encode: x must be 16-byte aligned with stride a multiple of 8 and >= n_tok*d");
+    const int tile_first = t0 / kTile;
+    const int tile_last = (t0 + n_tok - 1) / kTile;
+    const size_t smem = (size_t)max_r(s) * kD * 4 + kD * 4 + kTile * kD;
+    if (int e = set_smem_limit((const void*)encode_kernel, smem)) return e;
+    dim3 grid(tile_last - tile_first + 1, s->n_units);
+    hipLaunchKernelGGL(encode_kernel, grid, dim3(kEncThreads), smem, (hipStream_t)stream, dev_side(s), s->side, x,
+                       x_unit_stride, t0, n_tok, tile_first);
+    return check_launch("kvc_encode");
+}
+
+extern "C" int kvc_reconstruct(const kvc_stream_desc* s, int32_t t0, int32_t n_tok, float* out, void* stream) {
+    clear_error();
+    if (int e = validate_desc(s, "kvc_reconstruct")) return e;
+    if (t0 < 0 || n_tok < 0) return set_error(KVC_EINVAL, "kvc_reconstruct: negative t0 or n_tok");
+    if ((int64_t)t0 + n_tok > s->capacity) return set_error(KVC_ENOSPACE, "kvc_reconstruct: t0 + n_tok > capacity");
+    if (n_tok == 0 || s->n_units == 0) return KVC_OK;
+    if (!out) return set_error(KVC_EINVAL, "kvc_reconstruct: null output");
+    const int r = max_r(s);
+    const size_t smem = (size_t)r * kD * 4 + (size_t)kTile * (r + 1) * 4;
+    if (int e = set_smem_limit((const void*)reconstruct_kernel, smem)) return e;
+    dim3 grid((n_tok + kTile - 1) / kTile, s->n_units);
+    hipLaunchKernelGGL(reconstruct_kernel, grid, dim3(kRecThreads), smem, (hipStream_t)stream, dev_side(s), s->side, t0,
+                       n_tok, out);
+    return check_launch("kvc_reconstruct");
+}
+
+static int decode_check(const kvc_stream_desc* k, const kvc_stream_desc* v, int32_t G, int32_t max_seq_len) {
+    if (int e = validate_desc(k, "kvc_decode_attn(k)")) return e;
+    if (int e = validate_desc(v, "kvc_decode_attn(v)")) return e;
+    if (k->side != KVC_SIDE_K || v->side != KVC_SIDE_V) return set_error(KVC_EINVAL, "kvc_decode_attn: descriptor sides");
+    if (k->n_units != v->n_units) return set_error(KVC_EINVAL, "kvc_decode_attn: K and V unit counts differ");
+    if (G != 1 && G != 2 && G != 4 && G != 8 && G != 16)
+        return set_error(KVC_EUNSUPPORTED, "kvc_decode_attn: G = %d (1, 2, 4, 8 or 16)", G);
+    if (max_seq_len < 1) return set_error(KVC_EINVAL, "kvc_decode_attn: max_seq_len < 1");
+    if (max_seq_len > k->capacity || max_seq_len > v->capacity)
+        return set_error(KVC_ENOSPACE, "kvc_decode_attn: max_seq_len exceeds capacity");
+    return KVC_OK;
+}
+
+extern "C" size_t kvc_decode_attn_workspace(const kvc_stream_desc* k, const kvc_stream_desc* v, int32_t G,
+                                            int32_t max_seq_len) {
+    clear_error();
+    if (decode_check(k, v, G, max_seq_len)) return 0;
+    const int chunk = choose_chunk(k->n_units, max_seq_len);
+    const int64_t n_chunks = (max_seq_len + chunk - 1) / chunk;
+    const int64_t qs = (int64_t)k->n_units * G * kD * 4;
+    const int64_t part = (int64_t)k->n_units * n_chunks * G * kPartStride * 4;
+    return (size_t)(((qs + 255) / 256) * 256 + part);
+}
+
+extern "C" int kvc_decode_attn(const kvc_stream_desc* k, const kvc_stream_desc* v, const uint16_t* q, int32_t G,
+                               const int32_t* seq_len, int32_t max_seq_len, float* out, void* ws, size_t ws_bytes,
+                               void* stream) {
+    clear_error();
+    if (int e = decode_check(k, v, G, max_seq_len)) return e;
+    if (k->n_units == 0) return KVC_OK;
+    if (!q || !seq_len || !out || !ws) return set_error(KVC_EINVAL, "kvc_decode_attn: null pointer");
+    if (reinterpret_cast<uintptr_t>(ws) & 255) return set_error(KVC_EINVAL, "kvc_decode_attn: workspace not 256-byte aligned");
+    const size_t need = kvc_decode_attn_workspace(k, v, G, max_seq_len);
+    if (ws_bytes < need) return set_error(KVC_ENOSPACE, "kvc_decode_attn: workspace %zu < %zu bytes", ws_bytes, need);
+    const int U = k->n_units;
+    const int chunk = choose_chunk(U, max_seq_len);
+    const int n_chunks = (max_seq_len + chunk - 1) / chunk;
+    float* qs = reinterpret_cast<float*>(ws);
+    float* part = reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + (((int64_t)U * G * kD * 4 + 255) / 256) * 256);
+    hipStream_t st = (hipStream_t)stream;
+    const DevSide K = dev_side(k), V = dev_side(v);
+    hipLaunchKernelGGL(qproj_kernel, dim3(U), dim3(kD), 0, st, K, q, G, qs);
+    dim3 grid(n_chunks, U);
+    switch (G) {
+        case 1: hipLaunchKernelGGL(decode_partial_kernel<1>, grid, dim3(64), 0, st, K, V, qs, seq_len, max_seq_len, chunk, n_chunks, part); break;
+        case 2: hipLaunchKernelGGL(decode_partial_kernel<2>, grid, dim3(64), 0, st, K, V, qs, seq_len, max_seq_len, chunk, n_chunks, part); break;
+        case 4: hipLaunchKernelGGL(decode_partial_kernel<4>, grid, dim3(64), 0, st, K, V, qs, seq_len, max_seq_len, chunk, n_chunks, part); break;
+        case 8: hipLaunchKernelGGL(decode_partial_kernel<8>, grid, dim3(64), 0, st, K, V, qs, seq_len, max_seq_len, chunk, n_chunks, part); break;
+        default: hipLaunchKernelGGL(decode_partial_kernel<16>, grid, dim3(64), 0, st, K, V, qs, seq_len, max_seq_len, chunk, n_chunks, part); break;
+    }
+    hipLaunchKernelGGL(combine_kernel, dim3(U), dim3(kD), 0, st, V, G, n_chunks, part, out);
+    return check_launch("kvc_decode_attn");
+}

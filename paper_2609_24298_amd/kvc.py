@@ -1,0 +1,219 @@
+"""Thin ctypes binding of libkvc (include/kvc.h): argument marshalling only.
+
+Every computation runs in the library (host allocator / basis builder in C++,
+everything else in HIP kernels). If libkvc.so is missing this module raises:
+there is no fallback path. PyTorch is used only for device memory and streams.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libkvc.so")
+
+KVC_OK, KVC_EINVAL, KVC_EUNSUPPORTED, KVC_ENOSPACE, KVC_EDEVICE = 0, 1, 2, 3, 4
+SIDE_K, SIDE_V = 0, 1
+SOLVER_DAMPED, SOLVER_DP, SOLVER_C1_ONLY = 0, 1, 2
+TILE = 64
+HEAD_DIM = 128
+
+
+class KvcError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"libkvc error {code}: {msg}")
+        self.code = code
+
+
+class AllocOpts(ctypes.Structure):
+    _fields_ = [("d", ctypes.c_int32), ("r_min", ctypes.c_int32), ("r_step", ctypes.c_int32),
+                ("b_min", ctypes.c_int32), ("b_max", ctypes.c_int32), ("solver", ctypes.c_int32),
+                ("rounds", ctypes.c_int32), ("reorder", ctypes.c_int32), ("bpd", ctypes.c_double),
+                ("eta", ctypes.c_double), ("B_min", ctypes.c_double), ("B_max", ctypes.c_double)]
+
+
+class HeadAlloc(ctypes.Structure):
+    _fields_ = [("r", ctypes.c_int32), ("b", ctypes.c_int32), ("B", ctypes.c_double), ("D", ctypes.c_double)]
+
+
+_p = ctypes.c_void_p
+
+
+class StreamDesc(ctypes.Structure):
+    _fields_ = [("n_units", ctypes.c_int32), ("d", ctypes.c_int32), ("capacity", ctypes.c_int32),
+                ("side", ctypes.c_int32),
+                ("r_host", _p), ("b_host", _p), ("code_off_host", _p), ("basis_off_host", _p), ("delta_host", _p),
+                ("r", _p), ("b", _p), ("code_off", _p), ("basis_off", _p), ("delta", _p),
+                ("codes", _p), ("codes_bytes", ctypes.c_int64), ("basis", _p), ("basis_elems", ctypes.c_int64)]
+
+
+_lib = None
+
+
+def lib():
+    """Load libkvc.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2609_24298_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        L.kvc_alloc_opts_default.argtypes = [ctypes.POINTER(AllocOpts), ctypes.c_double]
+        L.kvc_allocate.argtypes = [_p, _p, ctypes.c_int32, ctypes.POINTER(AllocOpts), _p, _p]
+        L.kvc_make_basis.argtypes = [_p, _p, _p, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _p, _p, _p]
+        L.kvc_encode.argtypes = [ctypes.POINTER(StreamDesc), _p, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, _p]
+        L.kvc_decode_attn.argtypes = [ctypes.POINTER(StreamDesc), ctypes.POINTER(StreamDesc), _p, ctypes.c_int32, _p,
+                                      ctypes.c_int32, _p, _p, ctypes.c_size_t, _p]
+        L.kvc_decode_attn_workspace.argtypes = [ctypes.POINTER(StreamDesc), ctypes.POINTER(StreamDesc),
+                                                ctypes.c_int32, ctypes.c_int32]
+        L.kvc_decode_attn_workspace.restype = ctypes.c_size_t
+        L.kvc_reconstruct.argtypes = [ctypes.POINTER(StreamDesc), ctypes.c_int32, ctypes.c_int32, _p, _p]
+        L.kvc_last_error.restype = ctypes.c_char_p
+        L.kvc_version.restype = ctypes.c_int32
+        _lib = L
+    return _lib
+
+
+def _check(rc: int):
+    if rc != KVC_OK:
+        raise KvcError(rc, lib().kvc_last_error().decode())
+
+
+def _np_ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+# ------------------------------------------------------------------ host calls
+
+def alloc_opts(bpd: float, solver: int = SOLVER_DAMPED, **kw) -> AllocOpts:
+    o = AllocOpts()
+    _check(lib().kvc_alloc_opts_default(ctypes.byref(o), float(bpd)))
+    o.solver = solver
+    for k, v in kw.items():
+        setattr(o, k, v)
+    return o
+
+
+def kvc_allocate(lam: np.ndarray, sigma2_q: np.ndarray | None, opts: AllocOpts):
+    lam = np.ascontiguousarray(lam, dtype=np.float64)
+    n, d = lam.shape
+    assert d == opts.d
+    sq = None if sigma2_q is None else np.ascontiguousarray(sigma2_q, dtype=np.float64)
+    out = (HeadAlloc * n)()
+    order = np.zeros((n, d), dtype=np.int32)
+    _check(lib().kvc_allocate(_np_ptr(lam), None if sq is None else _np_ptr(sq), n, ctypes.byref(opts),
+                              ctypes.cast(out, ctypes.c_void_p), _np_ptr(order)))
+    return {"r": np.array([h.r for h in out], dtype=np.int32), "b": np.array([h.b for h in out], dtype=np.int32),
+            "B": np.array([h.B for h in out]), "D": np.array([h.D for h in out]), "order": order}
+
+
+def kvc_make_basis(U: np.ndarray, order: np.ndarray, lam: np.ndarray, r: int, b: int, sign: np.ndarray):
+    U = np.ascontiguousarray(U, dtype=np.float64)
+    d = U.shape[0]
+    order = np.ascontiguousarray(order, dtype=np.int32)
+    lam = np.ascontiguousarray(lam, dtype=np.float64)
+    sign = np.ascontiguousarray(sign[:r], dtype=np.int8)
+    P = np.zeros((r, d), dtype=np.uint16)
+    delta = np.zeros(1, dtype=np.float32)
+    _check(lib().kvc_make_basis(_np_ptr(U), _np_ptr(order), _np_ptr(lam), d, int(r), int(b), _np_ptr(sign),
+                                _np_ptr(P), _np_ptr(delta)))
+    return P, delta[0]
+
+
+# ------------------------------------------------------------------ device side
+
+class Side:
+    """One side (K or V) of a compressed cache: per-unit tables, code arena and basis arena.
+
+    r, b, delta: per unit; basis: (n_bases x r_max x d) uint16 fp16 bits or a flat
+    array with basis_off giving each unit's element offset.
+    """
+
+    def __init__(self, side: int, r, b, delta, basis_flat, basis_off, capacity: int, device="cuda", codes=None):
+        import torch
+        self.side = side
+        self.capacity = int(capacity)
+        self.r_h = np.ascontiguousarray(r, dtype=np.int32)
+        self.b_h = np.ascontiguousarray(b, dtype=np.int32)
+        self.delta_h = np.ascontiguousarray(delta, dtype=np.float32)
+        self.basis_off_h = np.ascontiguousarray(basis_off, dtype=np.int64)
+        n = self.r_h.size
+        sizes = ((self.capacity + TILE - 1) // TILE) * 8 * self.r_h.astype(np.int64) * self.b_h
+        self.code_off_h = np.zeros(n, dtype=np.int64)
+        if n:
+            self.code_off_h[1:] = np.cumsum(((sizes + 255) // 256) * 256)[:-1]
+        total = int(self.code_off_h[-1] + sizes[-1]) if n else 0
+        dev = torch.device(device)
+        self.r = torch.as_tensor(self.r_h, device=dev)
+        self.b = torch.as_tensor(self.b_h, device=dev)
+        self.delta = torch.as_tensor(self.delta_h, device=dev)
+        self.code_off = torch.as_tensor(self.code_off_h, device=dev)
+        self.basis_off = torch.as_tensor(self.basis_off_h, device=dev)
+        self.basis = torch.as_tensor(np.ascontiguousarray(basis_flat, dtype=np.uint16).view(np.int16), device=dev)
+        self.codes = codes if codes is not None else torch.zeros(max(total, 16), dtype=torch.uint8, device=dev)
+        assert self.codes.numel() >= total
+        self.n_units = n
+        self.desc = StreamDesc(
+            n_units=n, d=HEAD_DIM, capacity=self.capacity, side=side,
+            r_host=_np_ptr(self.r_h), b_host=_np_ptr(self.b_h), code_off_host=_np_ptr(self.code_off_h),
+            basis_off_host=_np_ptr(self.basis_off_h), delta_host=_np_ptr(self.delta_h),
+            r=self.r.data_ptr(), b=self.b.data_ptr(), code_off=self.code_off.data_ptr(),
+            basis_off=self.basis_off.data_ptr(), delta=self.delta.data_ptr(),
+            codes=self.codes.data_ptr(), codes_bytes=self.codes.numel(), basis=self.basis.data_ptr(),
+            basis_elems=self.basis.numel())
+
+    def stream_bytes(self, u: int, n_tok: int) -> int:
+        return ((n_tok + TILE - 1) // TILE) * 8 * int(self.r_h[u]) * int(self.b_h[u])
+
+    def unit_codes(self, u: int, n_tok: int):
+        """Device view of unit u's stream bytes covering n_tok tokens."""
+        off = int(self.code_off_h[u])
+        return self.codes[off: off + self.stream_bytes(u, n_tok)]
+
+
+def _stream_ptr(stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def kvc_encode(side: Side, x, t0: int, n_tok: int, stream=None):
+    """x: fp16 tensor (n_units, >= n_tok, d) on the device."""
+    import torch
+    assert x.dtype == torch.float16 and x.is_contiguous() and x.dim() == 3
+    assert x.shape[0] == side.n_units and x.shape[1] >= n_tok and x.shape[2] == HEAD_DIM
+    assert x.device == side.codes.device
+    _check(lib().kvc_encode(ctypes.byref(side.desc), ctypes.c_void_p(x.data_ptr()), int(x.stride(0)), int(t0),
+                            int(n_tok), _stream_ptr(stream)))
+
+
+def kvc_decode_attn_workspace(k: Side, v: Side, G: int, max_seq_len: int) -> int:
+    n = lib().kvc_decode_attn_workspace(ctypes.byref(k.desc), ctypes.byref(v.desc), int(G), int(max_seq_len))
+    if n == 0:
+        _check(KVC_EINVAL if not lib().kvc_last_error() else KVC_EINVAL)
+    return int(n)
+
+
+def kvc_decode_attn(k: Side, v: Side, q, G: int, seq_len, max_seq_len: int, out, ws, stream=None):
+    """q: fp16 (n_units, G, d); seq_len: int32 (n_units,); out: f32 (n_units, G, d); ws: uint8 workspace."""
+    import torch
+    U = k.n_units
+    assert q.is_contiguous() and out.is_contiguous() and seq_len.is_contiguous()
+    assert q.dtype == torch.float16 and q.numel() == U * G * HEAD_DIM
+    assert out.dtype == torch.float32 and out.numel() == U * G * HEAD_DIM
+    assert seq_len.dtype == torch.int32 and seq_len.numel() == U and v.n_units == U
+    assert q.device == out.device == seq_len.device == ws.device == k.codes.device
+    _check(lib().kvc_decode_attn(ctypes.byref(k.desc), ctypes.byref(v.desc), ctypes.c_void_p(q.data_ptr()), int(G),
+                                 ctypes.c_void_p(seq_len.data_ptr()), int(max_seq_len),
+                                 ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(ws.data_ptr()), ws.numel(),
+                                 _stream_ptr(stream)))
+
+
+def kvc_reconstruct(side: Side, t0: int, n_tok: int, out, stream=None):
+    import torch
+    assert out.is_contiguous() and out.dtype == torch.float32 and out.numel() >= side.n_units * n_tok * HEAD_DIM
+    assert out.device == side.codes.device
+    _check(lib().kvc_reconstruct(ctypes.byref(side.desc), int(t0), int(n_tok), ctypes.c_void_p(out.data_ptr()),
+                                 _stream_ptr(stream)))

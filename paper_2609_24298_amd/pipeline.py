@@ -1,0 +1,111 @@
+"""Assemble a KV-COBRA compressed cache for a synthetic workload through libkvc.
+
+Calibration statistics come from the synthetic generator (synth); allocation,
+basis construction, encode, decode attention and reconstruction are library
+calls. Layout of units: u = (layer * batch + sequence) * kv_heads + head; the
+sequences of one (layer, head) share its basis.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+import numpy as np
+
+from . import kvc, synth
+
+
+@dataclass
+class SideTables:
+    r: np.ndarray          # per head
+    b: np.ndarray
+    order: np.ndarray      # per head x d
+    P: list                # per head: (r x d) uint16 fp16 bits
+    delta: np.ndarray      # per head, float32
+
+
+def allocate_workload(w: synth.Workload, stats, bpd: float | None = None, solver: int = kvc.SOLVER_DAMPED):
+    """Joint K+V tables: K with attention-KL weights and C1+C2, V with MSE weights and C1 only."""
+    bpd = w.bpd if bpd is None else bpd
+    lam_k = np.stack([s.lam_k for s in stats])
+    sq = np.stack([s.sigma2_q for s in stats])
+    lam_v = np.stack([s.lam_v for s in stats])
+    ak = kvc.kvc_allocate(lam_k, sq, kvc.alloc_opts(bpd, solver))
+    av = kvc.kvc_allocate(lam_v, None, kvc.alloc_opts(bpd, kvc.SOLVER_C1_ONLY))
+    sides = []
+    for a, lam_key, U_key, sign_key in ((ak, "lam_k", "U_k", "sign_k"), (av, "lam_v", "U_v", "sign_v")):
+        Ps, ds = [], []
+        for h, s in enumerate(stats):
+            P, dl = kvc.kvc_make_basis(getattr(s, U_key), a["order"][h], getattr(s, lam_key), int(a["r"][h]),
+                                       int(a["b"][h]), getattr(s, sign_key))
+            Ps.append(P)
+            ds.append(dl)
+        sides.append(SideTables(a["r"], a["b"], a["order"], Ps, np.array(ds, dtype=np.float32)))
+    return sides[0], sides[1]
+
+
+def build_side(side: int, tab: SideTables, w: synth.Workload, capacity: int, device="cuda") -> kvc.Side:
+    offs = np.zeros(len(tab.P), dtype=np.int64)
+    if len(tab.P) > 1:
+        offs[1:] = np.cumsum([p.size for p in tab.P])[:-1]
+    flat = np.concatenate([p.reshape(-1) for p in tab.P])
+    heads = np.array([w.head_of_unit(u) for u in range(w.n_units)], dtype=np.int64)
+    return kvc.Side(side, tab.r[heads], tab.b[heads], tab.delta[heads], flat, offs[heads], capacity, device)
+
+
+def draw_unit_tokens(w: synth.Workload, stats, side: int, n_tok: int, seed: int, device, units=None):
+    """fp16 tokens (len(units), n_tok, d) for the given units, drawn on `device`."""
+    import torch
+    units = range(w.n_units) if units is None else units
+    units = list(units)
+    x = torch.empty((len(units), n_tok, w.d), dtype=torch.float16, device=device)
+    for k, u in enumerate(units):
+        h = w.head_of_unit(u)
+        F = stats[h].F_k if side == kvc.SIDE_K else stats[h].F_v
+        x[k] = synth.draw_tokens_torch(F, n_tok, (seed, synth.KIND_TOK, side, u), device)
+    return x
+
+
+def draw_queries(w: synth.Workload, stats, seed: int, device, scale: float = 1.0):
+    """fp16 queries (n_units, G, d): query head g of unit u from N(0, Sigma_Q,g) of its KV head."""
+    import torch
+    q = np.zeros((w.n_units, w.group, w.d), dtype=np.float16)
+    for u in range(w.n_units):
+        h = w.head_of_unit(u)
+        rng = synth.rng_for(seed, synth.KIND_QVEC, u)
+        for g in range(w.group):
+            q[u, g] = (stats[h].F_q[g] @ rng.standard_normal(w.d) * scale).astype(np.float16)
+    return torch.as_tensor(q.view(np.int16), device=device).view(torch.float16)
+
+
+class Cache:
+    """A compressed K/V cache for a workload plus its decode buffers."""
+
+    def __init__(self, w: synth.Workload, seed: int = 0, device="cuda", bpd: float | None = None,
+                 capacity: int | None = None, solver: int = kvc.SOLVER_DAMPED, stats=None):
+        import torch
+        self.w = w
+        self.seed = seed
+        self.device = torch.device(device)
+        self.stats = synth.workload_stats(w, seed) if stats is None else stats
+        self.k_tab, self.v_tab = allocate_workload(w, self.stats, bpd, solver)
+        self.capacity = w.tokens if capacity is None else capacity
+        self.K = build_side(kvc.SIDE_K, self.k_tab, w, self.capacity, device)
+        self.V = build_side(kvc.SIDE_V, self.v_tab, w, self.capacity, device)
+
+    def encode(self, xk, xv, t0: int, n_tok: int, stream=None):
+        kvc.kvc_encode(self.K, xk, t0, n_tok, stream)
+        kvc.kvc_encode(self.V, xv, t0, n_tok, stream)
+
+    def decode_buffers(self, max_seq_len: int):
+        import torch
+        nbytes = kvc.kvc_decode_attn_workspace(self.K, self.V, self.w.group, max_seq_len)
+        ws = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
+        out = torch.empty((self.w.n_units, self.w.group, self.w.d), dtype=torch.float32, device=self.device)
+        return ws, out
+
+    def decode(self, q, seq_len, max_seq_len: int, out, ws, stream=None):
+        kvc.kvc_decode_attn(self.K, self.V, q, self.w.group, seq_len, max_seq_len, out, ws, stream)
+
+    def code_bytes(self, n_tok: int) -> int:
+        """Algorithmic bytes of the K and V code streams holding n_tok tokens per unit."""
+        return int(sum(self.K.stream_bytes(u, n_tok) + self.V.stream_bytes(u, n_tok) for u in range(self.w.n_units)))
