@@ -29,8 +29,9 @@
  *    planes in that order;
  *  - slot phi of a plane lies in word phi / (32/p) at bit
  *    8*(iota % 4) + p*(iota / 4), iota = phi % (32/p);
- *  - slot of (token t in the tile, coordinate i):
- *      K side: phi = t*r + i;
+ *  - slot of (token t in the tile, coordinate i), g16 = r/16, rho = r%16:
+ *      K side: i < 16*g16: phi = (i/16)*1024 + t*16 + i%16 (token-major in
+ *              groups of 16 coordinates); else phi = 1024*g16 + t*rho + (i - 16*g16);
  *      V side: phi = i*64 + psi(t), psi(16a + 4c + e) = 16c + 4a + e;
  *  - kvc_encode writes only the slots of the tokens it encodes; slots of
  *    tokens never encoded keep the arena's contents (zero if the caller

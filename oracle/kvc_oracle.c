@@ -84,7 +84,11 @@ static int n_planes(int b, int *w) {
 }
 
 static int slot_of(int side, int t, int i, int r) {
-    if (side == 0) return t * r + i;
+    if (side == 0) {
+        int g16 = r / 16, rho = r % 16;
+        if (i < 16 * g16) return (i / 16) * 1024 + t * 16 + i % 16;
+        return 1024 * g16 + t * rho + (i - 16 * g16);
+    }
     int a = t / 16, c = (t / 4) % 4, e = t % 4;
     return i * 64 + 16 * c + 4 * a + e;
 }

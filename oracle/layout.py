@@ -17,8 +17,10 @@ definition, and the oracle packs to it independently of the GPU encoder.
 * Inside a plane: 2*r*p little-endian 32-bit words. Slot phi in [0, 64 r) lies
   in word phi // (32/p); with iota = phi % (32/p) its bits start at
   8 * (iota % 4) + p * (iota // 4).
-* Slot of (token t in tile, coordinate i):
-  K side: phi = t * r + i                   (token-major)
+* Slot of (token t in tile, coordinate i), with g16 = r // 16, rho = r % 16:
+  K side: i < 16 g16:  phi = (i // 16) * 1024 + t * 16 + i % 16
+                       (token-major inside each group of 16 coordinates)
+          otherwise:   phi = 1024 g16 + t * rho + (i - 16 g16)   (the tail group)
   V side: phi = i * 64 + psi(t), psi(16 a + 4 c + e) = 16 c + 4 a + e
   (coordinate-major with a fixed 4x4 transpose of the token order).
 * Slots of tokens past the end of the last tile hold zero.
@@ -58,7 +60,12 @@ def psi(t: int) -> int:
 
 
 def slot(side: int, t: int, i: int, r: int) -> int:
-    return t * r + i if side == SIDE_K else i * TILE + psi(t)
+    if side == SIDE_V:
+        return i * TILE + psi(t)
+    g16, rho = r // 16, r % 16
+    if i < 16 * g16:
+        return (i // 16) * 1024 + t * 16 + i % 16
+    return 1024 * g16 + t * rho + (i - 16 * g16)
 
 
 def slot_bit(phi: int, p: int) -> tuple[int, int]:

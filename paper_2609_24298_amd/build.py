@@ -35,14 +35,17 @@ def build(verbose: bool = True) -> str:
     os.makedirs(BUILD, exist_ok=True)
     hipcc = _hipcc()
     host_o = os.path.join(BUILD, "kvc_host.o")
-    dev_o = os.path.join(BUILD, "kvc_kernels.o")
     _run(["g++", "-std=c++17", "-O2", "-fPIC", "-ffp-contract=off", "-fno-fast-math", "-Wall",
           "-I", INCLUDE, "-c", os.path.join(CSRC, "kvc_host.cpp"), "-o", host_o])
-    _run([hipcc, "-std=c++17", "-O3", "-fPIC", f"--offload-arch={ARCH}", "-ffp-contract=fast",
-          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-          "-I", INCLUDE, "-I", CSRC, "-c", os.path.join(CSRC, "kvc_kernels.hip"), "-o", dev_o])
+    objs = [host_o]
+    for src in ("kvc_kernels.hip", "kvc_decode.hip"):
+        o = os.path.join(BUILD, src.replace(".hip", ".o"))
+        _run([hipcc, "-std=c++17", "-O3", "-fPIC", f"--offload-arch={ARCH}", "-ffp-contract=fast",
+              "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+              "-I", INCLUDE, "-I", CSRC, "-c", os.path.join(CSRC, src), "-o", o])
+        objs.append(o)
     tmp = LIB + ".tmp%d" % os.getpid()
-    _run([hipcc, "-shared", f"--offload-arch={ARCH}", "-o", tmp, host_o, dev_o])
+    _run([hipcc, "-shared", f"--offload-arch={ARCH}", "-o", tmp] + objs)
     os.replace(tmp, LIB)
     return LIB
 

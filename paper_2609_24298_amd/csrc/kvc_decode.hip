@@ -1,0 +1,566 @@
+// Decode attention over the packed KV-COBRA cache on CDNA4 (gfx950): kernels
+// and the kvc_decode_attn launcher.
+//
+// The logits and the probability-weighted sum of values are dense contractions
+// in the rank space: S = Qt (G x r_K) . C_K^T (r_K x tokens) and
+// A = P (G x tokens) . C_V (tokens x r_V). Both run on int8 matrix cores
+// (v_mfma_i32_16x16x64_i8) with exact int32 accumulation:
+//  * codes enter as int8 (raw codes for b <= 7; c - 128 for b = 8);
+//  * the rank-space query q~ = P_K q is split into three balanced base-254
+//    int8 limbs with a per-query scale (relative error ~1e-7 of max|q~|);
+//  * the softmax weights p in [0, 1] are quantised to 21 bits,
+//    P = round(p (2^21 - 1)), and split into three 7-bit limbs;
+//  * centring (c - 2^(b-1)) is exact in integers: the logits subtract
+//    2^(b-1) sum_i Q_i, and the value accumulator carries an all-ones virtual
+//    coordinate whose column gives sum_t P_t (also the softmax denominator).
+// Per work item = (unit, context chunk) one wavefront walks the chunk in
+// 64-token tiles. Logits for 4 sub-tiles x 16 tokens come from the MFMA
+// accumulators, limbs are combined with row rotations (DPP), the online
+// softmax keeps a running max per query head, and the PV products accumulate
+// in int32 MFMA accumulators across tiles, flushed to fp32 (in LDS) only when
+// the running max of some head grows. A second kernel merges the chunks and
+// applies step_V and the V basis.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+
+#include "kvc_device.h"
+#include "kvc_internal.h"
+
+namespace kvc {
+
+constexpr int kD = KVC_HEAD_DIM;
+constexpr int kTile = KVC_TILE_TOKENS;
+constexpr int kPartStride = 132;  // floats per (item, query head): m, l, pad, pad, acc[128]
+constexpr int kAccStride = 132;   // LDS fp32 accumulator row: coordinates 0..r_V (r_V = all-ones column)
+constexpr int kLimbs = 3;
+constexpr float kLazy = 6.f;               // the running max is raised only when a tile beats it by > 2^6
+constexpr float kPScale = 32767.984375f;   // (2^21 - 1) / 2^6: p <= 2^6 maps to P < 2^21
+
+typedef int32_t v4i __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ v4i mfma_i8(v4i a, v4i b, v4i c) {
+    return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);
+}
+
+// Value of lane (lane + n) mod 16 within each row of 16 lanes (DPP row rotate).
+template <int N>
+__device__ __forceinline__ float row_ror(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x120 + N, 0xf, 0xf, false));
+}
+
+// Planes of a b-bit code, widest first (b = 8: one plane): width of plane k,
+// its bit shift inside the code and its offset in units of 8*r bytes.
+__host__ __device__ constexpr int n_planes(int b) { return b == 8 ? 1 : ((b & 4) ? 1 : 0) + ((b & 2) ? 1 : 0) + (b & 1); }
+__host__ __device__ constexpr int plane_w(int b, int k) {
+    return b == 8 ? 8 : (k == 0 ? ((b & 4) ? 4 : ((b & 2) ? 2 : 1))
+                               : (k == 1 ? ((b & 4) ? ((b & 2) ? 2 : 1) : 1) : 1));
+}
+__host__ __device__ constexpr int plane_sh(int b, int k) {
+    return k + 1 >= n_planes(b) ? 0 : plane_w(b, k + 1) + plane_sh(b, k + 1);
+}
+__host__ __device__ constexpr int plane_off(int b, int k) { return k == 0 ? 0 : plane_w(b, k - 1) + plane_off(b, k - 1); }
+
+__device__ __forceinline__ constexpr uint32_t plane_mask(int p) {
+    return p == 8 ? 0xffffffffu : (p == 4 ? 0x0f0f0f0fu : (p == 2 ? 0x03030303u : 0x01010101u));
+}
+
+// 16 slots [phi0, phi0 + 16) of one plane of width P, phi0 a multiple of 16:
+// dword d, byte j holds the plane value of slot phi0 + 4d + j.
+template <int P>
+__device__ __forceinline__ void plane_frag16(const uint8_t* __restrict__ plane, int phi0, uint32_t d[4]) {
+    constexpr uint32_t M = plane_mask(P);
+    if constexpr (P == 8) {
+        const uint4 w = *reinterpret_cast<const uint4*>(plane + phi0);
+        d[0] = w.x; d[1] = w.y; d[2] = w.z; d[3] = w.w;
+    } else if constexpr (P == 4) {
+        const uint2 w = *reinterpret_cast<const uint2*>(plane + (phi0 >> 1));
+        d[0] = w.x & M; d[1] = (w.x >> 4) & M; d[2] = w.y & M; d[3] = (w.y >> 4) & M;
+    } else if constexpr (P == 2) {
+        const uint32_t w = *reinterpret_cast<const uint32_t*>(plane + (phi0 >> 2));
+        d[0] = w & M; d[1] = (w >> 2) & M; d[2] = (w >> 4) & M; d[3] = (w >> 6) & M;
+    } else {
+        const uint32_t w = *reinterpret_cast<const uint32_t*>(plane + ((phi0 >> 5) << 2)) >> ((phi0 & 16) >> 2);
+        d[0] = w & M; d[1] = (w >> 1) & M; d[2] = (w >> 2) & M; d[3] = (w >> 3) & M;
+    }
+}
+
+template <int B, int K>
+__device__ __forceinline__ void add_plane16(const uint8_t* __restrict__ tile, int r, int phi0, uint32_t acc[4]) {
+    if constexpr (K < n_planes(B)) {
+        uint32_t f[4];
+        plane_frag16<plane_w(B, K)>(tile + 8 * r * plane_off(B, K), phi0, f);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[j] |= f[j] << plane_sh(B, K);
+    }
+}
+
+// Codes of 16 aligned slots of a tile (rank r, B bits), one byte each.
+template <int B>
+__device__ __forceinline__ v4i code_frag16(const uint8_t* __restrict__ tile, int r, int phi0) {
+    uint32_t acc[4] = {0, 0, 0, 0};
+    add_plane16<B, 0>(tile, r, phi0, acc);
+    add_plane16<B, 1>(tile, r, phi0, acc);
+    add_plane16<B, 2>(tile, r, phi0, acc);
+    return v4i{(int)acc[0], (int)acc[1], (int)acc[2], (int)acc[3]};
+}
+
+template <int B, int K>
+__device__ __forceinline__ uint32_t plane_subdword(const uint8_t* __restrict__ tile, int r, int sd) {
+    if constexpr (K < n_planes(B)) {
+        constexpr int P = plane_w(B, K);
+        constexpr int SPW = 8 / P;  // sub-dwords per word
+        const uint32_t w = reinterpret_cast<const uint32_t*>(tile + 8 * r * plane_off(B, K))[sd / SPW];
+        return ((w >> (P * (sd % SPW))) & plane_mask(P)) << plane_sh(B, K);
+    } else {
+        return 0u;
+    }
+}
+
+// Codes of the 4 slots of sub-dword sd of a tile (any alignment), one byte each.
+template <int B>
+__device__ __forceinline__ uint32_t code_subdword(const uint8_t* __restrict__ tile, int r, int sd) {
+    return plane_subdword<B, 0>(tile, r, sd) | plane_subdword<B, 1>(tile, r, sd) | plane_subdword<B, 2>(tile, r, sd);
+}
+
+// ---------------------------------------------------------------- q~ limbs
+
+// Per unit and query head: q~ = (step_K log2(e) / sqrt(d)) P_K q, its scale
+// sigma = max|q~| / 127 and three int8 limbs with q~ ~ sigma (L0 + L1/254 + L2/254^2);
+// corr[limb][g] = 2^(b_K - 1) sum_i L_limb,i (0 for b_K = 8, whose codes are centred on load).
+__global__ __launch_bounds__(kD) void qprep_kernel(DevSide K, const uint16_t* __restrict__ q, int G,
+                                                   int8_t* __restrict__ qlimb, float* __restrict__ qscale,
+                                                   int32_t* __restrict__ qcorr) {
+    __shared__ float qsh[16][kD];
+    __shared__ float fred[kD / 64];
+    __shared__ int ired[kLimbs][kD / 64];
+    const int u = blockIdx.x, i = threadIdx.x, lane = i & 63, wv = i >> 6;
+    for (int g = 0; g < G; ++g) qsh[g][i] = h2f(q[((int64_t)u * G + g) * kD + i]);
+    __syncthreads();
+    const int r = K.r[u], b = K.b[u];
+    const int hk = b == 8 ? 0 : (1 << (b - 1));
+    const float scale0 = K.delta[u] * 1.4426950408889634f * 0.08838834764831845f;  // log2(e) / sqrt(128)
+    const uint16_t* __restrict__ P = K.basis + K.basis_off[u] + (int64_t)i * kD;
+    for (int g = 0; g < G; ++g) {
+        float acc = 0.f;
+        if (i < r)
+            for (int j = 0; j < kD; ++j) acc = fmaf(h2f(P[j]), qsh[g][j], acc);
+        const float qt = acc * scale0;
+        float m = fabsf(qt);
+        for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
+        if (lane == 0) fred[wv] = m;
+        __syncthreads();
+        const float amax = fmaxf(fred[0], fred[1]);
+        const float sigma = amax > 0.f ? amax / 127.f : 1.f;
+        const float x = qt / sigma;
+        const float l0 = fminf(fmaxf(rintf(x), -127.f), 127.f);
+        const float r1 = (x - l0) * 254.f;
+        const float l1 = fminf(fmaxf(rintf(r1), -127.f), 127.f);
+        const float r2 = (r1 - l1) * 254.f;
+        const float l2 = fminf(fmaxf(rintf(r2), -127.f), 127.f);
+        const int L[kLimbs] = {(int)l0, (int)l1, (int)l2};
+#pragma unroll
+        for (int k = 0; k < kLimbs; ++k) {
+            qlimb[(((int64_t)u * kLimbs + k) * G + g) * kD + i] = (int8_t)L[k];
+            int s = L[k];
+            for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
+            if (lane == 0) ired[k][wv] = s;
+        }
+        __syncthreads();
+        if (i < kLimbs) qcorr[((int64_t)u * kLimbs + i) * G + g] = hk * (ired[i][0] + ired[i][1]);
+        if (i == 0) qscale[(int64_t)u * G + g] = sigma;
+        __syncthreads();
+    }
+}
+
+// ---------------------------------------------------------------- partials
+
+template <int G> struct Shape {
+    static constexpr int NT = (kLimbs * G + 15) / 16;  // logit N-tiles (columns = limb * G + g)
+    static constexpr int MT = (kLimbs * G + 15) / 16;  // PV M-tiles (rows = limb * G + g)
+    static constexpr int NV = kD / 16 + 1;             // V N-tiles incl. the all-ones coordinate
+};
+
+// Logits of one 64-token tile: lane (grp, col) gets s[st][i] for token 16 st + 4 grp + i and
+// query head col % G, in the log2 domain (-inf past `end`).
+template <int BK, int G>
+__device__ __forceinline__ void logits_tile(const uint8_t* __restrict__ ktile, int rk, uint8_t* __restrict__ tail,
+                                            int lane, int tok0, int end,
+                                            const v4i (&qB)[2][Shape<G>::NT], const float (&kcol)[Shape<G>::NT],
+                                            const float (&bcol)[Shape<G>::NT], float (&s)[4][4]) {
+    constexpr int NT = Shape<G>::NT;
+    constexpr int KX = BK == 8 ? (int)0x80808080 : 0;  // b = 8 codes enter centred (c - 128)
+    const int col = lane & 15, grp = lane >> 4;
+    const int g16 = rk >> 4, rho = rk & 15;
+    const int nk = (rk + 63) >> 6;
+    // Tail group (r_K % 16 coordinates): transpose its codes to [token][16] bytes in LDS.
+    if (rho) {
+        const int base_sd = g16 << 8;  // first sub-dword of the tail (slot 1024 g16)
+        for (int sd = lane; sd < 16 * rho; sd += 64) {
+            const uint32_t cw = code_subdword<BK>(ktile, rk, base_sd + sd);
+            const int q0 = 4 * sd, q1 = q0 + 2;
+            const int t0i = q0 / rho, t1i = q1 / rho;
+            *reinterpret_cast<uint16_t*>(tail + t0i * 16 + (q0 - t0i * rho)) = (uint16_t)(cw & 0xffff);
+            *reinterpret_cast<uint16_t*>(tail + t1i * 16 + (q1 - t1i * rho)) = (uint16_t)(cw >> 16);
+        }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int st = 0; st < 4; ++st) {
+        v4i S[NT];
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) S[nt] = v4i{0, 0, 0, 0};
+        const int t = 16 * st + col;
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            if (ks < nk) {
+                const int cg = 4 * ks + grp;  // this lane's group of 16 coordinates
+                v4i A = {0, 0, 0, 0};
+                if (cg < g16) A = code_frag16<BK>(ktile, rk, (cg << 10) + (t << 4));
+                else if (cg == g16 && rho) A = *reinterpret_cast<const v4i*>(tail + t * 16);
+                A ^= v4i{KX, KX, KX, KX};
+#pragma unroll
+                for (int nt = 0; nt < NT; ++nt) S[nt] = mfma_i8(A, qB[ks][nt], S[nt]);
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            float v = 0.f;
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) v += fmaf((float)S[nt][i], kcol[nt], bcol[nt]);
+            if (G <= 8) v += row_ror<8>(v);
+            if (G <= 4) v += row_ror<4>(v);
+            if (G <= 2) v += row_ror<2>(v);
+            if (G <= 1) v += row_ror<1>(v);
+            s[st][i] = tok0 + 16 * st + 4 * grp + i < end ? v : -INFINITY;
+        }
+    }
+    if (rho) __syncthreads();  // the tail buffer is rewritten by the next tile
+}
+
+// PV of one tile: B operand lane (grp, col) = coordinate 16 nt + col, tokens 16 st + 4 grp + i at slot 4 st + i;
+// coordinate rv is the all-ones column.
+template <int BV, int G>
+__device__ __forceinline__ void pv_tile(const uint8_t* __restrict__ vtile, int rv, int lane,
+                                        const v4i (&Ap)[Shape<G>::MT], v4i (&Cpv)[Shape<G>::MT][Shape<G>::NV]) {
+    constexpr int MT = Shape<G>::MT, NV = Shape<G>::NV;
+    constexpr int VX = BV == 8 ? (int)0x80808080 : 0;
+    const int col = lane & 15, grp = lane >> 4;
+    const int nv = rv / 16 + 1;
+#pragma unroll
+    for (int nt = 0; nt < NV; ++nt) {
+        if (nt < nv) {
+            const int coord = 16 * nt + col;
+            v4i B = {0, 0, 0, 0};
+            if (coord < rv) {
+                B = code_frag16<BV>(vtile, rv, (coord << 6) + (grp << 4));
+                B ^= v4i{VX, VX, VX, VX};
+            } else if (coord == rv) {
+                B = v4i{0x01010101, 0x01010101, 0x01010101, 0x01010101};
+            }
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) Cpv[mt][nt] = mfma_i8(Ap[mt], B, Cpv[mt][nt]);
+        }
+    }
+}
+
+template <int G>
+__global__ __launch_bounds__(64) void decode_mfma_kernel(DevSide K, DevSide V, const int8_t* __restrict__ qlimb,
+                                                         const float* __restrict__ qscale,
+                                                         const int32_t* __restrict__ qcorr,
+                                                         const int32_t* __restrict__ seq_len, int max_seq, int chunk,
+                                                         int n_chunks, float* __restrict__ part) {
+    constexpr int NT = Shape<G>::NT, MT = Shape<G>::MT, NV = Shape<G>::NV;
+    extern __shared__ float smem[];
+    float* accs = smem;                                                              // [3G][kAccStride] fp32
+    int* stage = reinterpret_cast<int*>(smem + kLimbs * G * kAccStride);            // [16 MT][kAccStride] int32
+    float* alph = smem + kLimbs * G * kAccStride + 16 * MT * kAccStride;            // [16]
+    uint8_t* tail = reinterpret_cast<uint8_t*>(alph + 16);                           // [64][16] K tail codes
+
+    const int u = blockIdx.y, c = blockIdx.x, lane = threadIdx.x;
+    const int col = lane & 15, grp = lane >> 4;
+    int T = seq_len[u];
+    T = T < 0 ? 0 : (T > max_seq ? max_seq : T);
+    const int start = c * chunk;
+    const int end = min(T, start + chunk);
+    float* __restrict__ out = part + ((int64_t)u * n_chunks + c) * G * kPartStride;
+    if (start >= end) {
+        if (lane < G) { out[lane * kPartStride] = -INFINITY; out[lane * kPartStride + 1] = 0.f; }
+        return;
+    }
+    const int rk = K.r[u], bk = K.b[u], rv = V.r[u], bv = V.b[u];
+    const int hv = bv == 8 ? 0 : (1 << (bv - 1));
+    const int nk = (rk + 63) >> 6;
+    const int nv = rv / 16 + 1;
+    const uint8_t* __restrict__ kstream = K.codes + K.code_off[u];
+    const uint8_t* __restrict__ vstream = V.codes + V.code_off[u];
+
+    // Logit B operands (q~ limbs) and per-column constants.
+    v4i qB[2][NT];
+    float kcol[NT], bcol[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+        const int cc = 16 * nt + col;
+        const int limb = cc / G, g = cc % G;
+        const bool ok = cc < kLimbs * G;
+        const float ls = limb == 0 ? 1.f : (limb == 1 ? (1.f / 254.f) : (1.f / 64516.f));
+        kcol[nt] = ok ? qscale[(int64_t)u * G + g] * ls : 0.f;
+        bcol[nt] = ok ? -(float)qcorr[((int64_t)u * kLimbs + limb) * G + g] * kcol[nt] : 0.f;
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            v4i v = {0, 0, 0, 0};
+            if (ok && ks < nk)
+                v = *reinterpret_cast<const v4i*>(qlimb + (((int64_t)u * kLimbs + limb) * G + g) * kD + 64 * ks + 16 * grp);
+            qB[ks][nt] = v;
+        }
+    }
+    for (int k = lane; k < kLimbs * G * kAccStride; k += 64) accs[k] = 0.f;
+    __syncthreads();
+
+    v4i Cpv[MT][NV];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < NV; ++nt) Cpv[mt][nt] = v4i{0, 0, 0, 0};
+    float m_run = -INFINITY;  // running max (log2 domain) of this lane's query head g = col % G
+
+    // Adds the int32 PV accumulators into the fp32 LDS rows, each row rescaled by its head's alpha:
+    // stage the integers in LDS, then one pass over (row, coordinate) with centring by the all-ones column.
+    auto flush = [&](float alpha_own) {
+        if (lane < G) alph[lane] = alpha_own;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                int* srow = stage + (16 * mt + 4 * grp + i) * kAccStride;
+#pragma unroll
+                for (int nt = 0; nt < NV; ++nt) {
+                    if (nt < nv && 16 * nt + col <= rv) srow[16 * nt + col] = Cpv[mt][nt][i];  // coords 0..rv
+                    Cpv[mt][nt][i] = 0;
+                }
+            }
+        __syncthreads();
+        const int w = rv + 1;
+        for (int k = lane; k < kLimbs * G * w; k += 64) {
+            const int row = k / w, coord = k - row * w;
+            const int plimb = row / G, g = row - plimb * G;
+            const int O = stage[row * kAccStride + rv];
+            const int v = coord < rv ? stage[row * kAccStride + coord] - hv * O : O;
+            const float ls = plimb == 0 ? 16384.f : (plimb == 1 ? 128.f : 1.f);
+            float& a = accs[row * kAccStride + coord];
+            a = fmaf(a, alph[g], (float)v * ls);
+        }
+        __syncthreads();
+    };
+
+    for (int tok0 = start; tok0 < end; tok0 += kTile) {
+        const uint8_t* __restrict__ ktile = kstream + (int64_t)(tok0 / kTile) * 8 * rk * bk;
+        const uint8_t* __restrict__ vtile = vstream + (int64_t)(tok0 / kTile) * 8 * rv * bv;
+        float s[4][4];
+        switch (bk) {
+            case 1: logits_tile<1, G>(ktile, rk, tail, lane, tok0, end, qB, kcol, bcol, s); break;
+            case 2: logits_tile<2, G>(ktile, rk, tail, lane, tok0, end, qB, kcol, bcol, s); break;
+            case 3: logits_tile<3, G>(ktile, rk, tail, lane, tok0, end, qB, kcol, bcol, s); break;
+            case 4: logits_tile<4, G>(ktile, rk, tail, lane, tok0, end, qB, kcol, bcol, s); break;
+            case 5: logits_tile<5, G>(ktile, rk, tail, lane, tok0, end, qB, kcol, bcol, s); break;
+            case 6: logits_tile<6, G>(ktile, rk, tail, lane, tok0, end, qB, kcol, bcol, s); break;
+            case 7: logits_tile<7, G>(ktile, rk, tail, lane, tok0, end, qB, kcol, bcol, s); break;
+            default: logits_tile<8, G>(ktile, rk, tail, lane, tok0, end, qB, kcol, bcol, s); break;
+        }
+
+        // Online softmax: running max per head; the int32 accumulators are flushed when it grows.
+        float mt_ = s[0][0];
+#pragma unroll
+        for (int st = 0; st < 4; ++st)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) mt_ = fmaxf(mt_, s[st][i]);
+        mt_ = fmaxf(mt_, __shfl_xor(mt_, 16));
+        mt_ = fmaxf(mt_, __shfl_xor(mt_, 32));
+        // lazy: keep the stale max while the tile stays within 2^kLazy of it (p <= 2^kLazy then)
+        const float m_new = mt_ > m_run + kLazy ? mt_ : m_run;
+        if (__any(m_new > m_run && m_run > -INFINITY)) flush(exp2f(m_run - m_new));
+        m_run = m_new;
+
+        // Probability limbs: P = round(p (2^21 - 1) / 2^kLazy) = L0 2^14 + L1 2^7 + L2 (p <= 2^kLazy);
+        // lane row 16 mt + col holds limb row / G.
+        uint32_t Pq[4][4];
+#pragma unroll
+        for (int st = 0; st < 4; ++st)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) Pq[st][i] = (uint32_t)fmaf(exp2f(s[st][i] - m_run), kPScale, 0.5f);
+        v4i Ap[MT];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+            const int row = 16 * mt + col;
+            const int plimb = row / G;
+            const uint32_t shift = 14 - 7 * plimb;
+            const uint32_t keep = plimb < kLimbs ? 0x7fu : 0u;
+#pragma unroll
+            for (int st = 0; st < 4; ++st) {
+                uint32_t w = 0;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) w |= ((Pq[st][i] >> shift) & keep) << (8 * i);
+                Ap[mt][st] = (int)w;
+            }
+        }
+
+        switch (bv) {
+            case 1: pv_tile<1, G>(vtile, rv, lane, Ap, Cpv); break;
+            case 2: pv_tile<2, G>(vtile, rv, lane, Ap, Cpv); break;
+            case 3: pv_tile<3, G>(vtile, rv, lane, Ap, Cpv); break;
+            case 4: pv_tile<4, G>(vtile, rv, lane, Ap, Cpv); break;
+            case 5: pv_tile<5, G>(vtile, rv, lane, Ap, Cpv); break;
+            case 6: pv_tile<6, G>(vtile, rv, lane, Ap, Cpv); break;
+            case 7: pv_tile<7, G>(vtile, rv, lane, Ap, Cpv); break;
+            default: pv_tile<8, G>(vtile, rv, lane, Ap, Cpv); break;
+        }
+    }
+    flush(1.f);
+    __syncthreads();
+
+    // Partial of each head: m, l = sum of P (all-ones column), centred accumulator; limbs summed here.
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+        const float mg = __shfl(m_run, g);
+        float* o = out + g * kPartStride;
+        float l = 0.f, a0 = 0.f, a1 = 0.f;
+#pragma unroll
+        for (int k = 0; k < kLimbs; ++k) {
+            const float* arow = accs + (k * G + g) * kAccStride;
+            l += arow[rv];
+            if (lane < rv) a0 += arow[lane];
+            if (lane + 64 < rv) a1 += arow[lane + 64];
+        }
+        if (lane == 0) { o[0] = mg; o[1] = l; }
+        o[4 + lane] = a0;
+        o[4 + 64 + lane] = a1;
+    }
+}
+
+// ---------------------------------------------------------------- combine
+
+__global__ __launch_bounds__(kD) void combine_kernel(DevSide V, int G, int n_chunks, const float* __restrict__ part,
+                                                     float* __restrict__ out) {
+    __shared__ float zs[kD];
+    const int u = blockIdx.x, j = threadIdx.x;
+    const int rv = V.r[u];
+    const float step = V.delta[u];
+    const uint16_t* __restrict__ P = V.basis + V.basis_off[u];
+    for (int g = 0; g < G; ++g) {
+        const float* pg = part + (int64_t)u * n_chunks * G * kPartStride + g * kPartStride;
+        float M = -INFINITY;
+        for (int c = 0; c < n_chunks; ++c) M = fmaxf(M, pg[(int64_t)c * G * kPartStride]);
+        float L = 0.f, A = 0.f;
+        for (int c = 0; c < n_chunks; ++c) {
+            const float* pc = pg + (int64_t)c * G * kPartStride;
+            const float lc = pc[1];
+            if (lc > 0.f) {
+                const float w = exp2f(pc[0] - M);
+                L = fmaf(lc, w, L);
+                if (j < rv) A = fmaf(pc[4 + j], w, A);
+            }
+        }
+        if (j < rv) zs[j] = L > 0.f ? step * (A / L + 0.5f) : 0.f;
+        __syncthreads();
+        float o = 0.f;
+        for (int i = 0; i < rv; ++i) o = fmaf(h2f(P[(int64_t)i * kD + j]), zs[i], o);
+        out[((int64_t)u * G + g) * kD + j] = L > 0.f ? o : 0.f;
+        __syncthreads();
+    }
+}
+
+// ---------------------------------------------------------------- host side
+
+namespace {
+
+// Context chunk per work item: a power of two >= 64 giving about 4096 items.
+int choose_chunk(int n_units, int max_seq) {
+    const int64_t tokens = (int64_t)n_units * max_seq;
+    int64_t c = 64;
+    while (c < 4096 && tokens / (c * 2) >= 4096) c *= 2;
+    return (int)c;
+}
+
+struct WsLayout {
+    int chunk, n_chunks;
+    int64_t qlimb, qscale, qcorr, part, total;  // byte offsets
+};
+
+WsLayout ws_layout(int U, int G, int max_seq) {
+    WsLayout L;
+    L.chunk = choose_chunk(U, max_seq);
+    L.n_chunks = (max_seq + L.chunk - 1) / L.chunk;
+    auto up = [](int64_t x) { return (x + 255) / 256 * 256; };
+    L.qlimb = 0;
+    L.qscale = up(L.qlimb + (int64_t)U * kLimbs * G * kD);
+    L.qcorr = up(L.qscale + (int64_t)U * G * 4);
+    L.part = up(L.qcorr + (int64_t)U * kLimbs * G * 4);
+    L.total = L.part + (int64_t)U * L.n_chunks * G * kPartStride * 4;
+    return L;
+}
+
+int decode_check(const kvc_stream_desc* k, const kvc_stream_desc* v, int32_t G, int32_t max_seq_len) {
+    if (int e = validate_desc(k, "kvc_decode_attn(k)")) return e;
+    if (int e = validate_desc(v, "kvc_decode_attn(v)")) return e;
+    if (k->side != KVC_SIDE_K || v->side != KVC_SIDE_V) return set_error(KVC_EINVAL, "kvc_decode_attn: descriptor sides");
+    if (k->n_units != v->n_units) return set_error(KVC_EINVAL, "kvc_decode_attn: K and V unit counts differ");
+    if (G != 1 && G != 2 && G != 4 && G != 8 && G != 16)
+        return set_error(KVC_EUNSUPPORTED, "kvc_decode_attn: G = %d (1, 2, 4, 8 or 16)", G);
+    if (max_seq_len < 1) return set_error(KVC_EINVAL, "kvc_decode_attn: max_seq_len < 1");
+    if (max_seq_len > k->capacity || max_seq_len > v->capacity)
+        return set_error(KVC_ENOSPACE, "kvc_decode_attn: max_seq_len exceeds capacity");
+    return KVC_OK;
+}
+
+template <int G>
+void launch_partials(dim3 grid, hipStream_t st, const DevSide& K, const DevSide& V, const int8_t* ql, const float* qs,
+                     const int32_t* qc, const int32_t* seq_len, int max_seq, int chunk, int n_chunks, float* part) {
+    const size_t smem = (size_t)kLimbs * G * kAccStride * 4 + (size_t)16 * Shape<G>::MT * kAccStride * 4 + 16 * 4 + 64 * 16;
+    hipLaunchKernelGGL(decode_mfma_kernel<G>, grid, dim3(64), smem, st, K, V, ql, qs, qc, seq_len, max_seq, chunk,
+                       n_chunks, part);
+}
+
+}  // namespace
+}  // namespace kvc
+
+using namespace kvc;
+
+extern "C" size_t kvc_decode_attn_workspace(const kvc_stream_desc* k, const kvc_stream_desc* v, int32_t G,
+                                            int32_t max_seq_len) {
+    clear_error();
+    if (decode_check(k, v, G, max_seq_len)) return 0;
+    return (size_t)ws_layout(k->n_units, G, max_seq_len).total;
+}
+
+extern "C" int kvc_decode_attn(const kvc_stream_desc* k, const kvc_stream_desc* v, const uint16_t* q, int32_t G,
+                               const int32_t* seq_len, int32_t max_seq_len, float* out, void* ws, size_t ws_bytes,
+                               void* stream) {
+    clear_error();
+    if (int e = decode_check(k, v, G, max_seq_len)) return e;
+    if (k->n_units == 0) return KVC_OK;
+    if (!q || !seq_len || !out || !ws) return set_error(KVC_EINVAL, "kvc_decode_attn: null pointer");
+    if (reinterpret_cast<uintptr_t>(ws) & 255) return set_error(KVC_EINVAL, "kvc_decode_attn: workspace not 256-byte aligned");
+    const int U = k->n_units;
+    const WsLayout L = ws_layout(U, G, max_seq_len);
+    if ((int64_t)ws_bytes < L.total)
+        return set_error(KVC_ENOSPACE, "kvc_decode_attn: workspace %zu < %lld bytes", ws_bytes, (long long)L.total);
+    char* w = reinterpret_cast<char*>(ws);
+    int8_t* ql = reinterpret_cast<int8_t*>(w + L.qlimb);
+    float* qs = reinterpret_cast<float*>(w + L.qscale);
+    int32_t* qc = reinterpret_cast<int32_t*>(w + L.qcorr);
+    float* part = reinterpret_cast<float*>(w + L.part);
+    hipStream_t st = (hipStream_t)stream;
+    const DevSide K = dev_side(k), V = dev_side(v);
+    hipLaunchKernelGGL(qprep_kernel, dim3(U), dim3(kD), 0, st, K, q, G, ql, qs, qc);
+    const dim3 grid(L.n_chunks, U);
+    switch (G) {
+        case 1: launch_partials<1>(grid, st, K, V, ql, qs, qc, seq_len, max_seq_len, L.chunk, L.n_chunks, part); break;
+        case 2: launch_partials<2>(grid, st, K, V, ql, qs, qc, seq_len, max_seq_len, L.chunk, L.n_chunks, part); break;
+        case 4: launch_partials<4>(grid, st, K, V, ql, qs, qc, seq_len, max_seq_len, L.chunk, L.n_chunks, part); break;
+        case 8: launch_partials<8>(grid, st, K, V, ql, qs, qc, seq_len, max_seq_len, L.chunk, L.n_chunks, part); break;
+        default: launch_partials<16>(grid, st, K, V, ql, qs, qc, seq_len, max_seq_len, L.chunk, L.n_chunks, part); break;
+    }
+    hipLaunchKernelGGL(combine_kernel, dim3(U), dim3(kD), 0, st, V, G, L.n_chunks, part, out);
+    return check_launch("kvc_decode_attn");
+}

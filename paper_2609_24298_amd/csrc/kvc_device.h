@@ -6,6 +6,9 @@
 
 #include <cstdint>
 
+#include "kvc.h"
+#include "kvc_internal.h"
+
 namespace kvc {
 
 // Per-side tables passed to kernels by value.
@@ -19,9 +22,23 @@ struct DevSide {
     const uint16_t* basis;
 };
 
-// Slot of (token t in tile, coordinate i): token-major for K, coordinate-major
-// with the 4x4 (a, c) transpose of the token index for V.
-__device__ __forceinline__ int slot_k(int t, int i, int r) { return t * r + i; }
+// Slot of (token t in tile, coordinate i). K: token-major inside groups of 16
+// coordinates (so a token's 16 codes of a group are 16 aligned slots), the
+// r % 16 tail group token-major after them. V: coordinate-major with the 4x4
+// (a, c) transpose of the token index.
+__device__ __forceinline__ int slot_k(int t, int i, int r) {
+    const int g16 = r >> 4;
+    if (i < 16 * g16) return ((i >> 4) << 10) + (t << 4) + (i & 15);
+    return (g16 << 10) + t * (r & 15) + (i - 16 * g16);
+}
+// Inverse of slot_k: token and coordinate of slot phi.
+__device__ __forceinline__ void unslot_k(int phi, int r, int& t, int& i) {
+    const int g16 = r >> 4;
+    if (phi < (g16 << 10)) { t = (phi >> 4) & 63; i = ((phi >> 10) << 4) + (phi & 15); return; }
+    const int rho = r & 15, q = phi - (g16 << 10);
+    t = q / rho;
+    i = 16 * g16 + (q - t * rho);
+}
 __device__ __forceinline__ int psi(int t) { return (t & 0x03) | ((t & 0x0c) << 2) | ((t & 0x30) >> 2); }
 __device__ __forceinline__ int slot_v(int t, int i) { return i * 64 + psi(t); }
 
@@ -56,6 +73,18 @@ __device__ __forceinline__ void half_parts(uint16_t h, int32_t& m, int& e) {
     if (ex == 0) { m = fr; e = -24; }
     else { m = 1024 + fr; e = ex - 25; }
     if (h & 0x8000) m = -m;
+}
+
+// ---------------------------------------------------------------- host helpers
+
+inline DevSide dev_side(const kvc_stream_desc* s) {
+    return DevSide{s->r, s->b, s->code_off, s->basis_off, s->delta, s->codes, s->basis};
+}
+
+inline int check_launch(const char* what) {
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return set_error(KVC_EDEVICE, "%s: %s", what, hipGetErrorString(e));
+    return KVC_OK;
 }
 
 }  // namespace kvc

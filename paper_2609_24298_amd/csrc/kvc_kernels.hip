@@ -1,5 +1,6 @@
-// Device half of libkvc: HIP kernels for CDNA4 (gfx950) and their C-ABI
-// launchers (encode, reconstruct, decode attention).
+// Device half of libkvc, compression side: HIP kernels for CDNA4 (gfx950) and
+// their C-ABI launchers (kvc_encode, kvc_reconstruct). Decode attention lives
+// in kvc_decode.hip.
 //
 // Kernels
 //  encode_kernel        one (unit, 64-token tile) per 256-thread block: the
@@ -9,13 +10,6 @@
 //                       are settled exactly in 128-bit integers, and the tile
 //                       is bit-packed from LDS with one thread per output word.
 //  reconstruct_kernel   x_hat = P^T z for a 64-token block of one unit.
-//  qproj_kernel         q~ = P_K q per unit and query head, pre-scaled by
-//                       step_K * log2(e) / sqrt(d) (rank-space logits).
-//  decode_partial_kernel  one (unit, context chunk) per wavefront: logits in
-//                       rank space from the K codes, online softmax, and the
-//                       probability-weighted sum of centred V codes.
-//  combine_kernel       merges the chunk partials of a unit and applies the
-//                       V step and basis: out = P_V^T (step_V (a / l + 1/2)).
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -28,8 +22,6 @@ namespace kvc {
 
 constexpr int kD = KVC_HEAD_DIM;
 constexpr int kTile = KVC_TILE_TOKENS;
-constexpr int kMaxG = 16;
-constexpr int kPartStride = 132;  // floats per (item, query head): m, l, pad, pad, acc[128]
 
 // ---------------------------------------------------------------- encode
 
@@ -172,7 +164,7 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(DevSide s, int side
         for (int iota = 0; iota < per_word; ++iota) {
             const int phi = lw * per_word + iota;
             int tt, i;
-            if (side == KVC_SIDE_K) { tt = phi / r; i = phi - tt * r; }
+            if (side == KVC_SIDE_K) unslot_k(phi, r, tt, i);
             else { i = phi >> 6; tt = psi(phi & 63); }
             const int tk = tok0 + tt;
             if (tk >= t0 && tk < t0 + n_tok) {
@@ -225,170 +217,14 @@ __global__ __launch_bounds__(kRecThreads) void reconstruct_kernel(DevSide s, int
     }
 }
 
-// ---------------------------------------------------------------- decode attention
-
-// q~[u][g][i] = (step_K * log2(e) / sqrt(d)) * sum_j P_K[i][j] q[u][g][j]; zero for i >= r_K.
-__global__ __launch_bounds__(kD) void qproj_kernel(DevSide k, const uint16_t* __restrict__ q, int G, float* __restrict__ qs) {
-    __shared__ float qsh[kMaxG][kD];
-    const int u = blockIdx.x, i = threadIdx.x;
-    for (int g = 0; g < G; ++g) qsh[g][i] = h2f((q[((int64_t)u * G + g) * kD + i]));
-    __syncthreads();
-    const int r = k.r[u];
-    const float scale = k.delta[u] * 1.4426950408889634f * 0.08838834764831845f;  // log2(e) / sqrt(128)
-    const uint16_t* __restrict__ P = k.basis + k.basis_off[u] + (int64_t)i * kD;
-    for (int g = 0; g < G; ++g) {
-        float acc = 0.f;
-        if (i < r)
-            for (int j = 0; j < kD; ++j) acc = fmaf(h2f((P[j])), qsh[g][j], acc);
-        qs[((int64_t)u * G + g) * kD + i] = acc * scale;
-    }
-}
-
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
-    return v;
-}
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-    return v;
-}
-
-// One wavefront per (unit, chunk). Logits use centred codes (c - 2^(b-1)); the
-// dropped +1/2 adds the same constant to every logit of a query, which softmax
-// ignores. The V accumulator also holds centred codes; combine adds the 1/2.
-template <int G>
-__global__ __launch_bounds__(64) void decode_partial_kernel(DevSide K, DevSide V, const float* __restrict__ qs,
-                                                            const int32_t* __restrict__ seq_len, int max_seq, int chunk,
-                                                            int n_chunks, float* __restrict__ part) {
-    __shared__ float qsh[G][kD];
-    __shared__ float psh[G][kTile];
-    const int u = blockIdx.y, c = blockIdx.x, lane = threadIdx.x;
-    int T = seq_len[u];
-    T = T < 0 ? 0 : (T > max_seq ? max_seq : T);
-    const int start = c * chunk;
-    const int end = min(T, start + chunk);
-    float* __restrict__ out = part + ((int64_t)u * n_chunks + c) * G * kPartStride;
-    if (start >= end) {
-        if (lane < G) { out[lane * kPartStride] = -INFINITY; out[lane * kPartStride + 1] = 0.f; }
-        return;
-    }
-    for (int g = 0; g < G; ++g) {
-        qsh[g][lane] = qs[((int64_t)u * G + g) * kD + lane];
-        qsh[g][lane + 64] = qs[((int64_t)u * G + g) * kD + lane + 64];
-    }
-    const int rk = K.r[u], bk = K.b[u], rv = V.r[u], bv = V.b[u];
-    const float hk = (float)(1 << (bk - 1)), hv = (float)(1 << (bv - 1));
-    const uint8_t* __restrict__ kstream = K.codes + K.code_off[u];
-    const uint8_t* __restrict__ vstream = V.codes + V.code_off[u];
-    float m[G], l[G], acc[G][2];
-#pragma unroll
-    for (int g = 0; g < G; ++g) { m[g] = -INFINITY; l[g] = 0.f; acc[g][0] = acc[g][1] = 0.f; }
-    __syncthreads();
-    for (int tok0 = start; tok0 < end; tok0 += kTile) {
-        const int tile = tok0 / kTile;
-        const uint8_t* ktile = kstream + (int64_t)tile * 8 * rk * bk;
-        const uint8_t* vtile = vstream + (int64_t)tile * 8 * rv * bv;
-        const bool valid = tok0 + lane < end;
-        float s[G];
-#pragma unroll
-        for (int g = 0; g < G; ++g) s[g] = 0.f;
-        for (int i = 0; i < rk; ++i) {
-            const float cf = (float)load_code(ktile, rk, bk, slot_k(lane, i, rk)) - hk;
-#pragma unroll
-            for (int g = 0; g < G; ++g) s[g] = fmaf(qsh[g][i], cf, s[g]);
-        }
-#pragma unroll
-        for (int g = 0; g < G; ++g) {
-            const float sv = valid ? s[g] : -INFINITY;
-            const float mn = fmaxf(m[g], wave_max(sv));
-            const float alpha = exp2f(m[g] - mn);
-            const float p = valid ? exp2f(sv - mn) : 0.f;
-            l[g] = l[g] * alpha + wave_sum(p);
-            acc[g][0] *= alpha;
-            acc[g][1] *= alpha;
-            m[g] = mn;
-            psh[g][lane] = p;
-        }
-        __syncthreads();
-#pragma unroll
-        for (int jj = 0; jj < 2; ++jj) {
-            const int i = lane + 64 * jj;
-            if (i < rv) {
-                for (int t2 = 0; t2 < kTile; ++t2) {
-                    const float cf = (float)load_code(vtile, rv, bv, slot_v(t2, i)) - hv;
-#pragma unroll
-                    for (int g = 0; g < G; ++g) acc[g][jj] = fmaf(psh[g][t2], cf, acc[g][jj]);
-                }
-            }
-        }
-        __syncthreads();
-    }
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-        if (lane == 0) { out[g * kPartStride] = m[g]; out[g * kPartStride + 1] = l[g]; }
-        out[g * kPartStride + 4 + lane] = acc[g][0];
-        out[g * kPartStride + 4 + lane + 64] = acc[g][1];
-    }
-}
-
-__global__ __launch_bounds__(kD) void combine_kernel(DevSide V, int G, int n_chunks, const float* __restrict__ part,
-                                                     float* __restrict__ out) {
-    __shared__ float zs[kD];
-    const int u = blockIdx.x, j = threadIdx.x;
-    const int rv = V.r[u];
-    const float step = V.delta[u];
-    const uint16_t* __restrict__ P = V.basis + V.basis_off[u];
-    for (int g = 0; g < G; ++g) {
-        const float* pg = part + (int64_t)u * n_chunks * G * kPartStride + g * kPartStride;
-        float M = -INFINITY;
-        for (int c = 0; c < n_chunks; ++c) M = fmaxf(M, pg[(int64_t)c * G * kPartStride]);
-        float L = 0.f, A = 0.f;
-        for (int c = 0; c < n_chunks; ++c) {
-            const float* pc = pg + (int64_t)c * G * kPartStride;
-            const float lc = pc[1];
-            if (lc > 0.f) {
-                const float w = exp2f(pc[0] - M);
-                L = fmaf(lc, w, L);
-                if (j < rv) A = fmaf(pc[4 + j], w, A);
-            }
-        }
-        if (j < rv) zs[j] = L > 0.f ? step * (A / L + 0.5f) : 0.f;
-        __syncthreads();
-        float o = 0.f;
-        for (int i = 0; i < rv; ++i) o = fmaf(h2f((P[(int64_t)i * kD + j])), zs[i], o);
-        out[((int64_t)u * G + g) * kD + j] = L > 0.f ? o : 0.f;
-        __syncthreads();
-    }
-}
-
 // ---------------------------------------------------------------- host side
 
 namespace {
-
-DevSide dev_side(const kvc_stream_desc* s) {
-    return DevSide{s->r, s->b, s->code_off, s->basis_off, s->delta, s->codes, s->basis};
-}
 
 int max_r(const kvc_stream_desc* s) {
     int m = 2;
     for (int u = 0; u < s->n_units; ++u) m = s->r_host[u] > m ? s->r_host[u] : m;
     return m;
-}
-
-int check_launch(const char* what) {
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return set_error(KVC_EDEVICE, "%s: %s", what, hipGetErrorString(e));
-    return KVC_OK;
-}
-
-// Context chunk per work item: a power of two >= 64 giving about 4096 items.
-int choose_chunk(int n_units, int max_seq) {
-    const int64_t tokens = (int64_t)n_units * max_seq;
-    int64_t c = 64;
-    while (c < 4096 && tokens / (c * 2) >= 4096) c *= 2;
-    return (int)c;
 }
 
 int set_smem_limit(const void* fn, size_t bytes) {
@@ -435,58 +271,4 @@ extern "C" int kvc_reconstruct(const kvc_stream_desc* s, int32_t t0, int32_t n_t
     hipLaunchKernelGGL(reconstruct_kernel, grid, dim3(kRecThreads), smem, (hipStream_t)stream, dev_side(s), s->side, t0,
                        n_tok, out);
     return check_launch("kvc_reconstruct");
-}
-
-static int decode_check(const kvc_stream_desc* k, const kvc_stream_desc* v, int32_t G, int32_t max_seq_len) {
-    if (int e = validate_desc(k, "kvc_decode_attn(k)")) return e;
-    if (int e = validate_desc(v, "kvc_decode_attn(v)")) return e;
-    if (k->side != KVC_SIDE_K || v->side != KVC_SIDE_V) return set_error(KVC_EINVAL, "kvc_decode_attn: descriptor sides");
-    if (k->n_units != v->n_units) return set_error(KVC_EINVAL, "kvc_decode_attn: K and V unit counts differ");
-    if (G != 1 && G != 2 && G != 4 && G != 8 && G != 16)
-        return set_error(KVC_EUNSUPPORTED, "kvc_decode_attn: G = %d (1, 2, 4, 8 or 16)", G);
-    if (max_seq_len < 1) return set_error(KVC_EINVAL, "kvc_decode_attn: max_seq_len < 1");
-    if (max_seq_len > k->capacity || max_seq_len > v->capacity)
-        return set_error(KVC_ENOSPACE, "kvc_decode_attn: max_seq_len exceeds capacity");
-    return KVC_OK;
-}
-
-extern "C" size_t kvc_decode_attn_workspace(const kvc_stream_desc* k, const kvc_stream_desc* v, int32_t G,
-                                            int32_t max_seq_len) {
-    clear_error();
-    if (decode_check(k, v, G, max_seq_len)) return 0;
-    const int chunk = choose_chunk(k->n_units, max_seq_len);
-    const int64_t n_chunks = (max_seq_len + chunk - 1) / chunk;
-    const int64_t qs = (int64_t)k->n_units * G * kD * 4;
-    const int64_t part = (int64_t)k->n_units * n_chunks * G * kPartStride * 4;
-    return (size_t)(((qs + 255) / 256) * 256 + part);
-}
-
-extern "C" int kvc_decode_attn(const kvc_stream_desc* k, const kvc_stream_desc* v, const uint16_t* q, int32_t G,
-                               const int32_t* seq_len, int32_t max_seq_len, float* out, void* ws, size_t ws_bytes,
-                               void* stream) {
-    clear_error();
-    if (int e = decode_check(k, v, G, max_seq_len)) return e;
-    if (k->n_units == 0) return KVC_OK;
-    if (!q || !seq_len || !out || !ws) return set_error(KVC_EINVAL, "kvc_decode_attn: null pointer");
-    if (reinterpret_cast<uintptr_t>(ws) & 255) return set_error(KVC_EINVAL, "kvc_decode_attn: workspace not 256-byte aligned");
-    const size_t need = kvc_decode_attn_workspace(k, v, G, max_seq_len);
-    if (ws_bytes < need) return set_error(KVC_ENOSPACE, "kvc_decode_attn: workspace %zu < %zu bytes", ws_bytes, need);
-    const int U = k->n_units;
-    const int chunk = choose_chunk(U, max_seq_len);
-    const int n_chunks = (max_seq_len + chunk - 1) / chunk;
-    float* qs = reinterpret_cast<float*>(ws);
-    float* part = reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + (((int64_t)U * G * kD * 4 + 255) / 256) * 256);
-    hipStream_t st = (hipStream_t)stream;
-    const DevSide K = dev_side(k), V = dev_side(v);
-    hipLaunchKernelGGL(qproj_kernel, dim3(U), dim3(kD), 0, st, K, q, G, qs);
-    dim3 grid(n_chunks, U);
-    switch (G) {
-        case 1: hipLaunchKernelGGL(decode_partial_kernel<1>, grid, dim3(64), 0, st, K, V, qs, seq_len, max_seq_len, chunk, n_chunks, part); break;
-        case 2: hipLaunchKernelGGL(decode_partial_kernel<2>, grid, dim3(64), 0, st, K, V, qs, seq_len, max_seq_len, chunk, n_chunks, part); break;
-        case 4: hipLaunchKernelGGL(decode_partial_kernel<4>, grid, dim3(64), 0, st, K, V, qs, seq_len, max_seq_len, chunk, n_chunks, part); break;
-        case 8: hipLaunchKernelGGL(decode_partial_kernel<8>, grid, dim3(64), 0, st, K, V, qs, seq_len, max_seq_len, chunk, n_chunks, part); break;
-        default: hipLaunchKernelGGL(decode_partial_kernel<16>, grid, dim3(64), 0, st, K, V, qs, seq_len, max_seq_len, chunk, n_chunks, part); break;
-    }
-    hipLaunchKernelGGL(combine_kernel, dim3(U), dim3(kD), 0, st, V, G, n_chunks, part, out);
-    return check_launch("kvc_decode_attn");
 }

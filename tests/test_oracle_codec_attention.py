@@ -89,7 +89,14 @@ def test_layout_hand_derived_bit_positions():
     c[5, 0] = 1
     s = onat.pack(c, 2, 1, ol.SIDE_V)
     assert list(np.nonzero(s)[0]) == [1] and s[1] == 16
-    # b = 8 on the K side is plain bytes in token-major order
+    # K side with a tail group, r = 18 (one group of 16 + 2 tail coordinates), b = 8 (plain bytes):
+    # token 1, coordinate 3 -> slot 0*1024 + 1*16 + 3 = 19; token 1, coordinate 17 -> slot 1024 + 1*2 + 1 = 1027
+    c18 = np.zeros((64, 18), dtype=np.uint8)
+    c18[1, 3] = 7
+    c18[1, 17] = 9
+    s = onat.pack(c18, 18, 8, ol.SIDE_K)
+    assert list(np.nonzero(s)[0]) == [19, 1027] and s[19] == 7 and s[1027] == 9
+    # b = 8 on the K side with r < 16 is plain bytes in token-major order
     c = np.arange(64 * 2, dtype=np.uint8).reshape(64, 2)
     s = onat.pack(c, 2, 8, ol.SIDE_K)
     assert np.array_equal(s, np.arange(128, dtype=np.uint8))
