@@ -13,13 +13,16 @@
 //  * centring (c - 2^(b-1)) is exact in integers: the logits subtract
 //    2^(b-1) sum_i Q_i, and the value accumulator carries an all-ones virtual
 //    coordinate whose column gives sum_t P_t (also the softmax denominator).
-// Per work item = (unit, context chunk) one wavefront walks the chunk in
-// 64-token tiles. Logits for 4 sub-tiles x 16 tokens come from the MFMA
-// accumulators, limbs are combined with row rotations (DPP), the online
-// softmax keeps a running max per query head, and the PV products accumulate
-// in int32 MFMA accumulators across tiles, flushed to fp32 (in LDS) only when
-// the running max of some head grows. A second kernel merges the chunks and
-// applies step_V and the V basis.
+// Per work item = (unit, context chunk) one wavefront walks the chunk in 64-token
+// tiles. Each packed K and V tile is staged in LDS with coalesced 16-byte loads;
+// operand fragments are extracted from LDS by code instantiated per bit width
+// (one switch per tile and side). Logits for 4 sub-tiles x 16 tokens come from
+// the MFMA accumulators, limbs are combined with row rotations (DPP), and the
+// online softmax keeps a lazily raised running max per query head. The PV
+// products accumulate in int32 MFMA accumulators across the whole chunk; when a
+// head's max grows they are rescaled in place. Centring and the limb sum happen
+// once at the end of the chunk. A second kernel merges the chunks and applies
+// step_V and the V basis.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -33,7 +36,7 @@ namespace kvc {
 constexpr int kD = KVC_HEAD_DIM;
 constexpr int kTile = KVC_TILE_TOKENS;
 constexpr int kPartStride = 132;  // floats per (item, query head): m, l, pad, pad, acc[128]
-constexpr int kAccStride = 132;   // LDS fp32 accumulator row: coordinates 0..r_V (r_V = all-ones column)
+constexpr int kAccStride = 132;   // LDS fp32 accumulator row: coordinates 0..127, 128 = all-ones column
 constexpr int kLimbs = 3;
 constexpr float kLazy = 6.f;               // the running max is raised only when a tile beats it by > 2^6
 constexpr float kPScale = 32767.984375f;   // (2^21 - 1) / 2^6: p <= 2^6 maps to P < 2^21
@@ -49,18 +52,6 @@ template <int N>
 __device__ __forceinline__ float row_ror(float v) {
     return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x120 + N, 0xf, 0xf, false));
 }
-
-// Planes of a b-bit code, widest first (b = 8: one plane): width of plane k,
-// its bit shift inside the code and its offset in units of 8*r bytes.
-__host__ __device__ constexpr int n_planes(int b) { return b == 8 ? 1 : ((b & 4) ? 1 : 0) + ((b & 2) ? 1 : 0) + (b & 1); }
-__host__ __device__ constexpr int plane_w(int b, int k) {
-    return b == 8 ? 8 : (k == 0 ? ((b & 4) ? 4 : ((b & 2) ? 2 : 1))
-                               : (k == 1 ? ((b & 4) ? ((b & 2) ? 2 : 1) : 1) : 1));
-}
-__host__ __device__ constexpr int plane_sh(int b, int k) {
-    return k + 1 >= n_planes(b) ? 0 : plane_w(b, k + 1) + plane_sh(b, k + 1);
-}
-__host__ __device__ constexpr int plane_off(int b, int k) { return k == 0 ? 0 : plane_w(b, k - 1) + plane_off(b, k - 1); }
 
 __device__ __forceinline__ constexpr uint32_t plane_mask(int p) {
     return p == 8 ? 0xffffffffu : (p == 4 ? 0x0f0f0f0fu : (p == 2 ? 0x03030303u : 0x01010101u));
@@ -86,6 +77,19 @@ __device__ __forceinline__ void plane_frag16(const uint8_t* __restrict__ plane, 
     }
 }
 
+// Planes of a b-bit code, widest first (b = 8: one plane): width of plane k, its bit
+// shift inside the code and its offset in units of 8*r bytes. Fragment extraction is
+// instantiated per b, so these fold to constants.
+__host__ __device__ constexpr int n_planes(int b) { return b == 8 ? 1 : ((b & 4) ? 1 : 0) + ((b & 2) ? 1 : 0) + (b & 1); }
+__host__ __device__ constexpr int plane_w(int b, int k) {
+    return b == 8 ? 8 : (k == 0 ? ((b & 4) ? 4 : ((b & 2) ? 2 : 1))
+                               : (k == 1 ? ((b & 4) ? ((b & 2) ? 2 : 1) : 1) : 1));
+}
+__host__ __device__ constexpr int plane_sh(int b, int k) {
+    return k + 1 >= n_planes(b) ? 0 : plane_w(b, k + 1) + plane_sh(b, k + 1);
+}
+__host__ __device__ constexpr int plane_off(int b, int k) { return k == 0 ? 0 : plane_w(b, k - 1) + plane_off(b, k - 1); }
+
 template <int B, int K>
 __device__ __forceinline__ void add_plane16(const uint8_t* __restrict__ tile, int r, int phi0, uint32_t acc[4]) {
     if constexpr (K < n_planes(B)) {
@@ -96,14 +100,16 @@ __device__ __forceinline__ void add_plane16(const uint8_t* __restrict__ tile, in
     }
 }
 
-// Codes of 16 aligned slots of a tile (rank r, B bits), one byte each.
+// Codes of 16 aligned slots of a tile (rank r, B bits), one byte each; b = 8 codes are
+// returned centred (c - 128) so that they fit int8.
 template <int B>
 __device__ __forceinline__ v4i code_frag16(const uint8_t* __restrict__ tile, int r, int phi0) {
     uint32_t acc[4] = {0, 0, 0, 0};
     add_plane16<B, 0>(tile, r, phi0, acc);
     add_plane16<B, 1>(tile, r, phi0, acc);
     add_plane16<B, 2>(tile, r, phi0, acc);
-    return v4i{(int)acc[0], (int)acc[1], (int)acc[2], (int)acc[3]};
+    constexpr uint32_t X = B == 8 ? 0x80808080u : 0u;
+    return v4i{(int)(acc[0] ^ X), (int)(acc[1] ^ X), (int)(acc[2] ^ X), (int)(acc[3] ^ X)};
 }
 
 template <int B, int K>
@@ -118,10 +124,11 @@ __device__ __forceinline__ uint32_t plane_subdword(const uint8_t* __restrict__ t
     }
 }
 
-// Codes of the 4 slots of sub-dword sd of a tile (any alignment), one byte each.
+// Codes of the 4 slots of sub-dword sd of a tile (any alignment), one byte each (b = 8 centred).
 template <int B>
 __device__ __forceinline__ uint32_t code_subdword(const uint8_t* __restrict__ tile, int r, int sd) {
-    return plane_subdword<B, 0>(tile, r, sd) | plane_subdword<B, 1>(tile, r, sd) | plane_subdword<B, 2>(tile, r, sd);
+    return (plane_subdword<B, 0>(tile, r, sd) | plane_subdword<B, 1>(tile, r, sd) | plane_subdword<B, 2>(tile, r, sd)) ^
+           (B == 8 ? 0x80808080u : 0u);
 }
 
 // ---------------------------------------------------------------- q~ limbs
@@ -182,101 +189,79 @@ template <int G> struct Shape {
     static constexpr int NV = kD / 16 + 1;             // V N-tiles incl. the all-ones coordinate
 };
 
-// Logits of one 64-token tile: lane (grp, col) gets s[st][i] for token 16 st + 4 grp + i and
-// query head col % G, in the log2 domain (-inf past `end`).
-template <int BK, int G>
-__device__ __forceinline__ void logits_tile(const uint8_t* __restrict__ ktile, int rk, uint8_t* __restrict__ tail,
-                                            int lane, int tok0, int end,
-                                            const v4i (&qB)[2][Shape<G>::NT], const float (&kcol)[Shape<G>::NT],
-                                            const float (&bcol)[Shape<G>::NT], float (&s)[4][4]) {
-    constexpr int NT = Shape<G>::NT;
-    constexpr int KX = BK == 8 ? (int)0x80808080 : 0;  // b = 8 codes enter centred (c - 128)
-    const int col = lane & 15, grp = lane >> 4;
+// K tail group (r_K % 16 coordinates) of the staged tile, transposed to [token][16] bytes in LDS.
+template <int BK>
+__device__ __forceinline__ void k_tail(const uint8_t* __restrict__ ktile, int rk, uint8_t* __restrict__ tail, int lane) {
     const int g16 = rk >> 4, rho = rk & 15;
-    const int nk = (rk + 63) >> 6;
-    // Tail group (r_K % 16 coordinates): transpose its codes to [token][16] bytes in LDS.
-    if (rho) {
-        const int base_sd = g16 << 8;  // first sub-dword of the tail (slot 1024 g16)
-        for (int sd = lane; sd < 16 * rho; sd += 64) {
-            const uint32_t cw = code_subdword<BK>(ktile, rk, base_sd + sd);
-            const int q0 = 4 * sd, q1 = q0 + 2;
-            const int t0i = q0 / rho, t1i = q1 / rho;
-            *reinterpret_cast<uint16_t*>(tail + t0i * 16 + (q0 - t0i * rho)) = (uint16_t)(cw & 0xffff);
-            *reinterpret_cast<uint16_t*>(tail + t1i * 16 + (q1 - t1i * rho)) = (uint16_t)(cw >> 16);
-        }
-        __syncthreads();
+    const float inv_rho = 1.f / (float)rho;
+    const int base_sd = g16 << 8;  // first sub-dword of the tail (slot 1024 g16)
+    for (int sd = lane; sd < 16 * rho; sd += 64) {
+        const uint32_t cw = code_subdword<BK>(ktile, rk, base_sd + sd);
+        const int q0 = 4 * sd, q1 = q0 + 2;
+        // q / rho for q < 64 rho: (q + 1/2) / rho sits >= 1/(2 rho) away from an integer, far above fp32 error
+        const int t0i = (int)(((float)q0 + 0.5f) * inv_rho), t1i = (int)(((float)q1 + 0.5f) * inv_rho);
+        *reinterpret_cast<uint16_t*>(tail + t0i * 16 + (q0 - t0i * rho)) = (uint16_t)(cw & 0xffff);
+        *reinterpret_cast<uint16_t*>(tail + t1i * 16 + (q1 - t1i * rho)) = (uint16_t)(cw >> 16);
     }
-#pragma unroll
-    for (int st = 0; st < 4; ++st) {
-        v4i S[NT];
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) S[nt] = v4i{0, 0, 0, 0};
-        const int t = 16 * st + col;
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-            if (ks < nk) {
-                const int cg = 4 * ks + grp;  // this lane's group of 16 coordinates
-                v4i A = {0, 0, 0, 0};
-                if (cg < g16) A = code_frag16<BK>(ktile, rk, (cg << 10) + (t << 4));
-                else if (cg == g16 && rho) A = *reinterpret_cast<const v4i*>(tail + t * 16);
-                A ^= v4i{KX, KX, KX, KX};
-#pragma unroll
-                for (int nt = 0; nt < NT; ++nt) S[nt] = mfma_i8(A, qB[ks][nt], S[nt]);
-            }
-        }
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            float v = 0.f;
-#pragma unroll
-            for (int nt = 0; nt < NT; ++nt) v += fmaf((float)S[nt][i], kcol[nt], bcol[nt]);
-            if (G <= 8) v += row_ror<8>(v);
-            if (G <= 4) v += row_ror<4>(v);
-            if (G <= 2) v += row_ror<2>(v);
-            if (G <= 1) v += row_ror<1>(v);
-            s[st][i] = tok0 + 16 * st + 4 * grp + i < end ? v : -INFINITY;
-        }
-    }
-    if (rho) __syncthreads();  // the tail buffer is rewritten by the next tile
 }
 
-// PV of one tile: B operand lane (grp, col) = coordinate 16 nt + col, tokens 16 st + 4 grp + i at slot 4 st + i;
-// coordinate rv is the all-ones column.
-template <int BV, int G>
-__device__ __forceinline__ void pv_tile(const uint8_t* __restrict__ vtile, int rv, int lane,
-                                        const v4i (&Ap)[Shape<G>::MT], v4i (&Cpv)[Shape<G>::MT][Shape<G>::NV]) {
-    constexpr int MT = Shape<G>::MT, NV = Shape<G>::NV;
-    constexpr int VX = BV == 8 ? (int)0x80808080 : 0;
+// K operand fragments of K-step ks for the 4 sub-tiles: lane (grp, col) = token 16 st + col,
+// coordinates 64 ks + 16 grp + [0, 16).
+template <int BK>
+__device__ __forceinline__ void k_frags(const uint8_t* __restrict__ ktile, const uint8_t* __restrict__ tail, int rk,
+                                        int ks, int lane, v4i (&Af)[4]) {
     const int col = lane & 15, grp = lane >> 4;
-    const int nv = rv / 16 + 1;
+    const int g16 = rk >> 4, rho = rk & 15;
+    const int cg = 4 * ks + grp;
 #pragma unroll
-    for (int nt = 0; nt < NV; ++nt) {
-        if (nt < nv) {
-            const int coord = 16 * nt + col;
-            v4i B = {0, 0, 0, 0};
-            if (coord < rv) {
-                B = code_frag16<BV>(vtile, rv, (coord << 6) + (grp << 4));
-                B ^= v4i{VX, VX, VX, VX};
-            } else if (coord == rv) {
-                B = v4i{0x01010101, 0x01010101, 0x01010101, 0x01010101};
-            }
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt) Cpv[mt][nt] = mfma_i8(Ap[mt], B, Cpv[mt][nt]);
-        }
+    for (int st = 0; st < 4; ++st) {
+        const int t = 16 * st + col;
+        v4i A = {0, 0, 0, 0};
+        if (cg < g16) A = code_frag16<BK>(ktile, rk, (cg << 10) + (t << 4));
+        else if (cg == g16 && rho) A = *reinterpret_cast<const v4i*>(tail + t * 16);
+        Af[st] = A;
     }
 }
+
+// V operand fragments of N-tiles nt0 .. nt0 + 4: lane (grp, col) = coordinate 16 nt + col, tokens
+// 16 st + 4 grp + i at slot 4 st + i; coordinate 128 is the all-ones column, other coordinates >= rv zero.
+template <int BV>
+__device__ __forceinline__ void v_frags(const uint8_t* __restrict__ vtile, int rv, int nt0, int lane, v4i (&Bf)[5]) {
+    const int col = lane & 15, grp = lane >> 4;
+#pragma unroll
+    for (int k = 0; k < 5; ++k) {
+        const int coord = 16 * (nt0 + k) + col;
+        v4i B = {0, 0, 0, 0};
+        if (coord < rv) B = code_frag16<BV>(vtile, rv, (coord << 6) + (grp << 4));
+        else if (coord == kD) B = v4i{0x01010101, 0x01010101, 0x01010101, 0x01010101};
+        Bf[k] = B;
+    }
+}
+
+// Runs CALL with the compile-time bit width B_ equal to the runtime value b.
+#define KVC_SWITCH_B(b, CALL)                                \
+    switch (b) {                                             \
+        case 1: { constexpr int B_ = 1; CALL; } break;       \
+        case 2: { constexpr int B_ = 2; CALL; } break;       \
+        case 3: { constexpr int B_ = 3; CALL; } break;       \
+        case 4: { constexpr int B_ = 4; CALL; } break;       \
+        case 5: { constexpr int B_ = 5; CALL; } break;       \
+        case 6: { constexpr int B_ = 6; CALL; } break;       \
+        case 7: { constexpr int B_ = 7; CALL; } break;       \
+        default: { constexpr int B_ = 8; CALL; } break;      \
+    }
 
 template <int G>
 __global__ __launch_bounds__(64) void decode_mfma_kernel(DevSide K, DevSide V, const int8_t* __restrict__ qlimb,
                                                          const float* __restrict__ qscale,
                                                          const int32_t* __restrict__ qcorr,
                                                          const int32_t* __restrict__ seq_len, int max_seq, int chunk,
-                                                         int n_chunks, float* __restrict__ part) {
+                                                         int n_chunks, float* __restrict__ part, int raw_bytes) {
     constexpr int NT = Shape<G>::NT, MT = Shape<G>::MT, NV = Shape<G>::NV;
     extern __shared__ float smem[];
-    float* accs = smem;                                                              // [3G][kAccStride] fp32
-    int* stage = reinterpret_cast<int*>(smem + kLimbs * G * kAccStride);            // [16 MT][kAccStride] int32
-    float* alph = smem + kLimbs * G * kAccStride + 16 * MT * kAccStride;            // [16]
-    uint8_t* tail = reinterpret_cast<uint8_t*>(alph + 16);                           // [64][16] K tail codes
+    float* accs = smem;                                                // [G][kAccStride] fp32: coords 0..127, 128 = sum P
+    uint8_t* tail = reinterpret_cast<uint8_t*>(smem + G * kAccStride);  // [64][16] K tail codes
+    uint4* raw = reinterpret_cast<uint4*>(tail + 64 * 16);             // raw K tile, then V tile
 
     const int u = blockIdx.y, c = blockIdx.x, lane = threadIdx.x;
     const int col = lane & 15, grp = lane >> 4;
@@ -292,7 +277,7 @@ __global__ __launch_bounds__(64) void decode_mfma_kernel(DevSide K, DevSide V, c
     const int rk = K.r[u], bk = K.b[u], rv = V.r[u], bv = V.b[u];
     const int hv = bv == 8 ? 0 : (1 << (bv - 1));
     const int nk = (rk + 63) >> 6;
-    const int nv = rv / 16 + 1;
+    const int nv = (rv + 15) >> 4;  // V N-tiles holding coordinates (N-tile 8 = all-ones column)
     const uint8_t* __restrict__ kstream = K.codes + K.code_off[u];
     const uint8_t* __restrict__ vstream = V.codes + V.code_off[u];
 
@@ -315,7 +300,7 @@ __global__ __launch_bounds__(64) void decode_mfma_kernel(DevSide K, DevSide V, c
             qB[ks][nt] = v;
         }
     }
-    for (int k = lane; k < kLimbs * G * kAccStride; k += 64) accs[k] = 0.f;
+    for (int k = lane; k < G * kAccStride; k += 64) accs[k] = 0.f;
     __syncthreads();
 
     v4i Cpv[MT][NV];
@@ -325,51 +310,94 @@ __global__ __launch_bounds__(64) void decode_mfma_kernel(DevSide K, DevSide V, c
         for (int nt = 0; nt < NV; ++nt) Cpv[mt][nt] = v4i{0, 0, 0, 0};
     float m_run = -INFINITY;  // running max (log2 domain) of this lane's query head g = col % G
 
-    // Adds the int32 PV accumulators into the fp32 LDS rows, each row rescaled by its head's alpha:
-    // stage the integers in LDS, then one pass over (row, coordinate) with centring by the all-ones column.
-    auto flush = [&](float alpha_own) {
-        if (lane < G) alph[lane] = alpha_own;
+    // When a head's running max grows (by more than 2^kLazy, so alpha <= 2^-kLazy) its int32
+    // accumulators are rescaled in place: C <- rint(C alpha). The rounding adds at most about one
+    // quantum of P per rescale, the size of one token's quantisation error; rows whose head kept
+    // its max are left untouched.
+    auto rescale = [&](float alpha_own) {
+        int lane = threadIdx.x;
+        asm volatile("" : "+v"(lane));
+        const int grp = lane >> 4;
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                int* srow = stage + (16 * mt + 4 * grp + i) * kAccStride;
+                const int row = 16 * mt + 4 * grp + i;
+                const float alpha = __shfl(alpha_own, (lane & 48) | (row % G));
+                if (alpha != 1.f) {
 #pragma unroll
-                for (int nt = 0; nt < NV; ++nt) {
-                    if (nt < nv && 16 * nt + col <= rv) srow[16 * nt + col] = Cpv[mt][nt][i];  // coords 0..rv
-                    Cpv[mt][nt][i] = 0;
+                    for (int nt = 0; nt < NV; ++nt) Cpv[mt][nt][i] = (int)rintf((float)Cpv[mt][nt][i] * alpha);
                 }
             }
-        __syncthreads();
-        const int w = rv + 1;
-        for (int k = lane; k < kLimbs * G * w; k += 64) {
-            const int row = k / w, coord = k - row * w;
-            const int plimb = row / G, g = row - plimb * G;
-            const int O = stage[row * kAccStride + rv];
-            const int v = coord < rv ? stage[row * kAccStride + coord] - hv * O : O;
-            const float ls = plimb == 0 ? 16384.f : (plimb == 1 ? 128.f : 1.f);
-            float& a = accs[row * kAccStride + coord];
-            a = fmaf(a, alph[g], (float)v * ls);
-        }
-        __syncthreads();
     };
 
+    const int kch = (8 * rk * bk) >> 4, vch = (8 * rv * bv) >> 4;  // 16-byte chunks per K / V tile
+    const uint8_t* ktile = reinterpret_cast<const uint8_t*>(raw);
+    const uint8_t* vtile = reinterpret_cast<const uint8_t*>(raw + kch);
     for (int tok0 = start; tok0 < end; tok0 += kTile) {
-        const uint8_t* __restrict__ ktile = kstream + (int64_t)(tok0 / kTile) * 8 * rk * bk;
-        const uint8_t* __restrict__ vtile = vstream + (int64_t)(tok0 / kTile) * 8 * rv * bv;
+        // An opaque per-tile copy of the lane id: lane-dependent fragment offsets are recomputed
+        // inside the loop instead of being hoisted and kept live in registers across it.
+        int lane_it = lane;
+        asm volatile("" : "+v"(lane_it));
+        // Stage the packed K and V tiles in LDS: coalesced 16-byte loads, 4 chunks per lane per round.
+        {
+            const uint4* kg = reinterpret_cast<const uint4*>(kstream + (int64_t)(tok0 / kTile) * 8 * rk * bk);
+            const uint4* vg = reinterpret_cast<const uint4*>(vstream + (int64_t)(tok0 / kTile) * 8 * rv * bv);
+            const int nch = kch + vch;
+            for (int c0 = 0; c0 < nch; c0 += 256) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int cc = c0 + 64 * j + lane_it;
+                    if (cc < nch) raw[cc] = cc < kch ? kg[cc] : vg[cc - kch];
+                }
+            }
+            __syncthreads();
+        }
+        // Logits: S[st] = sum over K-steps of codes (tokens x 64 coords) . q~ limbs (64 coords x columns).
+        if (rk & 15) {
+            KVC_SWITCH_B(bk, k_tail<B_>(ktile, rk, tail, lane_it));
+            __syncthreads();
+        }
+        v4i S[4][NT];
+#pragma unroll
+        for (int st = 0; st < 4; ++st)
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) S[st][nt] = v4i{0, 0, 0, 0};
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            if (ks < nk) {
+                v4i Af[4];
+                KVC_SWITCH_B(bk, k_frags<B_>(ktile, tail, rk, ks, lane_it, Af));
+#pragma unroll
+                for (int st = 0; st < 4; ++st)
+#pragma unroll
+                    for (int nt = 0; nt < NT; ++nt) S[st][nt] = mfma_i8(Af[st], qB[ks][nt], S[st][nt]);
+            }
+        }
+        // Limb columns -> logits: lane (grp, col) gets tokens 16 st + 4 grp + i for head col % G (log2 domain).
         float s[4][4];
-        switch (bk) {
-            case 1: logits_tile<1, G>(ktile, rk, tail, lane, tok0, end, qB, kcol, bcol, s); break;
-            case 2: logits_tile<2, G>(ktile, rk, tail, lane, tok0, end, qB, kcol, bcol, s); break;
-            case 3: logits_tile<3, G>(ktile, rk, tail, lane, tok0, end, qB, kcol, bcol, s); break;
-            case 4: logits_tile<4, G>(ktile, rk, tail, lane, tok0, end, qB, kcol, bcol, s); break;
-            case 5: logits_tile<5, G>(ktile, rk, tail, lane, tok0, end, qB, kcol, bcol, s); break;
-            case 6: logits_tile<6, G>(ktile, rk, tail, lane, tok0, end, qB, kcol, bcol, s); break;
-            case 7: logits_tile<7, G>(ktile, rk, tail, lane, tok0, end, qB, kcol, bcol, s); break;
-            default: logits_tile<8, G>(ktile, rk, tail, lane, tok0, end, qB, kcol, bcol, s); break;
+#pragma unroll
+        for (int st = 0; st < 4; ++st)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                float v = 0.f;
+#pragma unroll
+                for (int nt = 0; nt < NT; ++nt) v += fmaf((float)S[st][nt][i], kcol[nt], bcol[nt]);
+                if (G <= 8) v += row_ror<8>(v);
+                if (G <= 4) v += row_ror<4>(v);
+                if (G <= 2) v += row_ror<2>(v);
+                if (G <= 1) v += row_ror<1>(v);
+                s[st][i] = v;
+            }
+        if (tok0 + kTile > end) {  // last tile of the chunk: tokens past the end get zero weight
+#pragma unroll
+            for (int st = 0; st < 4; ++st)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    if (tok0 + 16 * st + 4 * (lane_it >> 4) + i >= end) s[st][i] = -INFINITY;
         }
 
-        // Online softmax: running max per head; the int32 accumulators are flushed when it grows.
+        // Online softmax: running max per head; the int32 accumulators are rescaled when it grows.
         float mt_ = s[0][0];
 #pragma unroll
         for (int st = 0; st < 4; ++st)
@@ -379,7 +407,7 @@ __global__ __launch_bounds__(64) void decode_mfma_kernel(DevSide K, DevSide V, c
         mt_ = fmaxf(mt_, __shfl_xor(mt_, 32));
         // lazy: keep the stale max while the tile stays within 2^kLazy of it (p <= 2^kLazy then)
         const float m_new = mt_ > m_run + kLazy ? mt_ : m_run;
-        if (__any(m_new > m_run && m_run > -INFINITY)) flush(exp2f(m_run - m_new));
+        if (__any(m_new > m_run && m_run > -INFINITY)) rescale(m_new > m_run ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.f);
         m_run = m_new;
 
         // Probability limbs: P = round(p (2^21 - 1) / 2^kLazy) = L0 2^14 + L1 2^7 + L2 (p <= 2^kLazy);
@@ -388,7 +416,7 @@ __global__ __launch_bounds__(64) void decode_mfma_kernel(DevSide K, DevSide V, c
 #pragma unroll
         for (int st = 0; st < 4; ++st)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) Pq[st][i] = (uint32_t)fmaf(exp2f(s[st][i] - m_run), kPScale, 0.5f);
+            for (int i = 0; i < 4; ++i) Pq[st][i] = (uint32_t)fmaf(__builtin_amdgcn_exp2f(s[st][i] - m_run), kPScale, 0.5f);
         v4i Ap[MT];
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
@@ -405,36 +433,53 @@ __global__ __launch_bounds__(64) void decode_mfma_kernel(DevSide K, DevSide V, c
             }
         }
 
-        switch (bv) {
-            case 1: pv_tile<1, G>(vtile, rv, lane, Ap, Cpv); break;
-            case 2: pv_tile<2, G>(vtile, rv, lane, Ap, Cpv); break;
-            case 3: pv_tile<3, G>(vtile, rv, lane, Ap, Cpv); break;
-            case 4: pv_tile<4, G>(vtile, rv, lane, Ap, Cpv); break;
-            case 5: pv_tile<5, G>(vtile, rv, lane, Ap, Cpv); break;
-            case 6: pv_tile<6, G>(vtile, rv, lane, Ap, Cpv); break;
-            case 7: pv_tile<7, G>(vtile, rv, lane, Ap, Cpv); break;
-            default: pv_tile<8, G>(vtile, rv, lane, Ap, Cpv); break;
+        // PV: Cpv[mt][nt] += P limbs (rows x 64 tokens) . V codes (64 tokens x 16 coords).
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+            const int nt0 = 5 * half;
+            v4i Bf[5];
+            KVC_SWITCH_B(bv, v_frags<B_>(vtile, rv, nt0, lane_it, Bf));
+#pragma unroll
+            for (int k = 0; k < 5; ++k)
+                if (nt0 + k < NV && (nt0 + k < nv || nt0 + k == NV - 1))
+#pragma unroll
+                    for (int mt = 0; mt < MT; ++mt) Cpv[mt][nt0 + k] = mfma_i8(Ap[mt], Bf[k], Cpv[mt][nt0 + k]);
         }
+        __syncthreads();  // raw is restaged by the next tile
     }
-    flush(1.f);
+    // Centre (exact, in integers, with the all-ones column O) and combine the three P limbs of each
+    // head into the fp32 LDS accumulator: accs[g][c] = sum_limb ls (C - 2^(b-1) O), accs[g][128] = sum_limb ls O.
+    {
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int row = 16 * mt + 4 * grp + i;
+                const int plimb = row / G, g = row - plimb * G;
+                const int O = __shfl(Cpv[mt][NV - 1][i], lane & 48);
+                const float ls = plimb == 0 ? 16384.f : (plimb == 1 ? 128.f : 1.f);
+                float* arow = accs + g * kAccStride;
+                if (plimb < kLimbs) {
+#pragma unroll
+                    for (int nt = 0; nt < NV - 1; ++nt) {
+                        const int coord = 16 * nt + col;
+                        if (nt < nv && coord < rv) atomicAdd(arow + coord, (float)(Cpv[mt][nt][i] - hv * O) * ls);
+                    }
+                    if (col == 0) atomicAdd(arow + kD, (float)O * ls);
+                }
+            }
+    }
     __syncthreads();
 
-    // Partial of each head: m, l = sum of P (all-ones column), centred accumulator; limbs summed here.
+    // Partial of each head: m, l = sum of P (all-ones column), centred accumulator.
 #pragma unroll
     for (int g = 0; g < G; ++g) {
         const float mg = __shfl(m_run, g);
         float* o = out + g * kPartStride;
-        float l = 0.f, a0 = 0.f, a1 = 0.f;
-#pragma unroll
-        for (int k = 0; k < kLimbs; ++k) {
-            const float* arow = accs + (k * G + g) * kAccStride;
-            l += arow[rv];
-            if (lane < rv) a0 += arow[lane];
-            if (lane + 64 < rv) a1 += arow[lane + 64];
-        }
-        if (lane == 0) { o[0] = mg; o[1] = l; }
-        o[4 + lane] = a0;
-        o[4 + 64 + lane] = a1;
+        const float* arow = accs + g * kAccStride;
+        if (lane == 0) { o[0] = mg; o[1] = arow[kD]; }
+        o[4 + lane] = lane < rv ? arow[lane] : 0.f;
+        o[4 + 64 + lane] = lane + 64 < rv ? arow[lane + 64] : 0.f;
     }
 }
 
@@ -514,11 +559,18 @@ int decode_check(const kvc_stream_desc* k, const kvc_stream_desc* v, int32_t G, 
 }
 
 template <int G>
-void launch_partials(dim3 grid, hipStream_t st, const DevSide& K, const DevSide& V, const int8_t* ql, const float* qs,
-                     const int32_t* qc, const int32_t* seq_len, int max_seq, int chunk, int n_chunks, float* part) {
-    const size_t smem = (size_t)kLimbs * G * kAccStride * 4 + (size_t)16 * Shape<G>::MT * kAccStride * 4 + 16 * 4 + 64 * 16;
+int launch_partials(dim3 grid, hipStream_t st, const DevSide& K, const DevSide& V, const int8_t* ql, const float* qs,
+                    const int32_t* qc, const int32_t* seq_len, int max_seq, int chunk, int n_chunks, float* part,
+                    int raw_bytes) {
+    const size_t smem = (size_t)G * kAccStride * 4 + 64 * 16 + (size_t)raw_bytes;
+    if (smem > 64 * 1024) {
+        const hipError_t e = hipFuncSetAttribute((const void*)decode_mfma_kernel<G>,
+                                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+        if (e != hipSuccess) return set_error(KVC_EDEVICE, "hipFuncSetAttribute: %s", hipGetErrorString(e));
+    }
     hipLaunchKernelGGL(decode_mfma_kernel<G>, grid, dim3(64), smem, st, K, V, ql, qs, qc, seq_len, max_seq, chunk,
-                       n_chunks, part);
+                       n_chunks, part, raw_bytes);
+    return KVC_OK;
 }
 
 }  // namespace
@@ -553,14 +605,21 @@ extern "C" int kvc_decode_attn(const kvc_stream_desc* k, const kvc_stream_desc* 
     hipStream_t st = (hipStream_t)stream;
     const DevSide K = dev_side(k), V = dev_side(v);
     hipLaunchKernelGGL(qprep_kernel, dim3(U), dim3(kD), 0, st, K, q, G, ql, qs, qc);
-    const dim3 grid(L.n_chunks, U);
-    switch (G) {
-        case 1: launch_partials<1>(grid, st, K, V, ql, qs, qc, seq_len, max_seq_len, L.chunk, L.n_chunks, part); break;
-        case 2: launch_partials<2>(grid, st, K, V, ql, qs, qc, seq_len, max_seq_len, L.chunk, L.n_chunks, part); break;
-        case 4: launch_partials<4>(grid, st, K, V, ql, qs, qc, seq_len, max_seq_len, L.chunk, L.n_chunks, part); break;
-        case 8: launch_partials<8>(grid, st, K, V, ql, qs, qc, seq_len, max_seq_len, L.chunk, L.n_chunks, part); break;
-        default: launch_partials<16>(grid, st, K, V, ql, qs, qc, seq_len, max_seq_len, L.chunk, L.n_chunks, part); break;
+    int raw_bytes = 16;
+    for (int u = 0; u < U; ++u) {
+        const int tb = 8 * k->r_host[u] * k->b_host[u] + 8 * v->r_host[u] * v->b_host[u];
+        raw_bytes = tb > raw_bytes ? tb : raw_bytes;
     }
+    const dim3 grid(L.n_chunks, U);
+    int e = KVC_OK;
+    switch (G) {
+        case 1: e = launch_partials<1>(grid, st, K, V, ql, qs, qc, seq_len, max_seq_len, L.chunk, L.n_chunks, part, raw_bytes); break;
+        case 2: e = launch_partials<2>(grid, st, K, V, ql, qs, qc, seq_len, max_seq_len, L.chunk, L.n_chunks, part, raw_bytes); break;
+        case 4: e = launch_partials<4>(grid, st, K, V, ql, qs, qc, seq_len, max_seq_len, L.chunk, L.n_chunks, part, raw_bytes); break;
+        case 8: e = launch_partials<8>(grid, st, K, V, ql, qs, qc, seq_len, max_seq_len, L.chunk, L.n_chunks, part, raw_bytes); break;
+        default: e = launch_partials<16>(grid, st, K, V, ql, qs, qc, seq_len, max_seq_len, L.chunk, L.n_chunks, part, raw_bytes); break;
+    }
+    if (e) return e;
     hipLaunchKernelGGL(combine_kernel, dim3(U), dim3(kD), 0, st, V, G, L.n_chunks, part, out);
     return check_launch("kvc_decode_attn");
 }
