@@ -14,17 +14,21 @@
 //    2^(b-1) sum_i Q_i, and the value accumulator carries an all-ones virtual
 //    coordinate whose column gives sum_t P_t (also the softmax denominator).
 // Per work item = (unit, context chunk) one wavefront walks the chunk in 64-token
-// tiles. Each packed K and V tile is staged in LDS with coalesced 16-byte loads;
+// tiles. Each packed K and V tile is staged in LDS with coalesced 16-byte loads
+// (the next tile's loads are in flight while the current one is computed);
 // operand fragments are extracted from LDS by code instantiated per bit width
-// (one switch per tile and side). Logits for 4 sub-tiles x 16 tokens come from
-// the MFMA accumulators, limbs are combined with row rotations (DPP), and the
-// online softmax keeps a lazily raised running max per query head. The PV
-// products accumulate in int32 MFMA accumulators across the whole chunk; when a
-// head's max grows they are rescaled in place. Centring and the limb sum happen
-// once at the end of the chunk. A second kernel merges the chunks and applies
-// step_V and the V basis.
+// (one switch per tile and side). The logits take the q~ limbs as the A operand
+// (rows = head x limb) and the K codes as B (columns = tokens), so each lane
+// receives the three limbs of one (head, token) pair and forms the logit alone.
+// The online softmax keeps a lazily raised running max per query head; the
+// probabilities are split into limbs and written to LDS in the token order of the
+// V layout, where they are read back as the A operand of the PV products. Those
+// accumulate in int32 MFMA accumulators across the whole chunk and are rescaled in
+// place when a head's max grows. Centring and the limb sum happen once at the end
+// of the chunk. A second kernel merges the chunks and applies step_V and the V basis.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 
@@ -184,10 +188,15 @@ __global__ __launch_bounds__(kD) void qprep_kernel(DevSide K, const uint16_t* __
 // ---------------------------------------------------------------- partials
 
 template <int G> struct Shape {
-    static constexpr int NT = (kLimbs * G + 15) / 16;  // logit N-tiles (columns = limb * G + g)
-    static constexpr int MT = (kLimbs * G + 15) / 16;  // PV M-tiles (rows = limb * G + g)
+    static constexpr int LM = (4 * G + 15) / 16;       // logit M-tiles: row 4 h + limb (limb 3 is zero)
+    static constexpr int PM = (kLimbs * G + 15) / 16;  // PV M-tiles: row limb * G + h
     static constexpr int NV = kD / 16 + 1;             // V N-tiles incl. the all-ones coordinate
 };
+
+// Token of logit column col in sub-tile st. With this order a lane's four tokens (st = 0..3) sit at
+// the consecutive V slots 4 col + st of the token permutation psi, so its probability limbs go to
+// LDS as one dword per limb.
+__device__ __forceinline__ int tok_of(int st, int col) { return 16 * (col & 3) + 4 * (col >> 2) + st; }
 
 // K tail group (r_K % 16 coordinates) of the staged tile, transposed to [token][16] bytes in LDS.
 template <int BK>
@@ -205,36 +214,29 @@ __device__ __forceinline__ void k_tail(const uint8_t* __restrict__ ktile, int rk
     }
 }
 
-// K operand fragments of K-step ks for the 4 sub-tiles: lane (grp, col) = token 16 st + col,
-// coordinates 64 ks + 16 grp + [0, 16).
+// K operand fragments of K-step ks for the 4 sub-tiles (logit B operand): lane (grp, col) = token
+// tok_of(st, col), coordinates 64 ks + 16 grp + [0, 16), read in the grouped layout without bounds:
+// groups past r_K read stale LDS bytes, which meet zero q~ limbs, and the lanes of the tail group are
+// replaced from the transposed tail by the caller. All reads stay below 1024 b_K bytes.
 template <int BK>
-__device__ __forceinline__ void k_frags(const uint8_t* __restrict__ ktile, const uint8_t* __restrict__ tail, int rk,
-                                        int ks, int lane, v4i (&Af)[4]) {
+__device__ __forceinline__ void k_frags(const uint8_t* __restrict__ ktile, int rk, int ks, int lane, v4i (&Bk)[4]) {
     const int col = lane & 15, grp = lane >> 4;
-    const int g16 = rk >> 4, rho = rk & 15;
     const int cg = 4 * ks + grp;
 #pragma unroll
-    for (int st = 0; st < 4; ++st) {
-        const int t = 16 * st + col;
-        v4i A = {0, 0, 0, 0};
-        if (cg < g16) A = code_frag16<BK>(ktile, rk, (cg << 10) + (t << 4));
-        else if (cg == g16 && rho) A = *reinterpret_cast<const v4i*>(tail + t * 16);
-        Af[st] = A;
-    }
+    for (int st = 0; st < 4; ++st) Bk[st] = code_frag16<BK>(ktile, rk, (cg << 10) + (tok_of(st, col) << 4));
 }
 
 // V operand fragments of N-tiles nt0 .. nt0 + 4: lane (grp, col) = coordinate 16 nt + col, tokens
-// 16 st + 4 grp + i at slot 4 st + i; coordinate 128 is the all-ones column, other coordinates >= rv zero.
+// 16 st + 4 grp + i at slot 4 st + i. Coordinates >= r_V read stale LDS bytes (below 1024 b_V bytes
+// past the tile start) into accumulator columns that are never used; N-tile 8 is the all-ones column.
 template <int BV>
-__device__ __forceinline__ void v_frags(const uint8_t* __restrict__ vtile, int rv, int nt0, int lane, v4i (&Bf)[5]) {
+__device__ __forceinline__ void v_frags(const uint8_t* __restrict__ vtile, int rv, int nt0, int lane, v4i ones,
+                                        v4i (&Bf)[5]) {
     const int col = lane & 15, grp = lane >> 4;
 #pragma unroll
     for (int k = 0; k < 5; ++k) {
-        const int coord = 16 * (nt0 + k) + col;
-        v4i B = {0, 0, 0, 0};
-        if (coord < rv) B = code_frag16<BV>(vtile, rv, (coord << 6) + (grp << 4));
-        else if (coord == kD) B = v4i{0x01010101, 0x01010101, 0x01010101, 0x01010101};
-        Bf[k] = B;
+        const int nt = nt0 + k;
+        Bf[k] = nt == kD / 16 ? ones : code_frag16<BV>(vtile, rv, ((16 * nt + col) << 6) + (grp << 4));
     }
 }
 
@@ -257,11 +259,13 @@ __global__ __launch_bounds__(64) void decode_mfma_kernel(DevSide K, DevSide V, c
                                                          const int32_t* __restrict__ qcorr,
                                                          const int32_t* __restrict__ seq_len, int max_seq, int chunk,
                                                          int n_chunks, float* __restrict__ part, int raw_bytes) {
-    constexpr int NT = Shape<G>::NT, MT = Shape<G>::MT, NV = Shape<G>::NV;
+    constexpr int LM = Shape<G>::LM, PM = Shape<G>::PM, NV = Shape<G>::NV;
     extern __shared__ float smem[];
-    float* accs = smem;                                                // [G][kAccStride] fp32: coords 0..127, 128 = sum P
-    uint8_t* tail = reinterpret_cast<uint8_t*>(smem + G * kAccStride);  // [64][16] K tail codes
-    uint4* raw = reinterpret_cast<uint4*>(tail + 64 * 16);             // raw K tile, then V tile
+    float* accs = smem;                                                   // [G][kAccStride] fp32: coords 0..127, 128 = sum P
+    float* alph = smem + G * kAccStride;                                  // [16] per-head rescale factors
+    uint8_t* pmat = reinterpret_cast<uint8_t*>(alph + 16);               // [16 PM][64] probability limbs, V slot order
+    uint8_t* tail = pmat + 16 * PM * kTile;                               // [64][16] K tail codes
+    uint4* raw = reinterpret_cast<uint4*>(tail + kTile * 16);            // raw K tile, then V tile
 
     const int u = blockIdx.y, c = blockIdx.x, lane = threadIdx.x;
     const int col = lane & 15, grp = lane >> 4;
@@ -281,189 +285,239 @@ __global__ __launch_bounds__(64) void decode_mfma_kernel(DevSide K, DevSide V, c
     const uint8_t* __restrict__ kstream = K.codes + K.code_off[u];
     const uint8_t* __restrict__ vstream = V.codes + V.code_off[u];
 
-    // Logit B operands (q~ limbs) and per-column constants.
-    v4i qB[2][NT];
-    float kcol[NT], bcol[NT];
+    // Logit A operands: lane (grp, col) = row 16 lm + col = (head 4 lm + col / 4, limb col % 4),
+    // coordinates 64 ks + 16 grp + [0, 16). The logit of (head 4 lm + grp, token) is
+    // sum_limb S_limb kq[lm][limb] + bq[lm] in the log2 domain (bq holds the centring correction).
+    v4i qA[2][LM];
+    float kq[LM][kLimbs], bq[LM];
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-        const int cc = 16 * nt + col;
-        const int limb = cc / G, g = cc % G;
-        const bool ok = cc < kLimbs * G;
-        const float ls = limb == 0 ? 1.f : (limb == 1 ? (1.f / 254.f) : (1.f / 64516.f));
-        kcol[nt] = ok ? qscale[(int64_t)u * G + g] * ls : 0.f;
-        bcol[nt] = ok ? -(float)qcorr[((int64_t)u * kLimbs + limb) * G + g] * kcol[nt] : 0.f;
+    for (int lm = 0; lm < LM; ++lm) {
+        const int h = 4 * lm + (col >> 2), limb = col & 3;
+        const bool ok = h < G && limb < kLimbs;
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
             v4i v = {0, 0, 0, 0};
             if (ok && ks < nk)
-                v = *reinterpret_cast<const v4i*>(qlimb + (((int64_t)u * kLimbs + limb) * G + g) * kD + 64 * ks + 16 * grp);
-            qB[ks][nt] = v;
+                v = *reinterpret_cast<const v4i*>(qlimb + (((int64_t)u * kLimbs + limb) * G + h) * kD + 64 * ks + 16 * grp);
+            qA[ks][lm] = v;
         }
+        const int hs = 4 * lm + grp;
+        float bsum = 0.f;
+#pragma unroll
+        for (int l = 0; l < kLimbs; ++l) {
+            const float ls = l == 0 ? 1.f : (l == 1 ? (1.f / 254.f) : (1.f / 64516.f));
+            kq[lm][l] = hs < G ? qscale[(int64_t)u * G + hs] * ls : 0.f;
+            if (hs < G) bsum = fmaf(-(float)qcorr[((int64_t)u * kLimbs + l) * G + hs], kq[lm][l], bsum);
+        }
+        bq[lm] = bsum;
     }
     for (int k = lane; k < G * kAccStride; k += 64) accs[k] = 0.f;
+    for (int k = lane; k < 16 * PM * kTile / 4; k += 64) reinterpret_cast<uint32_t*>(pmat)[k] = 0u;
     __syncthreads();
 
-    v4i Cpv[MT][NV];
+    v4i Cpv[PM][NV];
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
+    for (int pm = 0; pm < PM; ++pm)
 #pragma unroll
-        for (int nt = 0; nt < NV; ++nt) Cpv[mt][nt] = v4i{0, 0, 0, 0};
-    float m_run = -INFINITY;  // running max (log2 domain) of this lane's query head g = col % G
+        for (int nt = 0; nt < NV; ++nt) Cpv[pm][nt] = v4i{0, 0, 0, 0};
+    float m_run[LM];  // running max (log2 domain) of head 4 lm + grp
+#pragma unroll
+    for (int lm = 0; lm < LM; ++lm) m_run[lm] = -INFINITY;
 
     // When a head's running max grows (by more than 2^kLazy, so alpha <= 2^-kLazy) its int32
-    // accumulators are rescaled in place: C <- rint(C alpha). The rounding adds at most about one
-    // quantum of P per rescale, the size of one token's quantisation error; rows whose head kept
-    // its max are left untouched.
-    auto rescale = [&](float alpha_own) {
-        int lane = threadIdx.x;
-        asm volatile("" : "+v"(lane));
-        const int grp = lane >> 4;
+    // accumulator rows are rescaled in place: C <- rint(C alpha). The rounding adds at most about one
+    // quantum of P per rescale, the size of one token's quantisation error; rows of heads that kept
+    // their max are left untouched. Rare (a few tiles per chunk), so it is written for size.
+    auto rescale = [&](const float (&alpha)[LM]) {
+        int ln = threadIdx.x;
+        asm volatile("" : "+v"(ln));
+        const int gr = ln >> 4;
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
+        for (int lm = 0; lm < LM; ++lm)
+            if ((ln & 15) == 0 && 4 * lm + gr < G) alph[4 * lm + gr] = alpha[lm];
+        __syncthreads();
+#pragma unroll
+        for (int pm = 0; pm < PM; ++pm)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const int row = 16 * mt + 4 * grp + i;
-                const float alpha = __shfl(alpha_own, (lane & 48) | (row % G));
-                if (alpha != 1.f) {
+                const int row = 16 * pm + 4 * gr + i;
+                const float a = row < kLimbs * G ? alph[row % G] : 1.f;
+                const bool keep = a == 1.f;
 #pragma unroll
-                    for (int nt = 0; nt < NV; ++nt) Cpv[mt][nt][i] = (int)rintf((float)Cpv[mt][nt][i] * alpha);
+                for (int nt = 0; nt < NV; ++nt) {
+                    const int cur = Cpv[pm][nt][i];
+                    const int scaled = (int)rintf((float)cur * a);
+                    Cpv[pm][nt][i] = keep ? cur : scaled;
                 }
             }
+        __syncthreads();
     };
 
+    const v4i ones = col == 0 ? v4i{0x01010101, 0x01010101, 0x01010101, 0x01010101} : v4i{0, 0, 0, 0};
     const int kch = (8 * rk * bk) >> 4, vch = (8 * rv * bv) >> 4;  // 16-byte chunks per K / V tile
     const uint8_t* ktile = reinterpret_cast<const uint8_t*>(raw);
     const uint8_t* vtile = reinterpret_cast<const uint8_t*>(raw + kch);
+    // The packed K and V tiles are staged in LDS with coalesced 16-byte loads. The first 256 chunks
+    // of the next tile are loaded into registers while the current tile is computed; chunks past
+    // 256 (tiles of more than 4 KiB) are loaded when their tile is staged.
+    const int nch = kch + vch;
+    // Lanes past the last chunk reload chunk 0 (in bounds, cached) so that every load is unconditional.
+    auto load_chunk = [&](int tok, int cc) -> uint4 {
+        const uint4* kg = reinterpret_cast<const uint4*>(kstream + (int64_t)(tok / kTile) * 8 * rk * bk);
+        const uint4* vg = reinterpret_cast<const uint4*>(vstream + (int64_t)(tok / kTile) * 8 * rv * bv);
+        cc = cc < nch ? cc : 0;
+        return cc < kch ? kg[cc] : vg[cc - kch];
+    };
+    uint4 pf0 = load_chunk(start, lane), pf1 = load_chunk(start, 64 + lane), pf2 = load_chunk(start, 128 + lane),
+          pf3 = load_chunk(start, 192 + lane);
     for (int tok0 = start; tok0 < end; tok0 += kTile) {
         // An opaque per-tile copy of the lane id: lane-dependent fragment offsets are recomputed
         // inside the loop instead of being hoisted and kept live in registers across it.
         int lane_it = lane;
         asm volatile("" : "+v"(lane_it));
-        // Stage the packed K and V tiles in LDS: coalesced 16-byte loads, 4 chunks per lane per round.
-        {
-            const uint4* kg = reinterpret_cast<const uint4*>(kstream + (int64_t)(tok0 / kTile) * 8 * rk * bk);
-            const uint4* vg = reinterpret_cast<const uint4*>(vstream + (int64_t)(tok0 / kTile) * 8 * rv * bv);
-            const int nch = kch + vch;
-            for (int c0 = 0; c0 < nch; c0 += 256) {
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const int cc = c0 + 64 * j + lane_it;
-                    if (cc < nch) raw[cc] = cc < kch ? kg[cc] : vg[cc - kch];
-                }
-            }
-            __syncthreads();
+        const int col_it = lane_it & 15, grp_it = lane_it >> 4;
+        if (lane_it < nch) raw[lane_it] = pf0;
+        if (64 + lane_it < nch) raw[64 + lane_it] = pf1;
+        if (128 + lane_it < nch) raw[128 + lane_it] = pf2;
+        if (192 + lane_it < nch) raw[192 + lane_it] = pf3;
+        for (int c0 = 256; c0 < nch; c0 += 256) {
+            const uint4 m0 = load_chunk(tok0, c0 + lane_it), m1 = load_chunk(tok0, c0 + 64 + lane_it),
+                        m2 = load_chunk(tok0, c0 + 128 + lane_it), m3 = load_chunk(tok0, c0 + 192 + lane_it);
+            if (c0 + lane_it < nch) raw[c0 + lane_it] = m0;
+            if (c0 + 64 + lane_it < nch) raw[c0 + 64 + lane_it] = m1;
+            if (c0 + 128 + lane_it < nch) raw[c0 + 128 + lane_it] = m2;
+            if (c0 + 192 + lane_it < nch) raw[c0 + 192 + lane_it] = m3;
         }
-        // Logits: S[st] = sum over K-steps of codes (tokens x 64 coords) . q~ limbs (64 coords x columns).
+        __syncthreads();
+        if (tok0 + kTile < end) {
+            pf0 = load_chunk(tok0 + kTile, lane_it);
+            pf1 = load_chunk(tok0 + kTile, 64 + lane_it);
+            pf2 = load_chunk(tok0 + kTile, 128 + lane_it);
+            pf3 = load_chunk(tok0 + kTile, 192 + lane_it);
+        }
+        // Logits: S[lm][st] = q~ limbs (rows) . codes (64 coords x 16 tokens), summed over K-steps.
         if (rk & 15) {
             KVC_SWITCH_B(bk, k_tail<B_>(ktile, rk, tail, lane_it));
             __syncthreads();
         }
-        v4i S[4][NT];
+        v4i S[LM][4];
 #pragma unroll
-        for (int st = 0; st < 4; ++st)
+        for (int lm = 0; lm < LM; ++lm)
 #pragma unroll
-            for (int nt = 0; nt < NT; ++nt) S[st][nt] = v4i{0, 0, 0, 0};
+            for (int st = 0; st < 4; ++st) S[lm][st] = v4i{0, 0, 0, 0};
+        // All MFMAs are issued unconditionally (absent coordinates contribute zero fragments), which
+        // keeps the accumulator code straight-line.
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
-            if (ks < nk) {
-                v4i Af[4];
-                KVC_SWITCH_B(bk, k_frags<B_>(ktile, tail, rk, ks, lane_it, Af));
+            v4i Bk[4];
+            KVC_SWITCH_B(bk, k_frags<B_>(ktile, rk, ks, lane_it, Bk));
+            if ((rk & 15) && (rk >> 6) == ks) {  // this K-step holds the tail group: its lanes read the transposed copy
 #pragma unroll
-                for (int st = 0; st < 4; ++st)
-#pragma unroll
-                    for (int nt = 0; nt < NT; ++nt) S[st][nt] = mfma_i8(Af[st], qB[ks][nt], S[st][nt]);
+                for (int st = 0; st < 4; ++st) {
+                    const v4i tv = *reinterpret_cast<const v4i*>(tail + tok_of(st, col_it) * 16);
+                    if (grp_it == ((rk >> 4) & 3)) Bk[st] = tv;
+                }
             }
+#pragma unroll
+            for (int st = 0; st < 4; ++st)
+#pragma unroll
+                for (int lm = 0; lm < LM; ++lm) S[lm][st] = mfma_i8(qA[ks][lm], Bk[st], S[lm][st]);
         }
-        // Limb columns -> logits: lane (grp, col) gets tokens 16 st + 4 grp + i for head col % G (log2 domain).
-        float s[4][4];
+        // Lane (grp, col) holds the three limbs of head 4 lm + grp for token tok_of(st, col).
+        float s[LM][4];
 #pragma unroll
-        for (int st = 0; st < 4; ++st)
+        for (int lm = 0; lm < LM; ++lm)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                float v = 0.f;
-#pragma unroll
-                for (int nt = 0; nt < NT; ++nt) v += fmaf((float)S[st][nt][i], kcol[nt], bcol[nt]);
-                if (G <= 8) v += row_ror<8>(v);
-                if (G <= 4) v += row_ror<4>(v);
-                if (G <= 2) v += row_ror<2>(v);
-                if (G <= 1) v += row_ror<1>(v);
-                s[st][i] = v;
+            for (int st = 0; st < 4; ++st) {
+                float v = fmaf((float)S[lm][st][0], kq[lm][0], bq[lm]);
+                v = fmaf((float)S[lm][st][1], kq[lm][1], v);
+                s[lm][st] = fmaf((float)S[lm][st][2], kq[lm][2], v);
             }
         if (tok0 + kTile > end) {  // last tile of the chunk: tokens past the end get zero weight
 #pragma unroll
             for (int st = 0; st < 4; ++st)
+                if (tok0 + tok_of(st, col_it) >= end) {
 #pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    if (tok0 + 16 * st + 4 * (lane_it >> 4) + i >= end) s[st][i] = -INFINITY;
+                    for (int lm = 0; lm < LM; ++lm) s[lm][st] = -INFINITY;
+                }
         }
 
-        // Online softmax: running max per head; the int32 accumulators are rescaled when it grows.
-        float mt_ = s[0][0];
+        // Online softmax: running max per head over the 16 lanes of its row; the int32
+        // accumulators are rescaled when it grows past the lazy margin.
+        float alpha[LM];
+        bool grow = false;
 #pragma unroll
-        for (int st = 0; st < 4; ++st)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) mt_ = fmaxf(mt_, s[st][i]);
-        mt_ = fmaxf(mt_, __shfl_xor(mt_, 16));
-        mt_ = fmaxf(mt_, __shfl_xor(mt_, 32));
-        // lazy: keep the stale max while the tile stays within 2^kLazy of it (p <= 2^kLazy then)
-        const float m_new = mt_ > m_run + kLazy ? mt_ : m_run;
-        if (__any(m_new > m_run && m_run > -INFINITY)) rescale(m_new > m_run ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.f);
-        m_run = m_new;
+        for (int lm = 0; lm < LM; ++lm) {
+            float m = fmaxf(fmaxf(s[lm][0], s[lm][1]), fmaxf(s[lm][2], s[lm][3]));
+            m = fmaxf(m, row_ror<8>(m));
+            m = fmaxf(m, row_ror<4>(m));
+            m = fmaxf(m, row_ror<2>(m));
+            m = fmaxf(m, row_ror<1>(m));
+            // lazy: keep the stale max while the tile stays within 2^kLazy of it (p <= 2^kLazy then)
+            const float mn = m > m_run[lm] + kLazy ? m : m_run[lm];
+            alpha[lm] = mn > m_run[lm] ? __builtin_amdgcn_exp2f(m_run[lm] - mn) : 1.f;
+            grow = grow || (mn > m_run[lm] && m_run[lm] > -INFINITY);
+            m_run[lm] = mn;
+        }
+        if (__any(grow)) rescale(alpha);
 
-        // Probability limbs: P = round(p (2^21 - 1) / 2^kLazy) = L0 2^14 + L1 2^7 + L2 (p <= 2^kLazy);
-        // lane row 16 mt + col holds limb row / G.
-        uint32_t Pq[4][4];
+        // Probability limbs: P = round(p (2^21 - 1) / 2^kLazy) = L0 2^14 + L1 2^7 + L2 (p <= 2^kLazy).
+        // Row limb * G + h of pmat, bytes 4 col .. 4 col + 3 = tokens tok_of(0..3, col).
 #pragma unroll
-        for (int st = 0; st < 4; ++st)
+        for (int lm = 0; lm < LM; ++lm) {
+            const int h = 4 * lm + grp_it;
+            uint32_t P[4];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) Pq[st][i] = (uint32_t)fmaf(__builtin_amdgcn_exp2f(s[st][i] - m_run), kPScale, 0.5f);
-        v4i Ap[MT];
+            for (int st = 0; st < 4; ++st)
+                P[st] = (uint32_t)fmaf(__builtin_amdgcn_exp2f(s[lm][st] - m_run[lm]), kPScale, 0.5f);
+            if (G >= 4 * (lm + 1) || h < G) {
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-            const int row = 16 * mt + col;
-            const int plimb = row / G;
-            const uint32_t shift = 14 - 7 * plimb;
-            const uint32_t keep = plimb < kLimbs ? 0x7fu : 0u;
+                for (int l = 0; l < kLimbs; ++l) {
+                    const uint32_t sh = 14 - 7 * l;
+                    uint32_t w = (P[0] >> sh) & 0x7fu;
 #pragma unroll
-            for (int st = 0; st < 4; ++st) {
-                uint32_t w = 0;
-#pragma unroll
-                for (int i = 0; i < 4; ++i) w |= ((Pq[st][i] >> shift) & keep) << (8 * i);
-                Ap[mt][st] = (int)w;
+                    for (int st = 1; st < 4; ++st) w |= ((P[st] >> sh) & 0x7fu) << (8 * st);
+                    *reinterpret_cast<uint32_t*>(pmat + (l * G + h) * kTile + 4 * col_it) = w;
+                }
             }
         }
+        __syncthreads();
+        v4i Ap[PM];
+#pragma unroll
+        for (int pm = 0; pm < PM; ++pm)
+            Ap[pm] = *reinterpret_cast<const v4i*>(pmat + (16 * pm + col_it) * kTile + 16 * grp_it);
 
-        // PV: Cpv[mt][nt] += P limbs (rows x 64 tokens) . V codes (64 tokens x 16 coords).
+        // PV: Cpv[pm][nt] += P limbs (rows x 64 tokens) . V codes (64 tokens x 16 coords).
 #pragma unroll
         for (int half = 0; half < 2; ++half) {
             const int nt0 = 5 * half;
             v4i Bf[5];
-            KVC_SWITCH_B(bv, v_frags<B_>(vtile, rv, nt0, lane_it, Bf));
+            KVC_SWITCH_B(bv, v_frags<B_>(vtile, rv, nt0, lane_it, ones, Bf));
 #pragma unroll
             for (int k = 0; k < 5; ++k)
-                if (nt0 + k < NV && (nt0 + k < nv || nt0 + k == NV - 1))
+                if (nt0 + k < NV)
 #pragma unroll
-                    for (int mt = 0; mt < MT; ++mt) Cpv[mt][nt0 + k] = mfma_i8(Ap[mt], Bf[k], Cpv[mt][nt0 + k]);
+                    for (int pm = 0; pm < PM; ++pm) Cpv[pm][nt0 + k] = mfma_i8(Ap[pm], Bf[k], Cpv[pm][nt0 + k]);
         }
-        __syncthreads();  // raw is restaged by the next tile
+        __syncthreads();  // raw and pmat are rewritten by the next tile
     }
     // Centre (exact, in integers, with the all-ones column O) and combine the three P limbs of each
     // head into the fp32 LDS accumulator: accs[g][c] = sum_limb ls (C - 2^(b-1) O), accs[g][128] = sum_limb ls O.
     {
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
+        for (int pm = 0; pm < PM; ++pm)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const int row = 16 * mt + 4 * grp + i;
+                const int row = 16 * pm + 4 * grp + i;
                 const int plimb = row / G, g = row - plimb * G;
-                const int O = __shfl(Cpv[mt][NV - 1][i], lane & 48);
+                const int O = __shfl(Cpv[pm][NV - 1][i], lane & 48);
                 const float ls = plimb == 0 ? 16384.f : (plimb == 1 ? 128.f : 1.f);
                 float* arow = accs + g * kAccStride;
                 if (plimb < kLimbs) {
 #pragma unroll
                     for (int nt = 0; nt < NV - 1; ++nt) {
                         const int coord = 16 * nt + col;
-                        if (nt < nv && coord < rv) atomicAdd(arow + coord, (float)(Cpv[mt][nt][i] - hv * O) * ls);
+                        if (nt < nv && coord < rv) atomicAdd(arow + coord, (float)(Cpv[pm][nt][i] - hv * O) * ls);
                     }
                     if (col == 0) atomicAdd(arow + kD, (float)O * ls);
                 }
@@ -474,7 +528,7 @@ __global__ __launch_bounds__(64) void decode_mfma_kernel(DevSide K, DevSide V, c
     // Partial of each head: m, l = sum of P (all-ones column), centred accumulator.
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-        const float mg = __shfl(m_run, g);
+        const float mg = __shfl(m_run[g / 4], 16 * (g % 4));
         float* o = out + g * kPartStride;
         const float* arow = accs + g * kAccStride;
         if (lane == 0) { o[0] = mg; o[1] = arow[kD]; }
@@ -562,7 +616,7 @@ template <int G>
 int launch_partials(dim3 grid, hipStream_t st, const DevSide& K, const DevSide& V, const int8_t* ql, const float* qs,
                     const int32_t* qc, const int32_t* seq_len, int max_seq, int chunk, int n_chunks, float* part,
                     int raw_bytes) {
-    const size_t smem = (size_t)G * kAccStride * 4 + 64 * 16 + (size_t)raw_bytes;
+    const size_t smem = (size_t)G * kAccStride * 4 + 16 * 4 + (size_t)16 * Shape<G>::PM * kTile + kTile * 16 + (size_t)raw_bytes;
     if (smem > 64 * 1024) {
         const hipError_t e = hipFuncSetAttribute((const void*)decode_mfma_kernel<G>,
                                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
@@ -607,7 +661,9 @@ extern "C" int kvc_decode_attn(const kvc_stream_desc* k, const kvc_stream_desc* 
     hipLaunchKernelGGL(qprep_kernel, dim3(U), dim3(kD), 0, st, K, q, G, ql, qs, qc);
     int raw_bytes = 16;
     for (int u = 0; u < U; ++u) {
-        const int tb = 8 * k->r_host[u] * k->b_host[u] + 8 * v->r_host[u] * v->b_host[u];
+        // fragment reads run past the staged tiles (up to 1024 b bytes from each tile start)
+        const int kb = 8 * k->r_host[u] * k->b_host[u];
+        const int tb = std::max(1024 * k->b_host[u], kb + 1024 * v->b_host[u]);
         raw_bytes = tb > raw_bytes ? tb : raw_bytes;
     }
     const dim3 grid(L.n_chunks, U);
