@@ -177,6 +177,104 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(DevSide s, int side
     }
 }
 
+// ---------------------------------------------------------------- append
+
+// Appending a few tokens (a decode step adds one per unit): one block per unit, thread i
+// computes coordinate i of every new token from its basis row, decides the code as
+// encode_kernel does, and the new codes are merged into the packed words of their tiles.
+constexpr int kAppThreads = kD;
+constexpr int kAppMaxTok = 4;
+
+__global__ __launch_bounds__(kAppThreads) void append_kernel(DevSide s, int side, const uint16_t* __restrict__ x,
+                                                             int64_t x_stride, int t0, int n_tok) {
+    __shared__ float xs[kAppMaxTok][kD];
+    __shared__ float red[kAppMaxTok][kAppThreads / 64];
+    __shared__ uint8_t cs[kAppMaxTok][kD];
+    const int u = blockIdx.x, i = threadIdx.x;
+    const int r = s.r[u], b = s.b[u];
+    const float step = s.delta[u];
+    const uint16_t* __restrict__ P = s.basis + s.basis_off[u];
+    const uint16_t* __restrict__ xu = x + (int64_t)u * x_stride;
+    for (int t = 0; t < n_tok; ++t) {
+        const float v = h2f(xu[(int64_t)t * kD + i]);
+        xs[t][i] = v;
+        float s2 = v * v;
+        for (int o = 32; o > 0; o >>= 1) s2 += __shfl_xor(s2, o);
+        if ((i & 63) == 0) red[t][i >> 6] = s2;
+    }
+    __syncthreads();
+    if (i < r) {
+        float acc[kAppMaxTok] = {0.f, 0.f, 0.f, 0.f};
+        float pn2 = 0.f;
+        const uint4* Pr = reinterpret_cast<const uint4*>(P + (int64_t)i * kD);
+#pragma unroll 4
+        for (int q = 0; q < kD / 8; ++q) {
+            const uint4 w = Pr[q];
+            const uint32_t w4[4] = {w.x, w.y, w.z, w.w};
+            float pv[8];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                pv[2 * e] = h2f((uint16_t)(w4[e] & 0xffff));
+                pv[2 * e + 1] = h2f((uint16_t)(w4[e] >> 16));
+            }
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                pn2 = fmaf(pv[e], pv[e], pn2);
+#pragma unroll
+                for (int t = 0; t < kAppMaxTok; ++t)
+                    if (t < n_tok) acc[t] = fmaf(pv[e], xs[t][8 * q + e], acc[t]);
+            }
+        }
+        const float pn = sqrtf(pn2);
+#pragma unroll
+        for (int t = 0; t < kAppMaxTok; ++t)
+            if (t < n_tok) {
+                // same bound as encode_kernel: |acc - y| <= 2^-17 ||P_i|| ||x||, used with a 4x margin
+                const float xn = sqrtf(red[t][0] + red[t][1]);
+                cs[t][i] = (uint8_t)decide_code(acc[t], 0x1p-15f * pn * xn, step, b, P + (int64_t)i * kD,
+                                                xu + (int64_t)t * kD);
+            }
+    }
+    __syncthreads();
+    if (i >= r) return;
+    // Merge: thread (t, i) visits the word holding slot (t, i) in each plane. The word's first slot
+    // that belongs to a new token elects one thread per word, which rewrites the new tokens' bits
+    // of that word and keeps every other bit.
+    uint8_t* __restrict__ stream = s.codes + s.code_off[u];
+    for (int t = 0; t < n_tok; ++t) {
+        const int tok = t0 + t, tile = tok / kTile, tt = tok % kTile;
+        const int phi = side == KVC_SIDE_K ? slot_k(tt, i, r) : slot_v(tt, i);
+        uint8_t* __restrict__ tbase = stream + (int64_t)tile * 8 * r * b;
+        for (int p = 8; p >= 1; p >>= 1) {
+            if (b == 8 ? p != 8 : (p == 8 || !(b & p))) continue;
+            const int sh = b == 8 ? 0 : (b & (p - 1));
+            const int off = b == 8 ? 0 : (b & ~(2 * p - 1));
+            const int ppw = 32 / p;
+            const uint32_t vmask = p == 8 ? 0xffu : ((1u << p) - 1u);
+            const int lw = phi / ppw;
+            uint32_t val = 0, msk = 0;
+            bool first = true, leader = false;
+            for (int iota = 0; iota < ppw; ++iota) {
+                const int ph = lw * ppw + iota;
+                int t2, i2;
+                if (side == KVC_SIDE_K) unslot_k(ph, r, t2, i2);
+                else { i2 = ph >> 6; t2 = psi(ph & 63); }
+                const int tk = tile * kTile + t2 - t0;
+                if (tk >= 0 && tk < n_tok) {
+                    if (first) { leader = tk == t && i2 == i; first = false; }
+                    const int bit = 8 * (iota & 3) + p * (iota >> 2);
+                    val |= ((uint32_t)(cs[tk][i2] >> sh) & vmask) << bit;
+                    msk |= vmask << bit;
+                }
+            }
+            if (leader) {
+                uint32_t* wp = reinterpret_cast<uint32_t*>(tbase + 8 * r * off) + lw;
+                *wp = (*wp & ~msk) | val;
+            }
+        }
+    }
+}
+
 // ---------------------------------------------------------------- reconstruct
 
 constexpr int kRecThreads = 256;
@@ -247,6 +345,11 @@ extern "C" int kvc_encode(const kvc_stream_desc* s, const uint16_t* x, int64_t x
     if (n_tok == 0 || s->n_units == 0) return KVC_OK;
     if (!x || (reinterpret_cast<uintptr_t>(x) & 15) || (x_unit_stride & 7) || x_unit_stride < (int64_t)n_tok * kD)
         return set_error(KVC_EINVAL, "kvc_encode: x must be 16-byte aligned with stride a multiple of 8 and >= n_tok*d");
+    if (n_tok <= kAppMaxTok) {
+        hipLaunchKernelGGL(append_kernel, dim3(s->n_units), dim3(kAppThreads), 0, (hipStream_t)stream, dev_side(s),
+                           s->side, x, x_unit_stride, t0, n_tok);
+        return check_launch("kvc_encode");
+    }
     const int tile_first = t0 / kTile;
     const int tile_last = (t0 + n_tok - 1) / kTile;
     const size_t smem = (size_t)max_r(s) * kD * 4 + kD * 4 + kTile * kD;

@@ -240,6 +240,36 @@ def test_encode_every_rank_and_width(side):
         assert np.array_equal(got, exp), (r, b, int(np.sum(got != exp)))
 
 
+@pytest.mark.parametrize("side", [kvc.SIDE_K, kvc.SIDE_V])
+def test_append_few_tokens_every_rank_and_width(side):
+    # appends of 1..4 tokens (the decode-step path) across a tile boundary equal the oracle's stream
+    rng = np.random.default_rng(20 + side)
+    combos = [(r, b) for b in range(1, 9) for r in (2, 6, 16, 18, 34, 62, 96, 126, 128)]
+    Ps, ds, rs, bs = [], [], [], []
+    for r, b in combos:
+        Q, _ = np.linalg.qr(rng.standard_normal((128, 128)))
+        Ps.append(Q[:r].astype(np.float16).view(np.uint16))
+        ds.append(np.float32(rng.uniform(0.3, 1.2) * 1.596 / 2 ** (b - 1)))
+        rs.append(r)
+        bs.append(b)
+    T = 75
+    S = _custom_side(side, Ps, np.array(ds, np.float32), rs, bs, T)
+    x = (rng.standard_normal((len(combos), T, 128)) * rng.uniform(0.1, 4, (len(combos), 1, 1))).astype(np.float16)
+    xt = torch.as_tensor(x.view(np.int16), device="cuda").view(torch.float16)
+    log(f"[append] side={side} units={len(combos)}")
+    a, k = 0, 0
+    while a < T:
+        n = min(1 + k % 4, T - a)
+        kvc.kvc_encode(S, xt[:, a:a + n].contiguous(), a, n)
+        a, k = a + n, k + 1
+    torch.cuda.synchronize()
+    for u, (r, b) in enumerate(combos):
+        codes = onat.encode_codes(Ps[u], ds[u], b, x[u].view(np.uint16))
+        exp = onat.pack(codes, r, b, side)
+        got = S.unit_codes(u, T).cpu().numpy()
+        assert np.array_equal(got, exp), (r, b, int(np.sum(got != exp)))
+
+
 def test_encode_exact_thresholds_and_subnormals():
     # dyadic basis, power-of-two step and dyadic inputs put many projections exactly on
     # quantizer thresholds: the fp32 path cannot decide them, the exact path must
@@ -253,11 +283,17 @@ def test_encode_exact_thresholds_and_subnormals():
     S = _custom_side(kvc.SIDE_K, [P.view(np.uint16)], np.array([step]), [r], [b], T)
     xt = torch.as_tensor(x.view(np.int16), device="cuda").view(torch.float16)
     kvc.kvc_encode(S, xt, 0, T)
+    S1 = _custom_side(kvc.SIDE_K, [P.view(np.uint16)], np.array([step]), [r], [b], T)
+    for a in range(0, T, 3):  # the few-token append path decides the same ties
+        n = min(3, T - a)
+        kvc.kvc_encode(S1, xt[:, a:a + n].contiguous(), a, n)
     torch.cuda.synchronize()
     codes = onat.encode_codes(P.view(np.uint16), step, b, x[0].view(np.uint16))
     y = x[0].astype(np.float64) @ P.astype(np.float64).T
     assert np.mean(np.abs(y / 0.25 - np.round(y / 0.25)) < 1e-12) > 0.05     # many exact ties exercised
-    assert np.array_equal(S.unit_codes(0, T).cpu().numpy(), onat.pack(codes, r, b, kvc.SIDE_K))
+    exp = onat.pack(codes, r, b, kvc.SIDE_K)
+    assert np.array_equal(S.unit_codes(0, T).cpu().numpy(), exp)
+    assert np.array_equal(S1.unit_codes(0, T).cpu().numpy(), exp)
 
 
 def test_invalid_arguments_raise_before_launch(small):
