@@ -47,7 +47,7 @@ def decode_alg_bytes(cache, n_tok: int) -> int:
 
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
-    for f in ("kvc_kernels.hip", "kvc_device.h"):
+    for f in ("kvc_kernels.hip", "kvc_decode.hip", "kvc_device.h"):
         with open(os.path.join(ROOT, "paper_2609_24298_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -135,6 +135,9 @@ def main():
     ap.add_argument("--workload", default="llama8b_b8_t32k_2bpd")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calib", action="store_true",
+                    help="after the timed region, run one plain 1 GiB device-to-device copy (the reference kernel "
+                         "for scaling HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU (asked for {args.gpus}); the multi-GPU path is not part of "
@@ -231,6 +234,15 @@ def main():
         "encode": {"vectors_per_s": round(enc_vectors / t_enc, 1), "model_tokens_per_s": round(w.batch * T / t_enc, 1),
                    "ms": round(t_enc * 1e3, 3), "hbm_read_GBs": round(enc_read / t_enc / 1e9, 2)},
     }
+    if args.copy_calib:
+        n = 1 << 30
+        src = torch.ones(n, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"copy calibration: {n} bytes read and written")
+        del src, dst
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle) ...")
         try:

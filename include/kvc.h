@@ -187,7 +187,7 @@ int kvc_encode(const kvc_stream_desc* s, const uint16_t* x, int64_t x_unit_strid
 /*
  * kvc_decode_attn - one decode step of attention over the compressed cache.
  * Paper: table step 8 (dequantize on read); Section 4 (logits <q,k>/sqrt(d),
- * softmax); Appendix H "Wall-clock at the primitive level" (dequantize and
+ * softmax); Appendix I "Wall-clock at the primitive level" (dequantize and
  * undo the rotation in one fused pass).
  *
  *  k, v         descriptors of the K and V sides; same n_units, unit u pairs.

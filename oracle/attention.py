@@ -10,7 +10,7 @@ Passages followed
   x_hat = P^T z_hat with z_hat the dequantized codes.
 * Section 4: logits s_t = <q, k_t> / sqrt(d) with d the head dimension, and
   p = softmax(s).
-* Appendix H, "Wall-clock at the primitive level": the decode primitive
+* Appendix I, "Wall-clock at the primitive level": the decode primitive
   dequantizes and applies the inverse rotation in one pass. Since
   <q, P^T z> = <P q, z>, the logits are taken in the rank-r space here, and
   the value output is P_V^T (sum_t p_t z_V,t); both equal the dense

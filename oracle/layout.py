@@ -3,7 +3,7 @@
 Test infrastructure only: nothing in the product path may import this module.
 
 The paper stores r codes of b bits per token per head with no per-token
-metadata, i.e. exactly r*b/d bits per dimension (Appendix G, the paragraph on
+metadata, i.e. exactly r*b/d bits per dimension (Appendix E, the paragraph on
 the rotation-based methods), and dequantizes on the attention read (table step
 8). It leaves the byte layout open; the layout below is this implementation's
 definition, and the oracle packs to it independently of the GPU encoder.

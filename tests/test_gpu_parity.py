@@ -124,10 +124,13 @@ def test_small_decode_attention_parity(small, qscale):
     cache.decode(q, torch.as_tensor(seq, device="cuda"), w.tokens, out, ws)
     got = out.cpu().numpy()
     ref = _oracle_decode(w, ot, cache, xk, xv, q, seq)
+    worst = 0.0
     for u in range(w.n_units):
         for g in range(w.group):
             e = normwise(got[u, g], ref[u, g])
+            worst = max(worst, e)
             assert e <= TOL, (u, g, e)
+    log(f"[small] decode qscale={qscale}: max normwise error {worst:.2e}")
 
 
 def test_small_decode_ragged_lengths(small):

@@ -121,7 +121,7 @@ def test_pack_c_matches_python_and_round_trips(side, b):
 
 
 def test_storage_is_exactly_rb_over_d_bits_per_dimension():
-    # Appendix G: r*b/d bits per dimension, no per-token metadata (whole tiles)
+    # Appendix E: r*b/d bits per dimension, no per-token metadata (whole tiles)
     for r in (2, 16, 100, 128):
         for b in range(1, 9):
             n = 64 * 7
