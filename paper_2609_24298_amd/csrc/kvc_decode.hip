@@ -152,11 +152,25 @@ __global__ __launch_bounds__(kD) void qprep_kernel(DevSide K, const uint16_t* __
     const int r = K.r[u], b = K.b[u];
     const int hk = b == 8 ? 0 : (1 << (b - 1));
     const float scale0 = K.delta[u] * 1.4426950408889634f * 0.08838834764831845f;  // log2(e) / sqrt(128)
-    const uint16_t* __restrict__ P = K.basis + K.basis_off[u] + (int64_t)i * kD;
+    // basis row i, read once with 16-byte loads
+    float prow[kD];
+    {
+        const uint4* P4 = reinterpret_cast<const uint4*>(K.basis + K.basis_off[u] + (int64_t)(i < r ? i : 0) * kD);
+#pragma unroll
+        for (int c = 0; c < kD / 8; ++c) {
+            const uint4 w = P4[c];
+            const uint32_t w4[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                prow[8 * c + 2 * e] = i < r ? h2f((uint16_t)(w4[e] & 0xffff)) : 0.f;
+                prow[8 * c + 2 * e + 1] = i < r ? h2f((uint16_t)(w4[e] >> 16)) : 0.f;
+            }
+        }
+    }
     for (int g = 0; g < G; ++g) {
         float acc = 0.f;
-        if (i < r)
-            for (int j = 0; j < kD; ++j) acc = fmaf(h2f(P[j]), qsh[g][j], acc);
+#pragma unroll
+        for (int j = 0; j < kD; ++j) acc = fmaf(prow[j], qsh[g][j], acc);
         const float qt = acc * scale0;
         float m = fabsf(qt);
         for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
@@ -191,6 +205,8 @@ template <int G> struct Shape {
     static constexpr int LM = (4 * G + 15) / 16;       // logit M-tiles: row 4 h + limb (limb 3 is zero)
     static constexpr int PM = (kLimbs * G + 15) / 16;  // PV M-tiles: row limb * G + h
     static constexpr int NV = kD / 16 + 1;             // V N-tiles incl. the all-ones coordinate
+    // Wavefronts per SIMD the register budget is cut for (512 / W registers per lane, no spills).
+    static constexpr int W = G == 1 || G == 4 ? 4 : (G == 2 ? 3 : (G == 8 ? 2 : 1));
 };
 
 // Token of logit column col in sub-tile st. With this order a lane's four tokens (st = 0..3) sit at
@@ -254,7 +270,7 @@ __device__ __forceinline__ void v_frags(const uint8_t* __restrict__ vtile, int r
     }
 
 template <int G>
-__global__ __launch_bounds__(64) void decode_mfma_kernel(DevSide K, DevSide V, const int8_t* __restrict__ qlimb,
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(Shape<G>::W, Shape<G>::W))) void decode_mfma_kernel(DevSide K, DevSide V, const int8_t* __restrict__ qlimb,
                                                          const float* __restrict__ qscale,
                                                          const int32_t* __restrict__ qcorr,
                                                          const int32_t* __restrict__ seq_len, int max_seq, int chunk,
@@ -357,43 +373,44 @@ __global__ __launch_bounds__(64) void decode_mfma_kernel(DevSide K, DevSide V, c
     const int kch = (8 * rk * bk) >> 4, vch = (8 * rv * bv) >> 4;  // 16-byte chunks per K / V tile
     const uint8_t* ktile = reinterpret_cast<const uint8_t*>(raw);
     const uint8_t* vtile = reinterpret_cast<const uint8_t*>(raw + kch);
-    // The packed K and V tiles are staged in LDS with coalesced 16-byte loads. The first 256 chunks
-    // of the next tile are loaded into registers while the current tile is computed; chunks past
-    // 256 (tiles of more than 4 KiB) are loaded when their tile is staged.
+    // The packed K and V tiles are staged in LDS with coalesced 16-byte loads: chunk cc < kch of
+    // the K tile, then the V tile's, 64 chunks per round. The first 4 rounds of the next tile are
+    // loaded into registers while the current tile is computed; further rounds (tiles of more than
+    // 4 KiB) are loaded when their tile is staged. Lanes past the last chunk reload the V tile's last.
     const int nch = kch + vch;
-    // Lanes past the last chunk reload chunk 0 (in bounds, cached) so that every load is unconditional.
-    auto load_chunk = [&](int tok, int cc) -> uint4 {
-        const uint4* kg = reinterpret_cast<const uint4*>(kstream + (int64_t)(tok / kTile) * 8 * rk * bk);
-        const uint4* vg = reinterpret_cast<const uint4*>(vstream + (int64_t)(tok / kTile) * 8 * rv * bv);
-        cc = cc < nch ? cc : 0;
-        return cc < kch ? kg[cc] : vg[cc - kch];
+    const int64_t ktb = 8 * rk * bk, vtb = 8 * rv * bv;  // tile bytes
+    auto chunk_src = [&](int tile, int cc) -> const uint4* {
+        const uint4* kb = reinterpret_cast<const uint4*>(kstream + tile * ktb);
+        const uint4* vb = reinterpret_cast<const uint4*>(vstream + tile * vtb) - kch;
+        return (cc < kch ? kb : vb) + min(cc, nch - 1);
     };
-    uint4 pf0 = load_chunk(start, lane), pf1 = load_chunk(start, 64 + lane), pf2 = load_chunk(start, 128 + lane),
-          pf3 = load_chunk(start, 192 + lane);
+    uint4 pf0, pf1, pf2, pf3;
+    {
+        const int tile = start / kTile;
+        pf0 = *chunk_src(tile, lane);
+        pf1 = *chunk_src(tile, 64 + lane);
+        pf2 = *chunk_src(tile, 128 + lane);
+        pf3 = *chunk_src(tile, 192 + lane);
+    }
     for (int tok0 = start; tok0 < end; tok0 += kTile) {
         // An opaque per-tile copy of the lane id: lane-dependent fragment offsets are recomputed
         // inside the loop instead of being hoisted and kept live in registers across it.
         int lane_it = lane;
         asm volatile("" : "+v"(lane_it));
         const int col_it = lane_it & 15, grp_it = lane_it >> 4;
+        const int tile = tok0 / kTile;
         if (lane_it < nch) raw[lane_it] = pf0;
         if (64 + lane_it < nch) raw[64 + lane_it] = pf1;
         if (128 + lane_it < nch) raw[128 + lane_it] = pf2;
         if (192 + lane_it < nch) raw[192 + lane_it] = pf3;
-        for (int c0 = 256; c0 < nch; c0 += 256) {
-            const uint4 m0 = load_chunk(tok0, c0 + lane_it), m1 = load_chunk(tok0, c0 + 64 + lane_it),
-                        m2 = load_chunk(tok0, c0 + 128 + lane_it), m3 = load_chunk(tok0, c0 + 192 + lane_it);
-            if (c0 + lane_it < nch) raw[c0 + lane_it] = m0;
-            if (c0 + 64 + lane_it < nch) raw[c0 + 64 + lane_it] = m1;
-            if (c0 + 128 + lane_it < nch) raw[c0 + 128 + lane_it] = m2;
-            if (c0 + 192 + lane_it < nch) raw[c0 + 192 + lane_it] = m3;
-        }
+        for (int c0 = 256; c0 < nch; c0 += 64)
+            if (c0 + lane_it < nch) raw[c0 + lane_it] = *chunk_src(tile, c0 + lane_it);
         __syncthreads();
         if (tok0 + kTile < end) {
-            pf0 = load_chunk(tok0 + kTile, lane_it);
-            pf1 = load_chunk(tok0 + kTile, 64 + lane_it);
-            pf2 = load_chunk(tok0 + kTile, 128 + lane_it);
-            pf3 = load_chunk(tok0 + kTile, 192 + lane_it);
+            pf0 = *chunk_src(tile + 1, lane_it);
+            pf1 = *chunk_src(tile + 1, 64 + lane_it);
+            pf2 = *chunk_src(tile + 1, 128 + lane_it);
+            pf3 = *chunk_src(tile + 1, 192 + lane_it);
         }
         // Logits: S[lm][st] = q~ limbs (rows) . codes (64 coords x 16 tokens), summed over K-steps.
         if (rk & 15) {
@@ -541,13 +558,15 @@ __global__ __launch_bounds__(64) void decode_mfma_kernel(DevSide K, DevSide V, c
 
 __global__ __launch_bounds__(kD) void combine_kernel(DevSide V, int G, int n_chunks, const float* __restrict__ part,
                                                      float* __restrict__ out) {
-    __shared__ float zs[kD];
+    constexpr int kMaxG = 16;
+    __shared__ float zs[kMaxG][kD];
+    __shared__ float lsum[kMaxG];
     const int u = blockIdx.x, j = threadIdx.x;
     const int rv = V.r[u];
     const float step = V.delta[u];
-    const uint16_t* __restrict__ P = V.basis + V.basis_off[u];
+    const float* __restrict__ pu = part + (int64_t)u * n_chunks * G * kPartStride;
     for (int g = 0; g < G; ++g) {
-        const float* pg = part + (int64_t)u * n_chunks * G * kPartStride + g * kPartStride;
+        const float* pg = pu + g * kPartStride;
         float M = -INFINITY;
         for (int c = 0; c < n_chunks; ++c) M = fmaxf(M, pg[(int64_t)c * G * kPartStride]);
         float L = 0.f, A = 0.f;
@@ -560,36 +579,120 @@ __global__ __launch_bounds__(kD) void combine_kernel(DevSide V, int G, int n_chu
                 if (j < rv) A = fmaf(pc[4 + j], w, A);
             }
         }
-        if (j < rv) zs[j] = L > 0.f ? step * (A / L + 0.5f) : 0.f;
-        __syncthreads();
-        float o = 0.f;
-        for (int i = 0; i < rv; ++i) o = fmaf(h2f(P[(int64_t)i * kD + j]), zs[i], o);
-        out[((int64_t)u * G + g) * kD + j] = L > 0.f ? o : 0.f;
-        __syncthreads();
+        zs[g][j] = (L > 0.f && j < rv) ? step * (A / L + 0.5f) : 0.f;
+        if (j == 0) lsum[g] = L;
     }
+    __syncthreads();
+    // o_g = P_V^T z_g for every head in one pass over the basis (coalesced rows of P)
+    const uint16_t* __restrict__ P = V.basis + V.basis_off[u];
+    float o[kMaxG];
+#pragma unroll
+    for (int g = 0; g < kMaxG; ++g) o[g] = 0.f;
+    for (int i = 0; i < rv; ++i) {
+        const float p = h2f(P[(int64_t)i * kD + j]);
+#pragma unroll
+        for (int g = 0; g < kMaxG; ++g)
+            if (g < G) o[g] = fmaf(p, zs[g][i], o[g]);
+    }
+#pragma unroll
+    for (int g = 0; g < kMaxG; ++g)
+        if (g < G) out[((int64_t)u * G + g) * kD + j] = lsum[g] > 0.f ? o[g] : 0.f;
 }
 
 // ---------------------------------------------------------------- host side
 
 namespace {
 
-// Context chunk per work item: a power of two >= 64 giving about 4096 items.
-int choose_chunk(int n_units, int max_seq) {
-    const int64_t tokens = (int64_t)n_units * max_seq;
-    int64_t c = 64;
-    while (c < 4096 && tokens / (c * 2) >= 4096) c *= 2;
-    return (int)c;
+// Raw LDS bytes for the staged tiles: fragment reads run past the staged tiles (up to 1024 b bytes
+// from each tile start), so the region covers max(1024 b_K, 8 r_K b_K + 1024 b_V) over the units.
+int raw_tile_bytes(const kvc_stream_desc* k, const kvc_stream_desc* v) {
+    int raw = 16;
+    for (int u = 0; u < k->n_units; ++u) {
+        const int kb = 8 * k->r_host[u] * k->b_host[u];
+        raw = std::max(raw, std::max(1024 * k->b_host[u], kb + 1024 * v->b_host[u]));
+    }
+    return raw;
 }
 
+size_t partial_smem(int G, int raw_bytes) {
+    const int PM = (kLimbs * G + 15) / 16;
+    return (size_t)G * kAccStride * 4 + 16 * 4 + (size_t)16 * PM * kTile + kTile * 16 + (size_t)raw_bytes;
+}
+
+template <int G>
+int resident_blocks(size_t smem) {
+    int nb = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, decode_mfma_kernel<G>, 64, smem) != hipSuccess || nb <= 0) {
+        (void)hipGetLastError();
+        nb = 8;
+    }
+    return nb;
+}
+
+// Work items (wavefronts) the device holds at once for this launch; without a device, the
+// MI355X figures (256 CUs, 8 resident wavefronts each).
+int64_t resident_slots(int G, size_t smem) {
+    int dev = 0, ncu = 0;
+    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        ncu <= 0) {
+        (void)hipGetLastError();
+        ncu = 256;
+    }
+    int nb;
+    switch (G) {
+        case 1: nb = resident_blocks<1>(smem); break;
+        case 2: nb = resident_blocks<2>(smem); break;
+        case 4: nb = resident_blocks<4>(smem); break;
+        case 8: nb = resident_blocks<8>(smem); break;
+        default: nb = resident_blocks<16>(smem); break;
+    }
+    return (int64_t)ncu * nb;
+}
+
+// Split of each unit's context into n_chunks equal chunks of whole tiles. Among counts that give
+// at least one work item per resident slot, the count minimises
+//   rounds x (tiles per item + per-item overhead) + (straggler share) x tiles per item,
+// rounds = ceil(items / resident slots): whole rounds with no short remainder, and items short
+// enough that units of different cost even out (measured on the 32-layer 32k-token workload:
+// 9 chunks of 57 tiles beat 3 chunks of 171 by 11 % and 24 chunks of 22 by 12 %).
+constexpr int kItemOverheadTiles = 4;
+constexpr double kStragglerShare = 0.5;
+
 struct WsLayout {
-    int chunk, n_chunks;
+    int chunk, n_chunks, raw_bytes;
     int64_t qlimb, qscale, qcorr, part, total;  // byte offsets
 };
 
-WsLayout ws_layout(int U, int G, int max_seq) {
+WsLayout ws_layout(const kvc_stream_desc* k, const kvc_stream_desc* v, int G, int max_seq) {
     WsLayout L;
-    L.chunk = choose_chunk(U, max_seq);
-    L.n_chunks = (max_seq + L.chunk - 1) / L.chunk;
+    const int U = k->n_units;
+    L.raw_bytes = raw_tile_bytes(k, v);
+    const int64_t slots = resident_slots(G, partial_smem(G, L.raw_bytes));
+    const int tpu = (max_seq + kTile - 1) / kTile;
+    // Candidates that fill every resident slot rank by cost; if none can (few units, short
+    // contexts), the one with the most items wins.
+    bool best_full = false;
+    double best_cost = 0.0;
+    int64_t best_items = -1;
+    L.chunk = tpu * kTile;
+    L.n_chunks = 1;
+    for (int n = 1; n <= tpu && n <= 1024; ++n) {
+        const int c = (tpu + n - 1) / n;
+        if ((tpu + c - 1) / c != n) continue;
+        const int64_t items = (int64_t)U * n;
+        const bool full = items >= slots;
+        const int64_t rounds = (items + slots - 1) / slots;
+        const double cost = (double)rounds * (c + kItemOverheadTiles) + kStragglerShare * c;
+        const bool better = best_items < 0 || (full && !best_full) ||
+                            (full && best_full && cost < best_cost) || (!full && !best_full && items > best_items);
+        if (better) {
+            best_full = full;
+            best_cost = cost;
+            best_items = items;
+            L.chunk = c * kTile;
+            L.n_chunks = n;
+        }
+    }
     auto up = [](int64_t x) { return (x + 255) / 256 * 256; };
     L.qlimb = 0;
     L.qscale = up(L.qlimb + (int64_t)U * kLimbs * G * kD);
@@ -616,7 +719,7 @@ template <int G>
 int launch_partials(dim3 grid, hipStream_t st, const DevSide& K, const DevSide& V, const int8_t* ql, const float* qs,
                     const int32_t* qc, const int32_t* seq_len, int max_seq, int chunk, int n_chunks, float* part,
                     int raw_bytes) {
-    const size_t smem = (size_t)G * kAccStride * 4 + 16 * 4 + (size_t)16 * Shape<G>::PM * kTile + kTile * 16 + (size_t)raw_bytes;
+    const size_t smem = partial_smem(G, raw_bytes);
     if (smem > 64 * 1024) {
         const hipError_t e = hipFuncSetAttribute((const void*)decode_mfma_kernel<G>,
                                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
@@ -636,7 +739,7 @@ extern "C" size_t kvc_decode_attn_workspace(const kvc_stream_desc* k, const kvc_
                                             int32_t max_seq_len) {
     clear_error();
     if (decode_check(k, v, G, max_seq_len)) return 0;
-    return (size_t)ws_layout(k->n_units, G, max_seq_len).total;
+    return (size_t)ws_layout(k, v, G, max_seq_len).total;
 }
 
 extern "C" int kvc_decode_attn(const kvc_stream_desc* k, const kvc_stream_desc* v, const uint16_t* q, int32_t G,
@@ -648,7 +751,7 @@ extern "C" int kvc_decode_attn(const kvc_stream_desc* k, const kvc_stream_desc* 
     if (!q || !seq_len || !out || !ws) return set_error(KVC_EINVAL, "kvc_decode_attn: null pointer");
     if (reinterpret_cast<uintptr_t>(ws) & 255) return set_error(KVC_EINVAL, "kvc_decode_attn: workspace not 256-byte aligned");
     const int U = k->n_units;
-    const WsLayout L = ws_layout(U, G, max_seq_len);
+    const WsLayout L = ws_layout(k, v, G, max_seq_len);
     if ((int64_t)ws_bytes < L.total)
         return set_error(KVC_ENOSPACE, "kvc_decode_attn: workspace %zu < %lld bytes", ws_bytes, (long long)L.total);
     char* w = reinterpret_cast<char*>(ws);
@@ -659,13 +762,7 @@ extern "C" int kvc_decode_attn(const kvc_stream_desc* k, const kvc_stream_desc* 
     hipStream_t st = (hipStream_t)stream;
     const DevSide K = dev_side(k), V = dev_side(v);
     hipLaunchKernelGGL(qprep_kernel, dim3(U), dim3(kD), 0, st, K, q, G, ql, qs, qc);
-    int raw_bytes = 16;
-    for (int u = 0; u < U; ++u) {
-        // fragment reads run past the staged tiles (up to 1024 b bytes from each tile start)
-        const int kb = 8 * k->r_host[u] * k->b_host[u];
-        const int tb = std::max(1024 * k->b_host[u], kb + 1024 * v->b_host[u]);
-        raw_bytes = tb > raw_bytes ? tb : raw_bytes;
-    }
+    const int raw_bytes = L.raw_bytes;
     const dim3 grid(L.n_chunks, U);
     int e = KVC_OK;
     switch (G) {
