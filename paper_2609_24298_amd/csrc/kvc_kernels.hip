@@ -3,12 +3,14 @@
 // in kvc_decode.hip.
 //
 // Kernels
-//  encode_kernel        one (unit, 64-token tile) per 256-thread block: the
-//                       fp16 basis is staged in LDS as fp32, each thread
-//                       projects one token onto a quarter of the coordinates
-//                       in fp32 with a rigorous error bound, undecided codes
-//                       are settled exactly in 128-bit integers, and the tile
-//                       is bit-packed from LDS with one thread per output word.
+//  encode_mfma_kernel   bulk encode: per (unit, run of 64-token tiles), the
+//                       projection on fp16 matrix cores with fp32 accumulation,
+//                       codes decided against a rigorous error bound (undecided
+//                       elements settled in fp64, then exactly in 128-bit
+//                       integers), bit-packed from LDS group by group.
+//  append_kernel        1-4 new tokens per unit (a decode step's append): one
+//                       thread per coordinate, the same decision, and a merge of
+//                       the new bits into the packed words.
 //  reconstruct_kernel   x_hat = P^T z for a 64-token block of one unit.
 #include <hip/hip_runtime.h>
 
@@ -25,28 +27,34 @@ constexpr int kTile = KVC_TILE_TOKENS;
 
 // ---------------------------------------------------------------- encode
 
-// Exact code: y = sum_j P_ij x_j as an integer multiple of 2^-48 (|y| < 2^88),
-// k = clamp(floor(y / step) + 2^(b-1), 0, 2^b - 1) with floor division in
-// 128-bit integers. Used only for elements the fp32 path cannot decide.
-__device__ __noinline__ uint32_t exact_code(const uint16_t* __restrict__ Prow, const uint16_t* __restrict__ xrow,
-                                            float step, int b) {
+// Exact code: y = sum_j P_ij x_j as an integer N = y 2^48 (|y| < 2^88); the code
+// clamp(floor(y / step) + 2^(b-1), 0, 2^b - 1) equals the number of thresholds
+// j step, j in [1 - 2^(b-1), 2^(b-1) - 1], that y reaches, found by bisection with
+// exact 128-bit comparisons N >= j step 2^48 (no division). Used only for
+// elements the floating-point paths cannot decide.
+__device__ __forceinline__ uint32_t exact_code(const uint16_t* __restrict__ Prow, const uint16_t* __restrict__ xrow,
+                                               float step, int b) {
     __int128 N = 0;
     for (int j = 0; j < kD; ++j) {
         int32_t mp, mx;
         int ep, ex;
         half_parts(Prow[j], mp, ep);
         half_parts(xrow[j], mx, ex);
-        N += (__int128)((int64_t)mp * mx) * ((__int128)1 << (ep + ex + 48));
+        N += (__int128)((int64_t)mp * mx) << (ep + ex + 48);
     }
     const uint32_t u = __float_as_uint(step);
     const int64_t m = 0x800000 | (u & 0x7fffff);
     const int sD = (int)((u >> 23) & 255) - 150 + 48;  // >= 1 for step >= 2^-24
-    const __int128 D = (__int128)m << sD;
-    __int128 q = N / D;
-    if (N % D != 0 && N < 0) q -= 1;
-    const __int128 k = q + (1 << (b - 1));
-    const __int128 kmax = (1 << b) - 1;
-    return (uint32_t)(k < 0 ? 0 : (k > kmax ? kmax : k));
+    const int h = 1 << (b - 1);
+    // count = #{j in [lo, hi] : N >= j m 2^sD}; thresholds increase with j
+    int lo = 1 - h, hi = h - 1;  // the answer is lo + (number passed) - ... kept as a half-open search
+    int first_fail = hi + 1;     // smallest j with N < j D (hi + 1 if none)
+    while (lo <= hi) {
+        const int mid = (lo + hi) >> 1;
+        if (N >= ((__int128)((int64_t)mid * m) << sD)) lo = mid + 1;
+        else { first_fail = mid; hi = mid - 1; }
+    }
+    return (uint32_t)(first_fail - (1 - h));
 }
 
 // Code from the fp32 projection `acc` whose error is at most `err`
@@ -69,111 +77,251 @@ __device__ __forceinline__ uint32_t decide_code(float acc, float err, float step
     return exact_code(Prow, xrow, step, b);
 }
 
-// Plane of output word w of a tile: width p, bit shift in the code, word index in the plane.
-__device__ __forceinline__ void word_plane(int w, int r, int b, int& p, int& shift, int& lw) {
-    if (b == 8) { p = 8; shift = 0; lw = w; return; }
-    int rem = b;
+// ---------------------------------------------------------------- bulk encode on matrix cores
+
+// Bulk encode (any token count above the append path's): one 256-thread block per (unit, run of
+// tiles); each wavefront encodes whole 64-token tiles. The projection y = P x runs on
+// v_mfma_f32_16x16x32_f16 (exact fp16 products, fp32 accumulation) with the basis staged in LDS
+// and the tile's tokens held as operand fragments in registers. Codes are decided in fp32 against
+// the bound |y_mma - y| <= 2^-15 ||P_i|| ||x|| (four times the fp32 accumulation bound for 128
+// terms) plus the rounding of y / step; the rare undecided elements are re-evaluated by the whole
+// wavefront in fp64 (exact products, a 2^-45 ||P_i|| ||x|| sum bound) and, if still undecided,
+// exactly in 128-bit integers. Each group of 16 coordinates fills 1024 consecutive slots of the
+// stream layout (K: coordinate group; V: 16 coordinate rows), which are bit-packed from LDS as
+// soon as the group is decided.
+constexpr int kEncMmaThreads = 256;
+constexpr int kEncMmaTilesPerBlock = 16;
+constexpr int kPRow = kD + 8;  // LDS row stride of the staged basis, in halves
+
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ f4 mfma_f16(h8 a, h8 b, f4 c) { return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0); }
+
+__device__ __forceinline__ double wave_sum(double v) {
 #pragma unroll
-    for (int q = 4; q >= 1; q >>= 1) {
-        if (b & q) {
-            rem -= q;
-            const int nw = 2 * r * q;
-            if (w < nw) { p = q; shift = rem; lw = w; return; }
-            w -= nw;
-        }
-    }
-    p = 1; shift = 0; lw = w;  // not reached for w < 2*r*b
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    return v;
 }
 
-constexpr int kEncThreads = 256;
+// Code of coordinate c for token row `xrow`, decided by the whole wavefront: fp64 sum of the 128
+// exact products (lane takes j = 2 lane, 2 lane + 1), then the exact path if still undecided.
+// Uniform across the wavefront.
+__device__ uint32_t resolve_code_wave(const uint16_t* __restrict__ Pl_row, const uint16_t* __restrict__ Pg_row,
+                                      const uint16_t* __restrict__ xrow, float step, int b, float pn, float xn,
+                                      int lane) {
+    const uint32_t pw = *reinterpret_cast<const uint32_t*>(Pl_row + 2 * lane);
+    const uint32_t xw = *reinterpret_cast<const uint32_t*>(xrow + 2 * lane);
+    const double s = (double)h2f((uint16_t)(pw & 0xffff)) * (double)h2f((uint16_t)(xw & 0xffff)) +
+                     (double)h2f((uint16_t)(pw >> 16)) * (double)h2f((uint16_t)(xw >> 16));
+    const double y = wave_sum(s);
+    const double e = 0x1p-45 * (double)pn * (double)xn * 1.01;
+    const int h = 1 << (b - 1);
+    const double st = step;
+    const double jn = rint(y / st);
+    bool amb = !(e < 0.25 * st);
+    if (!amb && jn >= 1 - h && jn <= h - 1) amb = !(fabs(fma(-jn, st, y)) > e + 0x1p-50 * fabs(y));
+    if (!amb) return (uint32_t)fmin(fmax(floor(y / st) + h, 0.0), (double)((1 << b) - 1));
+    return exact_code(Pg_row, xrow, step, b);
+}
 
-__global__ __launch_bounds__(kEncThreads) void encode_kernel(DevSide s, int side, const uint16_t* __restrict__ x,
-                                                             int64_t x_stride, int t0, int n_tok, int tile_first) {
-    extern __shared__ float smem[];
-    const int u = blockIdx.y;
-    const int tile = tile_first + blockIdx.x;
+template <int side>
+__global__ __launch_bounds__(kEncMmaThreads) void encode_mfma_kernel(DevSide s, const uint16_t* __restrict__ x,
+                                                                    int64_t x_stride, int t0, int n_tok, int tile_first,
+                                                                    int n_tiles) {
+    extern __shared__ uint8_t esm[];
+    uint16_t* Pl = reinterpret_cast<uint16_t*>(esm);                   // [128][kPRow] fp16 basis, rows >= r zero
+    float* tolc = reinterpret_cast<float*>(Pl + kD * kPRow);           // [128] 2^-15 1.01 ||P_i|| / step (NaN for i >= r)
+    float* pnrm = tolc + kD;                                           // [128] ||P_i||
+    float* etoks = pnrm + kD;                                          // [4 waves][64] token norms
+    uint8_t* slots = reinterpret_cast<uint8_t*>(etoks + 4 * kTile);    // [4 waves][1024] codes of one slot group
+    const int u = blockIdx.y, tid = threadIdx.x;
     const int r = s.r[u], b = s.b[u];
     const float step = s.delta[u];
-    const uint16_t* __restrict__ P = s.basis + s.basis_off[u];
-    float* Ps = smem;                                   // [r][128] fp32 basis
-    float* pn = Ps + r * kD;                            // [r] row norms
-    uint8_t* cs = reinterpret_cast<uint8_t*>(pn + kD);  // [64][128] codes
-
-    for (int k = threadIdx.x; k < r * kD; k += kEncThreads) Ps[k] = h2f((P[k]));
+    const uint16_t* __restrict__ Pg = s.basis + s.basis_off[u];
+    for (int q = tid; q < kD * (kD / 8); q += kEncMmaThreads) {
+        const int row = q >> 4, c8 = q & 15;
+        uint4 v = {0u, 0u, 0u, 0u};
+        if (row < r) v = reinterpret_cast<const uint4*>(Pg + (int64_t)row * kD)[c8];
+        *reinterpret_cast<uint4*>(Pl + row * kPRow + 8 * c8) = v;
+    }
     __syncthreads();
-    if (threadIdx.x < r) {
+    if (tid < kD) {
         float s2 = 0.f;
-        for (int j = 0; j < kD; ++j) s2 = fmaf(Ps[threadIdx.x * kD + j], Ps[threadIdx.x * kD + j], s2);
-        pn[threadIdx.x] = sqrtf(s2);
-    }
-
-    const int t = threadIdx.x & 63, grp = threadIdx.x >> 6;
-    const int tok = tile * kTile + t;
-    const bool active = tok >= t0 && tok < t0 + n_tok;
-    const uint16_t* xrow = x + (int64_t)u * x_stride + (int64_t)(tok - t0) * kD;
-    float xv[kD];
-    float xn2 = 0.f;
-    if (active) {
-        const uint4* xr4 = reinterpret_cast<const uint4*>(xrow);
-#pragma unroll
-        for (int q = 0; q < kD / 8; ++q) {
-            const uint4 v = xr4[q];
-            const uint32_t w4[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                xv[8 * q + 2 * e] = h2f(((uint16_t)(w4[e] & 0xffff)));
-                xv[8 * q + 2 * e + 1] = h2f(((uint16_t)(w4[e] >> 16)));
-            }
+        for (int j = 0; j < kD; ++j) {
+            const float p = h2f(Pl[tid * kPRow + j]);
+            s2 = fmaf(p, p, s2);
         }
-#pragma unroll
-        for (int j = 0; j < kD; ++j) xn2 = fmaf(xv[j], xv[j], xn2);
-    }
-    // |acc - y| <= gamma_128 * sum_j |P_ij x_j| <= 2^-17 * ||P_i|| ||x||; 2^-15 leaves a 4x margin
-    // for the rounding of the norms themselves.
-    const float xn = sqrtf(xn2);
-    __syncthreads();
-    if (active) {
-        for (int i = grp; i < r; i += 4) {
-            const float4* Pr = reinterpret_cast<const float4*>(Ps + i * kD);
-            float acc = 0.f;
-#pragma unroll
-            for (int q = 0; q < kD / 4; ++q) {
-                const float4 pv = Pr[q];
-                acc = fmaf(pv.x, xv[4 * q], acc);
-                acc = fmaf(pv.y, xv[4 * q + 1], acc);
-                acc = fmaf(pv.z, xv[4 * q + 2], acc);
-                acc = fmaf(pv.w, xv[4 * q + 3], acc);
-            }
-            const float err = 0x1p-15f * pn[i] * xn;
-            cs[t * kD + i] = (uint8_t)decide_code(acc, err, step, b, P + (int64_t)i * kD, xrow);
-        }
+        pnrm[tid] = sqrtf(s2);
+        tolc[tid] = tid < r ? 0x1p-15f * 1.01f * sqrtf(s2) / step : __builtin_nanf("");
     }
     __syncthreads();
 
-    // Pack: one thread per 32-bit output word; partial tiles keep the other tokens' bits.
-    uint32_t* tw = reinterpret_cast<uint32_t*>(s.codes + s.code_off[u] + (int64_t)tile * 8 * r * b);
-    const int tok0 = tile * kTile;
-    const bool full = tok0 >= t0 && tok0 + kTile <= t0 + n_tok;
-    const int n_words = 2 * r * b;
-    for (int w = threadIdx.x; w < n_words; w += kEncThreads) {
-        int p, shift, lw;
-        word_plane(w, r, b, p, shift, lw);
-        const int per_word = 32 / p;
-        const uint32_t vmask = (1u << p) - 1u;
-        uint32_t val = 0, msk = 0;
-        for (int iota = 0; iota < per_word; ++iota) {
-            const int phi = lw * per_word + iota;
-            int tt, i;
-            if (side == KVC_SIDE_K) unslot_k(phi, r, tt, i);
-            else { i = phi >> 6; tt = psi(phi & 63); }
-            const int tk = tok0 + tt;
-            if (tk >= t0 && tk < t0 + n_tok) {
-                const int bit = 8 * (iota & 3) + p * (iota >> 2);
-                val |= ((uint32_t)(cs[tt * kD + i] >> shift) & vmask) << bit;
-                msk |= vmask << bit;
+    const int wv = tid >> 6, lane = tid & 63, col = lane & 15, grp = lane >> 4;
+    uint8_t* __restrict__ sb = slots + wv * 1024;
+    float* __restrict__ etok = etoks + wv * kTile;
+    const int h = 1 << (b - 1);
+    const float fh = (float)h, fmax_code = (float)(2 * h - 1), inv = 1.f / step;
+    const int g16 = r >> 4, rho = r & 15, n_mc = (r + 15) >> 4;
+    uint8_t* __restrict__ stream = s.codes + s.code_off[u];
+    const uint16_t* __restrict__ xu = x + (int64_t)u * x_stride;
+
+#pragma unroll 1
+    for (int tt = wv; tt < kEncMmaTilesPerBlock; tt += kEncMmaThreads / 64) {
+        const int tl_idx = blockIdx.x * kEncMmaTilesPerBlock + tt;
+        if (tl_idx >= n_tiles) break;
+        const int tile = tile_first + tl_idx, tok0 = tile * kTile;
+        const int lo = max(t0, tok0), hi = min(t0 + n_tok, tok0 + kTile);
+        const bool full = lo == tok0 && hi == tok0 + kTile;
+        uint8_t* __restrict__ tbase = stream + (int64_t)tile * 8 * r * b;
+
+        // Token fragments: token 16 nt + col, dims 32 ks + 8 grp + [0, 8). Tokens outside the range
+        // read a valid token and never reach the stream.
+        h8 xf[4][4];
+        float et[4];  // ||x|| of the lane's token (NaN outside the range: such elements are never undecided)
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) {
+            const int tk = tok0 + 16 * nt + col;
+            const bool ok = tk >= lo && tk < hi;
+            const h8* row = reinterpret_cast<const h8*>(xu + (int64_t)((ok ? tk : lo) - t0) * kD);
+            float s2 = 0.f;
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks) {
+                xf[nt][ks] = row[4 * ks + grp];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const h2 v = {xf[nt][ks][2 * e], xf[nt][ks][2 * e + 1]};
+                    s2 = __builtin_amdgcn_fdot2(v, v, s2, false);
+                }
             }
+            s2 += __shfl_xor(s2, 16);
+            s2 += __shfl_xor(s2, 32);
+            et[nt] = ok ? sqrtf(s2) : __builtin_nanf("");
+            if (grp == 0) etok[16 * nt + col] = et[nt];
         }
-        tw[w] = full ? val : ((tw[w] & ~msk) | val);
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll 1
+        for (int mc = 0; mc < n_mc; ++mc) {
+            h8 pf[4];
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks)
+                pf[ks] = *reinterpret_cast<const h8*>(Pl + (16 * mc + col) * kPRow + 32 * ks + 8 * grp);
+            f4 acc[4];
+#pragma unroll
+            for (int nt = 0; nt < 4; ++nt) {
+                acc[nt] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int ks = 0; ks < 4; ++ks)
+                    acc[nt] = side == KVC_SIDE_K ? mfma_f16(pf[ks], xf[nt][ks], acc[nt]) : mfma_f16(xf[nt][ks], pf[ks], acc[nt]);
+            }
+            // K: lane holds coordinates 16 mc + 4 grp + i of token 16 nt + col.
+            // V: lane holds tokens 16 nt + 4 grp + i of coordinate 16 mc + col.
+            uint32_t ambm = 0;
+            uint32_t cw[4];
+#pragma unroll 2
+            for (int nt = 0; nt < 4; ++nt) {
+                uint32_t w = 0;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    float tb;
+                    if constexpr (side == KVC_SIDE_K) tb = et[nt] * tolc[16 * mc + 4 * grp + i];
+                    else tb = etok[16 * nt + 4 * grp + i] * tolc[16 * mc + col];
+                    const float t = acc[nt][i] * inv;
+                    const float f = floorf(t);
+                    const float fr = t - f;
+                    const float d = fminf(fr, 1.f - fr);
+                    if (d <= fmaf(fabsf(t), 0x1p-22f, tb)) ambm |= 1u << (4 * nt + i);
+                    const uint32_t k = (uint32_t)__builtin_amdgcn_fmed3f(f + fh, 0.f, fmax_code);
+                    w |= k << (8 * i);
+                }
+                cw[nt] = w;
+            }
+            // place the codes in the group's 1024 slots
+            const bool tailg = mc == g16;  // K tail group (rho > 0)
+            if constexpr (side == KVC_SIDE_K) {
+                if (!tailg) {
+#pragma unroll
+                    for (int nt = 0; nt < 4; ++nt)
+                        *reinterpret_cast<uint32_t*>(sb + 16 * (16 * nt + col) + 4 * grp) = cw[nt];
+                } else {
+#pragma unroll
+                    for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+                        for (int i = 0; i < 4; ++i)
+                            if (4 * grp + i < rho) sb[(16 * nt + col) * rho + 4 * grp + i] = (uint8_t)(cw[nt] >> (8 * i));
+                }
+            } else if (16 * mc + col < r) {
+#pragma unroll
+                for (int nt = 0; nt < 4; ++nt) *reinterpret_cast<uint32_t*>(sb + 64 * col + 16 * grp + 4 * nt) = cw[nt];
+            }
+            // undecided elements: the whole wavefront settles them one by one
+            uint64_t pend = __ballot(ambm != 0);
+            while (pend) {
+                const int L = __builtin_ctzll(pend);
+                pend &= pend - 1;
+                uint32_t m = __shfl(ambm, L);
+                const int Lcol = L & 15, Lgrp = L >> 4;
+                while (m) {
+                    const int bit = __builtin_ctz(m);
+                    m &= m - 1;
+                    const int nt = bit >> 2, i = bit & 3;
+                    int tkn, c, sl;
+                    if constexpr (side == KVC_SIDE_K) {
+                        tkn = 16 * nt + Lcol;
+                        c = 16 * mc + 4 * Lgrp + i;
+                        sl = tailg ? tkn * rho + 4 * Lgrp + i : 16 * tkn + 4 * Lgrp + i;
+                    } else {
+                        tkn = 16 * nt + 4 * Lgrp + i;
+                        c = 16 * mc + Lcol;
+                        sl = 64 * Lcol + 16 * Lgrp + 4 * nt + i;
+                    }
+                    const uint16_t* xrow = xu + (int64_t)(tok0 + tkn - t0) * kD;
+                    float xn2 = 0.f;
+                    {
+                        const uint32_t xw = *reinterpret_cast<const uint32_t*>(xrow + 2 * lane);
+                        const float a0 = h2f((uint16_t)(xw & 0xffff)), a1 = h2f((uint16_t)(xw >> 16));
+                        xn2 = fmaf(a0, a0, a1 * a1);
+                        for (int o = 32; o > 0; o >>= 1) xn2 += __shfl_xor(xn2, o);
+                    }
+                    const uint32_t code = resolve_code_wave(Pl + c * kPRow, Pg + (int64_t)c * kD, xrow, step, b, pnrm[c],
+                                                            sqrtf(xn2), lane);
+                    if (lane == 0) sb[sl] = (uint8_t)code;
+                }
+            }
+            __builtin_amdgcn_wave_barrier();
+            // pack the group's slots [1024 mc, 1024 mc + n_sl) into every plane
+            const int n_sl = (rho && mc == n_mc - 1) ? 64 * rho : 1024;  // K tail group / V last coordinate rows
+            const int sl0 = 1024 * mc;
+            for (int p = 8, off = 0; p >= 1; p >>= 1) {
+                if (b == 8 ? p != 8 : (p == 8 || !(b & p))) continue;
+                const int sh = b == 8 ? 0 : (b & (p - 1));
+                const int ppw = 32 / p, nw = n_sl / ppw;
+                const uint32_t pm = (p == 8 ? 0xffu : ((1u << p) - 1u)) * 0x01010101u;
+                uint32_t* __restrict__ pw = reinterpret_cast<uint32_t*>(tbase + 8 * r * off) + sl0 / ppw;
+                for (int wi = lane; wi < nw; wi += 64) {
+                    const uint32_t* src = reinterpret_cast<const uint32_t*>(sb + wi * ppw);
+                    uint32_t word = 0;
+                    for (int m = 0; m < ppw / 4; ++m) word |= ((src[m] >> sh) & pm) << (p * m);
+                    if (full) {
+                        pw[wi] = word;
+                    } else {
+                        uint32_t msk = 0;
+                        for (int io = 0; io < ppw; ++io) {
+                            const int ph = sl0 + wi * ppw + io;
+                            int t2, i2;
+                            if constexpr (side == KVC_SIDE_K) unslot_k(ph, r, t2, i2);
+                            else { i2 = ph >> 6; t2 = psi(ph & 63); }
+                            const int tk = tok0 + t2;
+                            if (tk >= lo && tk < hi) msk |= (p == 8 ? 0xffu : ((1u << p) - 1u)) << (8 * (io & 3) + p * (io >> 2));
+                        }
+                        pw[wi] = (pw[wi] & ~msk) | (word & msk);
+                    }
+                }
+                off += p;
+            }
+            __builtin_amdgcn_wave_barrier();
+        }
     }
 }
 
@@ -181,7 +329,7 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(DevSide s, int side
 
 // Appending a few tokens (a decode step adds one per unit): one block per unit, thread i
 // computes coordinate i of every new token from its basis row, decides the code as
-// encode_kernel does, and the new codes are merged into the packed words of their tiles.
+// the bulk encoder does, and the new codes are merged into the packed words of their tiles.
 constexpr int kAppThreads = kD;
 constexpr int kAppMaxTok = 4;
 
@@ -229,7 +377,7 @@ __global__ __launch_bounds__(kAppThreads) void append_kernel(DevSide s, int side
 #pragma unroll
         for (int t = 0; t < kAppMaxTok; ++t)
             if (t < n_tok) {
-                // same bound as encode_kernel: |acc - y| <= 2^-17 ||P_i|| ||x||, used with a 4x margin
+                // |acc - y| <= 2^-17 ||P_i|| ||x|| for a 128-term fp32 sum, used with a 4x margin
                 const float xn = sqrtf(red[t][0] + red[t][1]);
                 cs[t][i] = (uint8_t)decide_code(acc[t], 0x1p-15f * pn * xn, step, b, P + (int64_t)i * kD,
                                                 xu + (int64_t)t * kD);
@@ -351,12 +499,15 @@ extern "C" int kvc_encode(const kvc_stream_desc* s, const uint16_t* x, int64_t x
         return check_launch("kvc_encode");
     }
     const int tile_first = t0 / kTile;
-    const int tile_last = (t0 + n_tok - 1) / kTile;
-    const size_t smem = (size_t)max_r(s) * kD * 4 + kD * 4 + kTile * kD;
-    if (int e = set_smem_limit((const void*)encode_kernel, smem)) return e;
-    dim3 grid(tile_last - tile_first + 1, s->n_units);
-    hipLaunchKernelGGL(encode_kernel, grid, dim3(kEncThreads), smem, (hipStream_t)stream, dev_side(s), s->side, x,
-                       x_unit_stride, t0, n_tok, tile_first);
+    const int n_tiles = (t0 + n_tok - 1) / kTile - tile_first + 1;
+    const size_t smem = (size_t)kD * kPRow * 2 + 2 * kD * 4 + (kEncMmaThreads / 64) * (kTile * 4 + 1024);
+    dim3 grid((n_tiles + kEncMmaTilesPerBlock - 1) / kEncMmaTilesPerBlock, s->n_units);
+    if (s->side == KVC_SIDE_K)
+        hipLaunchKernelGGL(encode_mfma_kernel<KVC_SIDE_K>, grid, dim3(kEncMmaThreads), smem, (hipStream_t)stream,
+                           dev_side(s), x, x_unit_stride, t0, n_tok, tile_first, n_tiles);
+    else
+        hipLaunchKernelGGL(encode_mfma_kernel<KVC_SIDE_V>, grid, dim3(kEncMmaThreads), smem, (hipStream_t)stream,
+                           dev_side(s), x, x_unit_stride, t0, n_tok, tile_first, n_tiles);
     return check_launch("kvc_encode");
 }
 
