@@ -81,19 +81,6 @@ __device__ __forceinline__ void plane_frag16(const uint8_t* __restrict__ plane, 
     }
 }
 
-// Planes of a b-bit code, widest first (b = 8: one plane): width of plane k, its bit
-// shift inside the code and its offset in units of 8*r bytes. Fragment extraction is
-// instantiated per b, so these fold to constants.
-__host__ __device__ constexpr int n_planes(int b) { return b == 8 ? 1 : ((b & 4) ? 1 : 0) + ((b & 2) ? 1 : 0) + (b & 1); }
-__host__ __device__ constexpr int plane_w(int b, int k) {
-    return b == 8 ? 8 : (k == 0 ? ((b & 4) ? 4 : ((b & 2) ? 2 : 1))
-                               : (k == 1 ? ((b & 4) ? ((b & 2) ? 2 : 1) : 1) : 1));
-}
-__host__ __device__ constexpr int plane_sh(int b, int k) {
-    return k + 1 >= n_planes(b) ? 0 : plane_w(b, k + 1) + plane_sh(b, k + 1);
-}
-__host__ __device__ constexpr int plane_off(int b, int k) { return k == 0 ? 0 : plane_w(b, k - 1) + plane_off(b, k - 1); }
-
 template <int B, int K>
 __device__ __forceinline__ void add_plane16(const uint8_t* __restrict__ tile, int r, int phi0, uint32_t acc[4]) {
     if constexpr (K < n_planes(B)) {
@@ -255,19 +242,6 @@ __device__ __forceinline__ void v_frags(const uint8_t* __restrict__ vtile, int r
         Bf[k] = nt == kD / 16 ? ones : code_frag16<BV>(vtile, rv, ((16 * nt + col) << 6) + (grp << 4));
     }
 }
-
-// Runs CALL with the compile-time bit width B_ equal to the runtime value b.
-#define KVC_SWITCH_B(b, CALL)                                \
-    switch (b) {                                             \
-        case 1: { constexpr int B_ = 1; CALL; } break;       \
-        case 2: { constexpr int B_ = 2; CALL; } break;       \
-        case 3: { constexpr int B_ = 3; CALL; } break;       \
-        case 4: { constexpr int B_ = 4; CALL; } break;       \
-        case 5: { constexpr int B_ = 5; CALL; } break;       \
-        case 6: { constexpr int B_ = 6; CALL; } break;       \
-        case 7: { constexpr int B_ = 7; CALL; } break;       \
-        default: { constexpr int B_ = 8; CALL; } break;      \
-    }
 
 template <int G>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(Shape<G>::W, Shape<G>::W))) void decode_mfma_kernel(DevSide K, DevSide V, const int8_t* __restrict__ qlimb,

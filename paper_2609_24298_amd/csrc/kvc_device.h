@@ -63,6 +63,32 @@ __device__ __forceinline__ uint32_t load_code(const uint8_t* __restrict__ tile, 
     return c;
 }
 
+// Planes of a b-bit code, widest first (b = 8: one plane): width of plane k, its bit
+// shift inside the code and its offset in units of 8*r bytes. Fragment extraction is
+// instantiated per b, so these fold to constants.
+__host__ __device__ constexpr int n_planes(int b) { return b == 8 ? 1 : ((b & 4) ? 1 : 0) + ((b & 2) ? 1 : 0) + (b & 1); }
+__host__ __device__ constexpr int plane_w(int b, int k) {
+    return b == 8 ? 8 : (k == 0 ? ((b & 4) ? 4 : ((b & 2) ? 2 : 1))
+                               : (k == 1 ? ((b & 4) ? ((b & 2) ? 2 : 1) : 1) : 1));
+}
+__host__ __device__ constexpr int plane_sh(int b, int k) {
+    return k + 1 >= n_planes(b) ? 0 : plane_w(b, k + 1) + plane_sh(b, k + 1);
+}
+__host__ __device__ constexpr int plane_off(int b, int k) { return k == 0 ? 0 : plane_w(b, k - 1) + plane_off(b, k - 1); }
+
+// Runs CALL with the compile-time bit width B_ equal to the runtime value b.
+#define KVC_SWITCH_B(b, CALL)                                \
+    switch (b) {                                             \
+        case 1: { constexpr int B_ = 1; CALL; } break;       \
+        case 2: { constexpr int B_ = 2; CALL; } break;       \
+        case 3: { constexpr int B_ = 3; CALL; } break;       \
+        case 4: { constexpr int B_ = 4; CALL; } break;       \
+        case 5: { constexpr int B_ = 5; CALL; } break;       \
+        case 6: { constexpr int B_ = 6; CALL; } break;       \
+        case 7: { constexpr int B_ = 7; CALL; } break;       \
+        default: { constexpr int B_ = 8; CALL; } break;      \
+    }
+
 // fp16 bits -> fp32 (exact).
 __device__ __forceinline__ float h2f(uint16_t h) { return (float)__builtin_bit_cast(_Float16, h); }
 

@@ -83,8 +83,8 @@ __device__ __forceinline__ uint32_t decide_code(float acc, float err, float step
 // tiles); each wavefront encodes whole 64-token tiles. The projection y = P x runs on
 // v_mfma_f32_16x16x32_f16 (exact fp16 products, fp32 accumulation) with the basis staged in LDS
 // and the tile's tokens held as operand fragments in registers. Codes are decided in fp32 against
-// the bound |y_mma - y| <= 2^-15 ||P_i|| ||x|| (four times the fp32 accumulation bound for 128
-// terms) plus the rounding of y / step; the rare undecided elements are re-evaluated by the whole
+// the bound |y_mma - y| <= 2^-16 ||P_i|| ||x|| (twice the bound for 128 terms summed with fp32
+// round-to-nearest, so it also holds for truncating additions) plus the rounding of y / step; the rare undecided elements are re-evaluated by the whole
 // wavefront in fp64 (exact products, a 2^-45 ||P_i|| ||x|| sum bound) and, if still undecided,
 // exactly in 128-bit integers. Each group of 16 coordinates fills 1024 consecutive slots of the
 // stream layout (K: coordinate group; V: 16 coordinate rows), which are bit-packed from LDS as
@@ -119,20 +119,51 @@ __device__ uint32_t resolve_code_wave(const uint16_t* __restrict__ Pl_row, const
     const double e = 0x1p-45 * (double)pn * (double)xn * 1.01;
     const int h = 1 << (b - 1);
     const double st = step;
-    const double jn = rint(y / st);
-    bool amb = !(e < 0.25 * st);
-    if (!amb && jn >= 1 - h && jn <= h - 1) amb = !(fabs(fma(-jn, st, y)) > e + 0x1p-50 * fabs(y));
-    if (!amb) return (uint32_t)fmin(fmax(floor(y / st) + h, 0.0), (double)((1 << b) - 1));
+    // jn: a threshold index near y / step; the sign of y - jn step is certain when |y - jn step|
+    // exceeds the bound, and then (for e < step / 4) y lies between jn - 1 and jn + 1 thresholds.
+    const double jn = rint(y * (1.0 / st));
+    const double d = fma(-jn, st, y);
+    if (e < 0.25 * st && fabs(d) > e + 0x1p-50 * fabs(y) && fabs(d) < 0.75 * st)
+        return (uint32_t)fmin(fmax(jn - (d < 0.0 ? 1.0 : 0.0) + h, 0.0), (double)((1 << b) - 1));
     return exact_code(Pg_row, xrow, step, b);
 }
 
+// Packs slots [sl0, sl0 + n_sl) of a tile (their codes are bytes sb[0 .. n_sl) in slot order)
+// into every bit plane of a B-bit code: word w of a plane of width p takes slots
+// [w 32/p, (w + 1) 32/p); dword m of those bytes holds slots 4m .. 4m + 3, shifted by p m.
+template <int B, int K>
+__device__ __forceinline__ void pack_plane(const uint8_t* __restrict__ sb, uint8_t* __restrict__ tbase, int r, int sl0,
+                                           int n_sl, int lane) {
+    if constexpr (K < n_planes(B)) {
+        constexpr int P = plane_w(B, K), SH = plane_sh(B, K), PPW = 32 / P;
+        constexpr uint32_t PM = (P == 8 ? 0xffu : ((1u << P) - 1u)) * 0x01010101u;
+        uint32_t* __restrict__ pw = reinterpret_cast<uint32_t*>(tbase + 8 * r * plane_off(B, K)) + sl0 / PPW;
+        const int nw = n_sl / PPW;
+        for (int wi = lane; wi < nw; wi += 64) {
+            const uint32_t* src = reinterpret_cast<const uint32_t*>(sb + wi * PPW);
+            uint32_t word = 0;
+#pragma unroll
+            for (int m = 0; m < PPW / 4; ++m) word |= ((src[m] >> SH) & PM) << (P * m);
+            pw[wi] = word;
+        }
+    }
+}
+
+template <int B>
+__device__ __forceinline__ void pack_group(const uint8_t* __restrict__ sb, uint8_t* __restrict__ tbase, int r, int sl0,
+                                           int n_sl, int lane) {
+    pack_plane<B, 0>(sb, tbase, r, sl0, n_sl, lane);
+    pack_plane<B, 1>(sb, tbase, r, sl0, n_sl, lane);
+    pack_plane<B, 2>(sb, tbase, r, sl0, n_sl, lane);
+}
+
 template <int side>
-__global__ __launch_bounds__(kEncMmaThreads) void encode_mfma_kernel(DevSide s, const uint16_t* __restrict__ x,
+__global__ __launch_bounds__(kEncMmaThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void encode_mfma_kernel(DevSide s, const uint16_t* __restrict__ x,
                                                                     int64_t x_stride, int t0, int n_tok, int tile_first,
                                                                     int n_tiles) {
     extern __shared__ uint8_t esm[];
     uint16_t* Pl = reinterpret_cast<uint16_t*>(esm);                   // [128][kPRow] fp16 basis, rows >= r zero
-    float* tolc = reinterpret_cast<float*>(Pl + kD * kPRow);           // [128] 2^-15 1.01 ||P_i|| / step (NaN for i >= r)
+    float* tolc = reinterpret_cast<float*>(Pl + kD * kPRow);           // [128] 2^-16 1.01 ||P_i|| / step (NaN for i >= r)
     float* pnrm = tolc + kD;                                           // [128] ||P_i||
     float* etoks = pnrm + kD;                                          // [4 waves][64] token norms
     uint8_t* slots = reinterpret_cast<uint8_t*>(etoks + 4 * kTile);    // [4 waves][1024] codes of one slot group
@@ -154,7 +185,7 @@ __global__ __launch_bounds__(kEncMmaThreads) void encode_mfma_kernel(DevSide s, 
             s2 = fmaf(p, p, s2);
         }
         pnrm[tid] = sqrtf(s2);
-        tolc[tid] = tid < r ? 0x1p-15f * 1.01f * sqrtf(s2) / step : __builtin_nanf("");
+        tolc[tid] = tid < r ? 0x1p-16f * 1.01f * sqrtf(s2) / step : __builtin_nanf("");
     }
     __syncthreads();
 
@@ -217,23 +248,23 @@ __global__ __launch_bounds__(kEncMmaThreads) void encode_mfma_kernel(DevSide s, 
             }
             // K: lane holds coordinates 16 mc + 4 grp + i of token 16 nt + col.
             // V: lane holds tokens 16 nt + 4 grp + i of coordinate 16 mc + col.
-            uint32_t ambm = 0;
+            // t = y / step + 2^(b-1): its floor, clamped, is the code; the element is undecided if an
+            // integer lies within the error bound (in step units) of t, which adds (|t| + 2^(b-1)) 2^-22
+            // for the rounding of 1 / step and of the fused multiply-add.
+            bool any_amb = false;
             uint32_t cw[4];
-#pragma unroll 2
+#pragma unroll
             for (int nt = 0; nt < 4; ++nt) {
                 uint32_t w = 0;
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    float tb;
-                    if constexpr (side == KVC_SIDE_K) tb = et[nt] * tolc[16 * mc + 4 * grp + i];
-                    else tb = etok[16 * nt + 4 * grp + i] * tolc[16 * mc + col];
-                    const float t = acc[nt][i] * inv;
+                    const float tb = side == KVC_SIDE_K ? et[nt] * tolc[16 * mc + 4 * grp + i]
+                                                        : etok[16 * nt + 4 * grp + i] * tolc[16 * mc + col];
+                    const float t = fmaf(acc[nt][i], inv, fh);
                     const float f = floorf(t);
                     const float fr = t - f;
-                    const float d = fminf(fr, 1.f - fr);
-                    if (d <= fmaf(fabsf(t), 0x1p-22f, tb)) ambm |= 1u << (4 * nt + i);
-                    const uint32_t k = (uint32_t)__builtin_amdgcn_fmed3f(f + fh, 0.f, fmax_code);
-                    w |= k << (8 * i);
+                    any_amb |= fminf(fr, 1.f - fr) <= fmaf(fabsf(t) + fh, 0x1p-22f, tb);
+                    w = __builtin_amdgcn_cvt_pk_u8_f32(__builtin_amdgcn_fmed3f(f, 0.f, fmax_code), i, w);
                 }
                 cw[nt] = w;
             }
@@ -255,70 +286,79 @@ __global__ __launch_bounds__(kEncMmaThreads) void encode_mfma_kernel(DevSide s, 
 #pragma unroll
                 for (int nt = 0; nt < 4; ++nt) *reinterpret_cast<uint32_t*>(sb + 64 * col + 16 * grp + 4 * nt) = cw[nt];
             }
-            // undecided elements: the whole wavefront settles them one by one
-            uint64_t pend = __ballot(ambm != 0);
-            while (pend) {
-                const int L = __builtin_ctzll(pend);
-                pend &= pend - 1;
-                uint32_t m = __shfl(ambm, L);
-                const int Lcol = L & 15, Lgrp = L >> 4;
-                while (m) {
-                    const int bit = __builtin_ctz(m);
-                    m &= m - 1;
-                    const int nt = bit >> 2, i = bit & 3;
-                    int tkn, c, sl;
-                    if constexpr (side == KVC_SIDE_K) {
-                        tkn = 16 * nt + Lcol;
-                        c = 16 * mc + 4 * Lgrp + i;
-                        sl = tailg ? tkn * rho + 4 * Lgrp + i : 16 * tkn + 4 * Lgrp + i;
-                    } else {
-                        tkn = 16 * nt + 4 * Lgrp + i;
-                        c = 16 * mc + Lcol;
-                        sl = 64 * Lcol + 16 * Lgrp + 4 * nt + i;
+            // undecided elements (rare): flag them again per lane, then the whole wavefront settles
+            // them one by one
+            if (__any(any_amb)) {
+                uint32_t ambm = 0;
+#pragma unroll
+                for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const float tb = side == KVC_SIDE_K ? et[nt] * tolc[16 * mc + 4 * grp + i]
+                                                            : etok[16 * nt + 4 * grp + i] * tolc[16 * mc + col];
+                        const float t = fmaf(acc[nt][i], inv, fh);
+                        const float fr = t - floorf(t);
+                        if (fminf(fr, 1.f - fr) <= fmaf(fabsf(t) + fh, 0x1p-22f, tb)) ambm |= 1u << (4 * nt + i);
                     }
-                    const uint16_t* xrow = xu + (int64_t)(tok0 + tkn - t0) * kD;
-                    float xn2 = 0.f;
-                    {
-                        const uint32_t xw = *reinterpret_cast<const uint32_t*>(xrow + 2 * lane);
-                        const float a0 = h2f((uint16_t)(xw & 0xffff)), a1 = h2f((uint16_t)(xw >> 16));
-                        xn2 = fmaf(a0, a0, a1 * a1);
-                        for (int o = 32; o > 0; o >>= 1) xn2 += __shfl_xor(xn2, o);
+                uint64_t pend = __ballot(ambm != 0);
+                while (pend) {
+                    const int L = __builtin_ctzll(pend);
+                    pend &= pend - 1;
+                    uint32_t m = __shfl(ambm, L);
+                    const int Lcol = L & 15, Lgrp = L >> 4;
+                    while (m) {
+                        const int bit = __builtin_ctz(m);
+                        m &= m - 1;
+                        const int nt = bit >> 2, i = bit & 3;
+                        int tkn, c, sl;
+                        if constexpr (side == KVC_SIDE_K) {
+                            tkn = 16 * nt + Lcol;
+                            c = 16 * mc + 4 * Lgrp + i;
+                            sl = tailg ? tkn * rho + 4 * Lgrp + i : 16 * tkn + 4 * Lgrp + i;
+                        } else {
+                            tkn = 16 * nt + 4 * Lgrp + i;
+                            c = 16 * mc + Lcol;
+                            sl = 64 * Lcol + 16 * Lgrp + 4 * nt + i;
+                        }
+                        const uint16_t* xrow = xu + (int64_t)(tok0 + tkn - t0) * kD;
+                        const uint32_t code = resolve_code_wave(Pl + c * kPRow, Pg + (int64_t)c * kD, xrow, step, b,
+                                                                pnrm[c], etok[tkn], lane);
+                        if (lane == 0) sb[sl] = (uint8_t)code;
                     }
-                    const uint32_t code = resolve_code_wave(Pl + c * kPRow, Pg + (int64_t)c * kD, xrow, step, b, pnrm[c],
-                                                            sqrtf(xn2), lane);
-                    if (lane == 0) sb[sl] = (uint8_t)code;
                 }
             }
             __builtin_amdgcn_wave_barrier();
             // pack the group's slots [1024 mc, 1024 mc + n_sl) into every plane
             const int n_sl = (rho && mc == n_mc - 1) ? 64 * rho : 1024;  // K tail group / V last coordinate rows
             const int sl0 = 1024 * mc;
-            for (int p = 8, off = 0; p >= 1; p >>= 1) {
-                if (b == 8 ? p != 8 : (p == 8 || !(b & p))) continue;
-                const int sh = b == 8 ? 0 : (b & (p - 1));
-                const int ppw = 32 / p, nw = n_sl / ppw;
-                const uint32_t pm = (p == 8 ? 0xffu : ((1u << p) - 1u)) * 0x01010101u;
-                uint32_t* __restrict__ pw = reinterpret_cast<uint32_t*>(tbase + 8 * r * off) + sl0 / ppw;
-                for (int wi = lane; wi < nw; wi += 64) {
-                    const uint32_t* src = reinterpret_cast<const uint32_t*>(sb + wi * ppw);
-                    uint32_t word = 0;
-                    for (int m = 0; m < ppw / 4; ++m) word |= ((src[m] >> sh) & pm) << (p * m);
-                    if (full) {
-                        pw[wi] = word;
-                    } else {
-                        uint32_t msk = 0;
+            if (full) {
+                KVC_SWITCH_B(b, pack_group<B_>(sb, tbase, r, sl0, n_sl, lane));
+            } else {
+                // partial tile: rewrite only the slots of tokens in [lo, hi)
+                for (int p = 8, off = 0; p >= 1; p >>= 1) {
+                    if (b == 8 ? p != 8 : (p == 8 || !(b & p))) continue;
+                    const int sh = b == 8 ? 0 : (b & (p - 1));
+                    const int ppw = 32 / p, nw = n_sl / ppw;
+                    const uint32_t vm = p == 8 ? 0xffu : ((1u << p) - 1u);
+                    uint32_t* __restrict__ pw = reinterpret_cast<uint32_t*>(tbase + 8 * r * off) + sl0 / ppw;
+                    for (int wi = lane; wi < nw; wi += 64) {
+                        uint32_t word = 0, msk = 0;
                         for (int io = 0; io < ppw; ++io) {
                             const int ph = sl0 + wi * ppw + io;
                             int t2, i2;
                             if constexpr (side == KVC_SIDE_K) unslot_k(ph, r, t2, i2);
                             else { i2 = ph >> 6; t2 = psi(ph & 63); }
                             const int tk = tok0 + t2;
-                            if (tk >= lo && tk < hi) msk |= (p == 8 ? 0xffu : ((1u << p) - 1u)) << (8 * (io & 3) + p * (io >> 2));
+                            if (tk >= lo && tk < hi) {
+                                const int bit = 8 * (io & 3) + p * (io >> 2);
+                                word |= (((uint32_t)sb[wi * ppw + io] >> sh) & vm) << bit;
+                                msk |= vm << bit;
+                            }
                         }
-                        pw[wi] = (pw[wi] & ~msk) | (word & msk);
+                        pw[wi] = (pw[wi] & ~msk) | word;
                     }
+                    off += p;
                 }
-                off += p;
             }
             __builtin_amdgcn_wave_barrier();
         }
