@@ -21,18 +21,23 @@
  *  - Every floating-point input must be finite.
  *
  * Packed code stream of one (unit, side), defined by this library (the
- * paper fixes only its size: exactly r*b bits per token, no metadata):
+ * paper fixes only its size: exactly r*b bits per token, no metadata,
+ * Appendix E):
  *  - tiles of 64 tokens, tile t at byte code_off + t * 8*r*b;
  *  - a b-bit code is split into planes (b = 8: one 8-bit plane; otherwise the
  *    binary expansion of b, widest first, widest = most significant bits);
- *    the plane of width p is 8*r*p bytes = 2*r*p little-endian 32-bit words,
- *    planes in that order;
- *  - slot phi of a plane lies in word phi / (32/p) at bit
- *    8*(iota % 4) + p*(iota / 4), iota = phi % (32/p);
+ *    the plane of width p is 8*r*p bytes, planes in that order;
+ *  - inside a plane, slot phi holds its p bits at bits [p*phi, p*phi + p) of
+ *    the plane (a little-endian bit stream);
  *  - slot of (token t in the tile, coordinate i), g16 = r/16, rho = r%16:
  *      K side: i < 16*g16: phi = (i/16)*1024 + t*16 + i%16 (token-major in
  *              groups of 16 coordinates); else phi = 1024*g16 + t*rho + (i - 16*g16);
- *      V side: phi = i*64 + psi(t), psi(16a + 4c + e) = 16c + 4a + e;
+ *      V side: phi = i*64 + 16*(t/16) + pos_b(t%16), with pos_b(m) = m (b = 8),
+ *              8*(m/8) + 2*(m%4) + (m/4)%2 (b = 4), 4*(m%4) + m/4 (other b):
+ *              coordinate-major, each quarter of 16 tokens in a fixed order;
+ *    so a token's codes of a group of 16 coordinates (K) and a quarter of 16
+ *    tokens of one coordinate (V) are one bit field of 16p bits, unpacked by
+ *    the decode kernels straight into matrix-core operands;
  *  - kvc_encode writes only the slots of the tokens it encodes; slots of
  *    tokens never encoded keep the arena's contents (zero if the caller
  *    zeroed the arena, which the reference packing assumes).

@@ -83,17 +83,24 @@ static int n_planes(int b, int *w) {
     return n;
 }
 
-static int slot_of(int side, int t, int i, int r) {
+/* Position inside a run of 16 slots of the m-th item (V side token order; see oracle/layout.py). */
+static int pos_b(int b, int m) {
+    if (b == 8) return m;
+    if (b == 4) return 8 * (m / 8) + 2 * (m % 4) + (m / 4) % 2;
+    return 4 * (m % 4) + m / 4;
+}
+
+static int slot_of(int side, int t, int i, int r, int b) {
     if (side == 0) {
         int g16 = r / 16, rho = r % 16;
         if (i < 16 * g16) return (i / 16) * 1024 + t * 16 + i % 16;
         return 1024 * g16 + t * rho + (i - 16 * g16);
     }
-    int a = t / 16, c = (t / 4) % 4, e = t % 4;
-    return i * 64 + 16 * c + 4 * a + e;
+    return i * 64 + 16 * (t / 16) + pos_b(b, t % 16);
 }
 
-/* codes[t*r+i] (t < n) -> stream of ceil(n/64) tiles (zero-filled by this function). */
+/* codes[t*r+i] (t < n) -> stream of ceil(n/64) tiles (zero-filled by this function).
+ * Slot phi of a plane of width p holds its bits at [p*phi, p*phi + p) of the plane. */
 void oracle_pack(const uint8_t *codes, int n, int r, int b, int side, uint8_t *out) {
     int w[3];
     int np = n_planes(b, w);
@@ -107,19 +114,13 @@ void oracle_pack(const uint8_t *codes, int n, int r, int b, int side, uint8_t *o
             int p = w[k];
             int sh = 0;
             for (int k2 = k + 1; k2 < np; ++k2) sh += w[k2];
-            int per_word = 32 / p;
             for (int t = 0; t < 64; ++t) {
                 int tok = tile * 64 + t;
                 if (tok >= n) continue;
                 for (int i = 0; i < r; ++i) {
                     uint32_t v = (codes[(int64_t)tok * r + i] >> sh) & ((1u << p) - 1);
-                    int phi = slot_of(side, t, i, r);
-                    int word = phi / per_word, iota = phi % per_word;
-                    int bit = 8 * (iota % 4) + p * (iota / 4);
-                    uint8_t *wp = base + plane_off + 4 * word;
-                    uint32_t cur = (uint32_t)wp[0] | ((uint32_t)wp[1] << 8) | ((uint32_t)wp[2] << 16) | ((uint32_t)wp[3] << 24);
-                    cur |= v << bit;
-                    wp[0] = cur & 255; wp[1] = (cur >> 8) & 255; wp[2] = (cur >> 16) & 255; wp[3] = cur >> 24;
+                    int64_t bitpos = (int64_t)p * slot_of(side, t, i, r, b);
+                    base[plane_off + bitpos / 8] |= (uint8_t)(v << (bitpos % 8));
                 }
             }
             plane_off += 8LL * r * p;
@@ -142,13 +143,8 @@ void oracle_unpack(const uint8_t *stream, int n, int r, int b, int side, uint8_t
                 int p = w[k];
                 int sh = 0;
                 for (int k2 = k + 1; k2 < np; ++k2) sh += w[k2];
-                int per_word = 32 / p;
-                int phi = slot_of(side, t, i, r);
-                int word = phi / per_word, iota = phi % per_word;
-                int bit = 8 * (iota % 4) + p * (iota / 4);
-                const uint8_t *wp = base + plane_off + 4 * word;
-                uint32_t cur = (uint32_t)wp[0] | ((uint32_t)wp[1] << 8) | ((uint32_t)wp[2] << 16) | ((uint32_t)wp[3] << 24);
-                c |= ((cur >> bit) & ((1u << p) - 1)) << sh;
+                int64_t bitpos = (int64_t)p * slot_of(side, t, i, r, b);
+                c |= ((uint32_t)(base[plane_off + bitpos / 8] >> (bitpos % 8)) & ((1u << p) - 1)) << sh;
                 plane_off += 8LL * r * p;
             }
             codes[(int64_t)tok * r + i] = (uint8_t)c;

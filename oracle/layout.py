@@ -14,15 +14,19 @@ definition, and the oracle packs to it independently of the GPU encoder.
   binary expansion of b, widest plane first (7 -> 4,2,1). The widest plane
   holds the most significant bits. Plane of width p occupies 8*r*p bytes, the
   planes follow one another in that order.
-* Inside a plane: 2*r*p little-endian 32-bit words. Slot phi in [0, 64 r) lies
-  in word phi // (32/p); with iota = phi % (32/p) its bits start at
-  8 * (iota % 4) + p * (iota // 4).
+* Inside a plane, slot phi in [0, 64 r) holds its p bits at bits
+  [p*phi, p*phi + p) of the plane, counting bit n as bit n % 8 of byte n // 8
+  (a plain little-endian bit stream).
 * Slot of (token t in tile, coordinate i), with g16 = r // 16, rho = r % 16:
   K side: i < 16 g16:  phi = (i // 16) * 1024 + t * 16 + i % 16
-                       (token-major inside each group of 16 coordinates)
+                       (groups of 16 coordinates, token-major inside a group)
           otherwise:   phi = 1024 g16 + t * rho + (i - 16 g16)   (the tail group)
-  V side: phi = i * 64 + psi(t), psi(16 a + 4 c + e) = 16 c + 4 a + e
-  (coordinate-major with a fixed 4x4 transpose of the token order).
+  V side: phi = i * 64 + 16 * (t // 16) + pos_b(t % 16)
+          (coordinate-major; each quarter of 16 tokens in a fixed order that
+          depends on b only, see pos_b).
+* pos_b(m) is the position inside a run of 16 slots given to the m-th item:
+  b = 8: m; b = 4: 8 (m // 8) + 2 (m % 4) + (m // 4) % 2; any other b:
+  4 (m % 4) + m // 4 (a 4 x 4 transpose). It is an involution for b != 4.
 * Slots of tokens past the end of the last tile hold zero.
 """
 from __future__ import annotations
@@ -54,14 +58,17 @@ def stream_bytes(n_tok: int, r: int, b: int) -> int:
     return ((n_tok + TILE - 1) // TILE) * tile_bytes(r, b)
 
 
-def psi(t: int) -> int:
-    a, c, e = t // 16, (t // 4) % 4, t % 4
-    return 16 * c + 4 * a + e
+def pos_b(b: int, m: int) -> int:
+    if b == 8:
+        return m
+    if b == 4:
+        return 8 * (m // 8) + 2 * (m % 4) + (m // 4) % 2
+    return 4 * (m % 4) + m // 4
 
 
-def slot(side: int, t: int, i: int, r: int) -> int:
+def slot(side: int, t: int, i: int, r: int, b: int) -> int:
     if side == SIDE_V:
-        return i * TILE + psi(t)
+        return i * TILE + 16 * (t // 16) + pos_b(b, t % 16)
     g16, rho = r // 16, r % 16
     if i < 16 * g16:
         return (i // 16) * 1024 + t * 16 + i % 16
@@ -69,10 +76,9 @@ def slot(side: int, t: int, i: int, r: int) -> int:
 
 
 def slot_bit(phi: int, p: int) -> tuple[int, int]:
-    """(word index, bit offset) of slot phi in a plane of width p."""
-    per_word = 32 // p
-    iota = phi % per_word
-    return phi // per_word, 8 * (iota % 4) + p * (iota // 4)
+    """(byte index, bit offset inside that byte) of slot phi in a plane of width p."""
+    n = p * phi
+    return n // 8, n % 8
 
 
 def pack(codes, r: int, b: int, side: int) -> bytes:
@@ -85,17 +91,14 @@ def pack(codes, r: int, b: int, side: int) -> bytes:
         base = tile * tile_bytes(r, b)
         plane_off = 0
         for p, sh in zip(widths, shifts):
-            words = [0] * (2 * r * p)
             for t in range(TILE):
                 tok = tile * TILE + t
                 if tok >= n:
                     continue
                 for i in range(r):
                     v = (int(codes[tok][i]) >> sh) & ((1 << p) - 1)
-                    w, bit = slot_bit(slot(side, t, i, r), p)
-                    words[w] |= v << bit
-            for w, val in enumerate(words):
-                out[base + plane_off + 4 * w: base + plane_off + 4 * w + 4] = val.to_bytes(4, "little")
+                    byte, bit = slot_bit(slot(side, t, i, r, b), p)
+                    out[base + plane_off + byte] |= v << bit
             plane_off += 8 * r * p
     return bytes(out)
 
@@ -109,8 +112,7 @@ def unpack(stream: bytes, n: int, r: int, b: int, side: int) -> list[list[int]]:
         plane_off = 0
         for p, sh in zip(widths, shifts):
             for i in range(r):
-                w, bit = slot_bit(slot(side, t, i, r), p)
-                word = int.from_bytes(stream[base + plane_off + 4 * w: base + plane_off + 4 * w + 4], "little")
-                codes[tok][i] |= ((word >> bit) & ((1 << p) - 1)) << sh
+                byte, bit = slot_bit(slot(side, t, i, r, b), p)
+                codes[tok][i] |= ((stream[base + plane_off + byte] >> bit) & ((1 << p) - 1)) << sh
             plane_off += 8 * r * p
     return codes

@@ -1,5 +1,6 @@
 // Decode attention over the packed KV-COBRA cache on CDNA4 (gfx950): kernels
-// and the kvc_decode_attn launcher.
+// and the kvc_decode_attn launcher (table step 8; App. I, "Wall-clock at the
+// primitive level").
 //
 // The logits and the probability-weighted sum of values are dense contractions
 // in the rank space: S = Qt (G x r_K) . C_K^T (r_K x tokens) and
@@ -8,24 +9,27 @@
 //  * codes enter as int8 (raw codes for b <= 7; c - 128 for b = 8);
 //  * the rank-space query q~ = P_K q is split into three balanced base-254
 //    int8 limbs with a per-query scale (relative error ~1e-7 of max|q~|);
-//  * the softmax weights p in [0, 1] are quantised to 21 bits,
-//    P = round(p (2^21 - 1)), and split into three 7-bit limbs;
+//  * the softmax weights p in [0, 2^6] are quantised to P < 2^23 and split into
+//    three signed byte limbs, P = S0 + 2^8 S1 + 2^16 S2;
 //  * centring (c - 2^(b-1)) is exact in integers: the logits subtract
 //    2^(b-1) sum_i Q_i, and the value accumulator carries an all-ones virtual
 //    coordinate whose column gives sum_t P_t (also the softmax denominator).
-// Per work item = (unit, context chunk) one wavefront walks the chunk in 64-token
-// tiles. Each packed K and V tile is staged in LDS with coalesced 16-byte loads
-// (the next tile's loads are in flight while the current one is computed);
-// operand fragments are extracted from LDS by code instantiated per bit width
-// (one switch per tile and side). The logits take the q~ limbs as the A operand
-// (rows = head x limb) and the K codes as B (columns = tokens), so each lane
-// receives the three limbs of one (head, token) pair and forms the logit alone.
-// The online softmax keeps a lazily raised running max per query head; the
-// probabilities are split into limbs and written to LDS in the token order of the
-// V layout, where they are read back as the A operand of the PV products. Those
-// accumulate in int32 MFMA accumulators across the whole chunk and are rescaled in
-// place when a head's max grows. Centring and the limb sum happen once at the end
-// of the chunk. A second kernel merges the chunks and applies step_V and the V basis.
+//
+// One wavefront per work item = (unit, context chunk) walks the chunk in
+// 64-token tiles. Each lane loads the packed fields its operand fragments need
+// straight into registers with buffer loads at loop-invariant offsets (the
+// stream layout puts a token's codes of a group of 16 coordinates, and a
+// quarter of 16 tokens of one value coordinate, in one bit field whose
+// unpacking lands directly in MFMA operand order); the next tile's loads are in
+// flight while the current one is computed. Only the K-step holding the tail
+// group (r_K % 16 coordinates, token fields that are not word aligned) is staged
+// through LDS and read back with funnel shifts. The logit lane (query head,
+// column) receives the three limbs of one (head, token) logit and forms it alone;
+// the online softmax keeps a lazily raised running max per head; probability
+// limbs go through LDS into the A operand of the PV products, whose int32
+// accumulators hold every limb of one (head, coordinate) in one lane, so a raise
+// of the max rescales them exactly in place. A second kernel merges the chunks
+// and applies step_V and the V basis.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -40,106 +44,445 @@ namespace kvc {
 constexpr int kD = KVC_HEAD_DIM;
 constexpr int kTile = KVC_TILE_TOKENS;
 constexpr int kPartStride = 132;  // floats per (item, query head): m, l, pad, pad, acc[128]
-constexpr int kAccStride = 132;   // LDS fp32 accumulator row: coordinates 0..127, 128 = all-ones column
 constexpr int kLimbs = 3;
-constexpr float kLazy = 6.f;               // the running max is raised only when a tile beats it by > 2^6
-constexpr float kPScale = 32767.984375f;   // (2^21 - 1) / 2^6: p <= 2^6 maps to P < 2^21
+constexpr float kLazy = 6.f;              // the running max is raised only when a tile beats it by > 2^6
+constexpr float kPScale = 130047.96875f;  // (2^23 - 2^16 - 2) / 2^6: p <= 2^6 maps to P < 2^23 - 2^16
+constexpr float kPBias = 32896.5f;        // 0x8080 (offsets of the two signed low limbs) + 1/2 (rounding)
+// Tiles per chunk at most: |S_l c| <= 2^14 per token keeps the int32 accumulators below 2^31
+// (2^28 per chunk, plus at most 2^29 carried by a rescale).
+constexpr int kMaxChunkTiles = 256;
+constexpr int kPRowBytes = 80;            // LDS row of the probability limbs (64 tokens + pad)
+constexpr uint32_t kLaneOOB = 0x10000000u;  // lane offset (in plane-width units) past any stream
+constexpr int kRsrcWord3 = 0x00020000;    // raw buffer, 32-bit data format (gfx9 family)
 
 typedef int32_t v4i __attribute__((ext_vector_type(4)));
+typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+typedef uint32_t v2u __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ v4i mfma_i8(v4i a, v4i b, v4i c) {
     return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);
 }
+__device__ __forceinline__ uint32_t perm(uint32_t hi, uint32_t lo, uint32_t sel) {
+    return __builtin_amdgcn_perm(hi, lo, sel);
+}
+__device__ __forceinline__ uint32_t funnel(uint32_t hi, uint32_t lo, uint32_t sh) {
+    return __builtin_amdgcn_alignbit(hi, lo, sh);
+}
 
-// Value of lane (lane + n) mod 16 within each row of 16 lanes (DPP row rotate).
+// Maximum over the 16 lanes of a DPP row (row rotations).
 template <int N>
 __device__ __forceinline__ float row_ror(float v) {
-    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x120 + N, 0xf, 0xf, false));
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x120 + N, 0xf, 0xf, true));
+}
+__device__ __forceinline__ float row_max(float m) {
+    m = fmaxf(m, row_ror<8>(m));
+    m = fmaxf(m, row_ror<4>(m));
+    m = fmaxf(m, row_ror<2>(m));
+    return fmaxf(m, row_ror<1>(m));
 }
 
-__device__ __forceinline__ constexpr uint32_t plane_mask(int p) {
-    return p == 8 ? 0xffffffffu : (p == 4 ? 0x0f0f0f0fu : (p == 2 ? 0x03030303u : 0x01010101u));
+// The partial kernel's work-group is one wavefront, whose LDS accesses execute in program order:
+// between an LDS write and a read of the same bytes only the compiler's reordering of memory
+// operations has to be stopped, which a wavefront-scope fence does without any wait.
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    __builtin_amdgcn_wave_barrier();
 }
 
-// 16 slots [phi0, phi0 + 16) of one plane of width P, phi0 a multiple of 16:
-// dword d, byte j holds the plane value of slot phi0 + 4d + j.
-template <int P>
-__device__ __forceinline__ void plane_frag16(const uint8_t* __restrict__ plane, int phi0, uint32_t d[4]) {
-    constexpr uint32_t M = plane_mask(P);
-    if constexpr (P == 8) {
-        const uint4 w = *reinterpret_cast<const uint4*>(plane + phi0);
-        d[0] = w.x; d[1] = w.y; d[2] = w.z; d[3] = w.w;
-    } else if constexpr (P == 4) {
-        const uint2 w = *reinterpret_cast<const uint2*>(plane + (phi0 >> 1));
-        d[0] = w.x & M; d[1] = (w.x >> 4) & M; d[2] = w.y & M; d[3] = (w.y >> 4) & M;
-    } else if constexpr (P == 2) {
-        const uint32_t w = *reinterpret_cast<const uint32_t*>(plane + (phi0 >> 2));
-        d[0] = w & M; d[1] = (w >> 2) & M; d[2] = (w >> 4) & M; d[3] = (w >> 6) & M;
-    } else {
-        const uint32_t w = *reinterpret_cast<const uint32_t*>(plane + ((phi0 >> 5) << 2)) >> ((phi0 & 16) >> 2);
-        d[0] = w & M; d[1] = (w >> 1) & M; d[2] = (w >> 2) & M; d[3] = (w >> 3) & M;
-    }
-}
+// ---------------------------------------------------------------- field unpacking
 
-template <int B, int K>
-__device__ __forceinline__ void add_plane16(const uint8_t* __restrict__ tile, int r, int phi0, uint32_t acc[4]) {
-    if constexpr (K < n_planes(B)) {
-        uint32_t f[4];
-        plane_frag16<plane_w(B, K)>(tile + 8 * r * plane_off(B, K), phi0, f);
+// One token's field (16 codes) of one plane: up to four 32-bit words, bit 0 aligned.
+struct Fld {
+    uint32_t w0, w1, w2, w3;
+};
+
+// The 16 codes of a field as int8 operand bytes: byte k of dword d holds the code at position
+// kidx_b^-1(4 d + k) of the field, i.e. operand index 4 d + k <-> position pos_b(4 d + k).
+// f[k] is plane k's field (widest first); hi1 selects the upper 16 bits of the word of a 1-bit
+// plane (two tokens share a word there). b = 8 codes come out centred (c - 128).
+template <int B>
+__device__ __forceinline__ v4i unpack16(const Fld (&f)[3], bool hi1) {
+    uint32_t D[4];
+    if constexpr (B == 8) {
+        D[0] = f[0].w0 ^ 0x80808080u;
+        D[1] = f[0].w1 ^ 0x80808080u;
+        D[2] = f[0].w2 ^ 0x80808080u;
+        D[3] = f[0].w3 ^ 0x80808080u;
+    } else if constexpr (B == 4) {  // nibble order
+        constexpr uint32_t M = 0x0f0f0f0fu;
+        D[0] = f[0].w0 & M;
+        D[1] = (f[0].w0 >> 4) & M;
+        D[2] = f[0].w1 & M;
+        D[3] = (f[0].w1 >> 4) & M;
+    } else {  // position 4 k + d -> byte k of dword d, for every plane
+        D[0] = D[1] = D[2] = D[3] = 0u;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[j] |= f[j] << plane_sh(B, K);
+        for (int k = 0; k < n_planes(B); ++k) {
+            const int P = plane_w(B, k), SH = plane_sh(B, k);
+            uint32_t E[4];
+            if (P == 4) {
+                constexpr uint32_t M = 0x0f0f0f0fu;
+                const uint32_t t02 = perm(f[k].w1, f[k].w0, 0x06040200u), t13 = perm(f[k].w1, f[k].w0, 0x07050301u);
+                E[0] = t02 & M;
+                E[1] = (t02 >> 4) & M;
+                E[2] = t13 & M;
+                E[3] = (t13 >> 4) & M;
+            } else if (P == 2) {
+                constexpr uint32_t M = 0x03030303u;
+#pragma unroll
+                for (int d = 0; d < 4; ++d) E[d] = (f[k].w0 >> (2 * d)) & M;
+            } else {
+                constexpr uint32_t M = 0x01010101u;
+                const uint32_t x = perm(f[k].w0 >> 4, f[k].w0, hi1 ? 0x07030602u : 0x05010400u);
+#pragma unroll
+                for (int d = 0; d < 4; ++d) E[d] = (x >> d) & M;
+            }
+#pragma unroll
+            for (int d = 0; d < 4; ++d) D[d] |= E[d] << SH;
+        }
+    }
+    return v4i{(int)D[0], (int)D[1], (int)D[2], (int)D[3]};
+}
+
+// Words of a K-step held per lane: 8 p bytes per plane of width p, either the fields of the lane's
+// four tokens (direct) or its share of the staged region (the K-step holding the tail group: the
+// plane's bytes from 512 p ks on, at most 496 p of them, 8 p bytes per lane).
+__host__ __device__ constexpr int k_step_words(int b) { return 2 * b; }
+__host__ __device__ constexpr int plane_stage_off(int b, int k) { return 512 * plane_off(b, k); }  // LDS bytes
+constexpr int kKBufWords = 16;  // prefetch registers per side
+__host__ __device__ constexpr bool k_prefetch_both(int b) { return 2 * k_step_words(b) <= kKBufWords; }
+// words of one value N-tile field per lane, and N-tiles prefetched
+__host__ __device__ constexpr int v_words(int b) {
+    return b == 8 ? 4 : ((b & 4 ? 2 : 0) + (b & 2 ? 1 : 0) + (b & 1 ? 1 : 0));
+}
+constexpr int kVBufWords = 16;  // value prefetch registers
+constexpr int kPrefetchDepth = 2;  // tiles of K and V loads in flight ahead of the one being processed
+__host__ __device__ constexpr int v_prefetch_tiles(int b) { return kVBufWords / v_words(b) < 8 ? kVBufWords / v_words(b) : 8; }
+
+// Direct loads of one K-step's fields into w[0 .. 2B).
+template <int B>
+__device__ __forceinline__ void k_load_direct(const __amdgpu_buffer_rsrc_t rs, int r, uint32_t lk, uint32_t* w) {
+    int o = 0;
+#pragma unroll
+    for (int k = 0; k < n_planes(B); ++k) {
+        const int P = plane_w(B, k);
+        const int voff = (int)(P * lk) + 8 * r * plane_off(B, k);
+        if (P == 1) {
+            const v2u v = __builtin_amdgcn_raw_buffer_load_b64(rs, voff, 0, 0);
+            w[o] = v[0];
+            w[o + 1] = v[1];
+        } else {
+#pragma unroll
+            for (int q = 0; q < P / 2; ++q) {
+                const v4u v = __builtin_amdgcn_raw_buffer_load_b128(rs, voff + 16 * q, 0, 0);
+                w[o + 4 * q] = v[0];
+                w[o + 4 * q + 1] = v[1];
+                w[o + 4 * q + 2] = v[2];
+                w[o + 4 * q + 3] = v[3];
+            }
+        }
+        o += 2 * P;
     }
 }
 
-// Codes of 16 aligned slots of a tile (rank r, B bits), one byte each; b = 8 codes are
-// returned centred (c - 128) so that they fit int8.
+// The lane's share of the staged region goes to LDS at 8 p lane of the plane's area.
 template <int B>
-__device__ __forceinline__ v4i code_frag16(const uint8_t* __restrict__ tile, int r, int phi0) {
-    uint32_t acc[4] = {0, 0, 0, 0};
-    add_plane16<B, 0>(tile, r, phi0, acc);
-    add_plane16<B, 1>(tile, r, phi0, acc);
-    add_plane16<B, 2>(tile, r, phi0, acc);
-    constexpr uint32_t X = B == 8 ? 0x80808080u : 0u;
-    return v4i{(int)(acc[0] ^ X), (int)(acc[1] ^ X), (int)(acc[2] ^ X), (int)(acc[3] ^ X)};
+__device__ __forceinline__ void k_write_stage(const uint32_t* w, uint8_t* __restrict__ stage, int lane) {
+    int o = 0;
+#pragma unroll
+    for (int k = 0; k < n_planes(B); ++k) {
+        const int P = plane_w(B, k);
+        uint8_t* dst = stage + plane_stage_off(B, k) + 8 * P * lane;
+        if (P == 1) {
+            *reinterpret_cast<v2u*>(dst) = v2u{w[o], w[o + 1]};
+        } else {
+#pragma unroll
+            for (int q = 0; q < P / 2; ++q)
+                *reinterpret_cast<v4u*>(dst + 16 * q) = v4u{w[o + 4 * q], w[o + 4 * q + 1], w[o + 4 * q + 2], w[o + 4 * q + 3]};
+        }
+        o += 2 * P;
+    }
 }
 
-template <int B, int K>
-__device__ __forceinline__ uint32_t plane_subdword(const uint8_t* __restrict__ tile, int r, int sd) {
-    if constexpr (K < n_planes(B)) {
-        constexpr int P = plane_w(B, K);
-        constexpr int SPW = 8 / P;  // sub-dwords per word
-        const uint32_t w = reinterpret_cast<const uint32_t*>(tile + 8 * r * plane_off(B, K))[sd / SPW];
-        return ((w >> (P * (sd % SPW))) & plane_mask(P)) << plane_sh(B, K);
+// Operand fragment of token st (0..3 of the lane's four) from one K-step's directly loaded fields.
+template <int B>
+__device__ __forceinline__ v4i k_frag_direct(const uint32_t* w, int st) {
+    Fld f[3];
+    int o = 0;
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+        if (k < n_planes(B)) {
+            const int P = plane_w(B, k);
+            if (P == 1) f[k] = Fld{w[o + (st >> 1)], 0u, 0u, 0u};
+            else if (P == 2) f[k] = Fld{w[o + st], 0u, 0u, 0u};
+            else if (P == 4) f[k] = Fld{w[o + 2 * st], w[o + 2 * st + 1], 0u, 0u};
+            else f[k] = Fld{w[o + 4 * st], w[o + 4 * st + 1], w[o + 4 * st + 2], w[o + 4 * st + 3]};
+            o += 2 * P;
+        } else {
+            f[k] = Fld{0u, 0u, 0u, 0u};
+        }
+    }
+    return unpack16<B>(f, (st & 1) != 0);
+}
+
+// Operand fragment of a token from the staged K-step: its field of plane k starts at bit p * x of the
+// plane's staged region.
+template <int B>
+__device__ __forceinline__ v4i k_frag_staged(const uint8_t* __restrict__ stage, uint32_t x) {
+    Fld f[3];
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+        if (k < n_planes(B)) {
+            const int P = plane_w(B, k);
+            const uint32_t bit = x * (uint32_t)P;
+            const uint32_t* s32 = reinterpret_cast<const uint32_t*>(stage + plane_stage_off(B, k)) + (bit >> 5);
+            const uint32_t d0 = s32[0], d1 = s32[1];
+            if (P <= 2) {
+                f[k] = Fld{funnel(d1, d0, bit), 0u, 0u, 0u};
+            } else if (P == 4) {
+                const uint32_t d2 = s32[2];
+                f[k] = Fld{funnel(d1, d0, bit), funnel(d2, d1, bit), 0u, 0u};
+            } else {
+                const uint32_t d2 = s32[2], d3 = s32[3], d4 = s32[4];
+                f[k] = Fld{funnel(d1, d0, bit), funnel(d2, d1, bit), funnel(d3, d2, bit), funnel(d4, d3, bit)};
+            }
+        } else {
+            f[k] = Fld{0u, 0u, 0u, 0u};
+        }
+    }
+    return unpack16<B>(f, false);
+}
+
+template <int B>
+__device__ __forceinline__ void k_fetch(uint32_t* w, const __amdgpu_buffer_rsrc_t rs, int rk, uint32_t lk) {
+    k_load_direct<B>(rs, rk, lk, w);
+}
+
+// Prefetch of a unit's first tile (both K-steps, for the widths whose two K-steps fit the prefetch
+// registers; wider codes are loaded when their tile is processed).
+template <int B>
+__device__ __forceinline__ void k_prefetch(uint32_t (&kb)[kKBufWords], const __amdgpu_buffer_rsrc_t rs, int rk, int nk,
+                                           int ks_t, const uint32_t (&LK)[2], int lane) {
+    constexpr int W0 = k_step_words(B);
+    (void)nk;
+    if constexpr (k_prefetch_both(B)) {
+        k_fetch<B>(kb, rs, rk, LK[0]);
+        k_fetch<B>(kb + W0, rs, rk, LK[1]);
+    }
+}
+
+// Logit of token 4 col + st for the lane's heads: three int32 limb sums -> log2-domain value + off.
+template <int LM>
+__device__ __forceinline__ void logit_of(const v4i (&acc)[LM], const float (&k0)[LM], const float (&k1)[LM],
+                                         const float (&k2)[LM], const float (&off)[LM], float (&s)[LM][4], int st) {
+#pragma unroll
+    for (int lm = 0; lm < LM; ++lm) {
+        float v = fmaf((float)acc[lm][2], k2[lm], off[lm]);
+        v = fmaf((float)acc[lm][1], k1[lm], v);
+        s[lm][st] = fmaf((float)acc[lm][0], k0[lm], v);
+    }
+}
+
+// Logits of one tile: s[lm][st] = logit + off for the lane's four tokens. The K-step holding the tail
+// group (if any) is staged in LDS; its token fields start at plane-width units xb + st xs. For the
+// widths whose two K-steps are prefetched, each token column is finished right after its MFMAs and
+// the next tile's fields are loaded into the freed registers; wider codes load each K-step here.
+template <int B, int LM, int KM>
+__device__ __forceinline__ void k_tile(uint32_t (&kb)[kKBufWords], uint32_t (&kb_next)[kKBufWords], bool stage_next,
+                                       const __amdgpu_buffer_rsrc_t rs,
+                                       const __amdgpu_buffer_rsrc_t rs_n, int rk, int nk_rt, int ks_t_rt,
+                                       const uint32_t (&LK)[2], uint32_t xb, uint32_t xs, int lane,
+                                       uint8_t* __restrict__ stage, const v4i (&qa)[2][LM], const float (&k0)[LM],
+                                       const float (&k1)[LM], const float (&k2)[LM], const float (&off)[LM],
+                                       float (&s)[LM][4]) {
+    constexpr int W0 = k_step_words(B);
+    // K-step structure fixed at compile time when KM >= 0 (see k_mode), else taken at run time
+    const int nk = KM >= 0 ? (KM < 2 ? 2 : 1) : nk_rt;
+    const int ks_t = KM >= 0 ? (KM == 1 ? 1 : (KM == 3 ? 0 : 2)) : ks_t_rt;
+    if constexpr (k_prefetch_both(B)) {
+        // The staged K-step goes to LDS first (constant indices into kb: a runtime one would move the
+        // array to scratch memory). Every load below is issued unconditionally, in the same order on
+        // every tile (absent K-steps read past the stream and return zero), so that the wait for a
+        // tile's data counts exactly the younger loads still in flight.
+        // The staged K-step of this tile is already in LDS when the caller staged it one tile ahead
+        // (stage_next on the previous tile); otherwise it is written now.
+        if (!stage_next) {
+            if (ks_t == 0) {
+                k_write_stage<B>(kb, stage, lane);
+                wave_lds_sync();
+            } else if (ks_t == 1 && nk > 1) {
+                k_write_stage<B>(kb + W0, stage, lane);
+                wave_lds_sync();
+            }
+        }
+#pragma unroll
+        for (int st = 0; st < 4; ++st) {
+            v4i acc[LM];
+            {
+                const v4i bk = ks_t == 0 ? k_frag_staged<B>(stage, xb + st * xs) : k_frag_direct<B>(kb, st);
+#pragma unroll
+                for (int lm = 0; lm < LM; ++lm) acc[lm] = mfma_i8(qa[0][lm], bk, v4i{0, 0, 0, 0});
+            }
+            if (nk > 1) {
+                const v4i bk = ks_t == 1 ? k_frag_staged<B>(stage, xb + st * xs) : k_frag_direct<B>(kb + W0, st);
+#pragma unroll
+                for (int lm = 0; lm < LM; ++lm) acc[lm] = mfma_i8(qa[1][lm], bk, acc[lm]);
+            }
+            logit_of<LM>(acc, k0, k1, k2, off, s, st);
+        }
+        k_load_direct<B>(rs_n, rk, LK[0], kb);
+        k_load_direct<B>(rs_n, rk, LK[1], kb + W0);
+        // stage the next tile's K-step (loaded into the other register set one tile ago) now, away from
+        // the loop head
+        if (stage_next) {
+            wave_lds_sync();
+            if (ks_t == 0) k_write_stage<B>(kb_next, stage, lane);
+            else if (ks_t == 1 && nk > 1) k_write_stage<B>(kb_next + W0, stage, lane);
+            wave_lds_sync();
+        }
     } else {
-        return 0u;
+        v4i S[LM][4];
+#pragma unroll
+        for (int lm = 0; lm < LM; ++lm)
+#pragma unroll
+            for (int st = 0; st < 4; ++st) S[lm][st] = v4i{0, 0, 0, 0};
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            if (ks >= nk) break;
+            k_fetch<B>(kb, rs, rk, LK[ks]);
+            if (ks == ks_t) {
+                k_write_stage<B>(kb, stage, lane);
+                wave_lds_sync();
+            }
+#pragma unroll
+            for (int st = 0; st < 4; ++st) {
+                const v4i bk = ks == ks_t ? k_frag_staged<B>(stage, xb + st * xs) : k_frag_direct<B>(kb, st);
+#pragma unroll
+                for (int lm = 0; lm < LM; ++lm) S[lm][st] = mfma_i8(qa[ks][lm], bk, S[lm][st]);
+            }
+            if (ks == ks_t) wave_lds_sync();
+        }
+#pragma unroll
+        for (int st = 0; st < 4; ++st) {
+            v4i acc[LM];
+#pragma unroll
+            for (int lm = 0; lm < LM; ++lm) acc[lm] = S[lm][st];
+            logit_of<LM>(acc, k0, k1, k2, off, s, st);
+        }
     }
 }
 
-// Codes of the 4 slots of sub-dword sd of a tile (any alignment), one byte each (b = 8 centred).
+// Value field words of N-tile nt for this lane (coordinate 16 nt + col, tokens 16 grp + ...).
 template <int B>
-__device__ __forceinline__ uint32_t code_subdword(const uint8_t* __restrict__ tile, int r, int sd) {
-    return (plane_subdword<B, 0>(tile, r, sd) | plane_subdword<B, 1>(tile, r, sd) | plane_subdword<B, 2>(tile, r, sd)) ^
-           (B == 8 ? 0x80808080u : 0u);
+__device__ __forceinline__ void v_load(const __amdgpu_buffer_rsrc_t rs, int r, uint32_t lv, int nt, uint32_t* w) {
+    int o = 0;
+#pragma unroll
+    for (int k = 0; k < n_planes(B); ++k) {
+        const int P = plane_w(B, k);
+        const int voff = (int)(P * lv) + 8 * r * plane_off(B, k) + 128 * P * nt;
+        if (P == 1) {
+            w[o++] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(rs, voff, 0, 0);
+        } else if (P == 2) {
+            w[o++] = __builtin_amdgcn_raw_buffer_load_b32(rs, voff, 0, 0);
+        } else if (P == 4) {
+            const v2u v = __builtin_amdgcn_raw_buffer_load_b64(rs, voff, 0, 0);
+            w[o++] = v[0];
+            w[o++] = v[1];
+        } else {
+            const v4u v = __builtin_amdgcn_raw_buffer_load_b128(rs, voff, 0, 0);
+            w[o++] = v[0];
+            w[o++] = v[1];
+            w[o++] = v[2];
+            w[o++] = v[3];
+        }
+    }
+}
+
+template <int B>
+__device__ __forceinline__ v4i v_frag(const uint32_t* w) {
+    Fld f[3];
+    int o = 0;
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+        if (k < n_planes(B)) {
+            const int P = plane_w(B, k);
+            if (P <= 2) f[k] = Fld{w[o], 0u, 0u, 0u};
+            else if (P == 4) f[k] = Fld{w[o], w[o + 1], 0u, 0u};
+            else f[k] = Fld{w[o], w[o + 1], w[o + 2], w[o + 3]};
+            o += P <= 2 ? 1 : P / 2;
+        } else {
+            f[k] = Fld{0u, 0u, 0u, 0u};
+        }
+    }
+    return unpack16<B>(f, false);
+}
+
+template <int B>
+__device__ __forceinline__ void v_prefetch(uint32_t (&vb)[kVBufWords], const __amdgpu_buffer_rsrc_t rs, int r,
+                                           uint32_t lv, int nv) {
+    constexpr int VW = v_words(B);
+    (void)nv;
+#pragma unroll
+    for (int nt = 0; nt < v_prefetch_tiles(B); ++nt) v_load<B>(rs, r, lv, nt, vb + nt * VW);
+}
+
+// PV MFMAs of one tile (N-tiles nt < nv; the first v_prefetch_tiles come from the prefetched
+// words, the rest are loaded here), then the next tile's prefetch (rs_next; a zero-sized
+// descriptor when there is none).
+template <int B, int LM>
+__device__ __forceinline__ void v_tile(uint32_t* vb, const __amdgpu_buffer_rsrc_t rs, const __amdgpu_buffer_rsrc_t rs_next,
+                                       int r, uint32_t lv, int nv, const v4i (&ap)[LM], v4i (&C)[LM][9]) {
+    constexpr int VW = v_words(B), NPF = v_prefetch_tiles(B);
+    // Every N-tile is processed, also those past the rank (their loads read beyond the plane, bounded
+    // by the stream, into accumulator columns that are never output): no branches, and every tile
+    // issues the same loads in the same order, so the waits for a tile's data stay exact.
+    (void)nv;
+#pragma unroll
+    for (int nt = 0; nt < 8; ++nt) {
+        uint32_t w[4];
+        if (nt < NPF) {
+#pragma unroll
+            for (int q = 0; q < VW; ++q) w[q] = vb[nt * VW + q];
+        } else {
+            v_load<B>(rs, r, lv, nt, w);
+        }
+        const v4i bv = v_frag<B>(w);
+#pragma unroll
+        for (int pm = 0; pm < LM; ++pm) C[pm][nt] = mfma_i8(ap[pm], bv, C[pm][nt]);
+        if (nt < NPF) v_load<B>(rs_next, r, lv, nt, vb + nt * VW);
+    }
 }
 
 // ---------------------------------------------------------------- q~ limbs
 
-// Per unit and query head: q~ = (step_K log2(e) / sqrt(d)) P_K q, its scale
-// sigma = max|q~| / 127 and three int8 limbs with q~ ~ sigma (L0 + L1/254 + L2/254^2);
-// corr[limb][g] = 2^(b_K - 1) sum_i L_limb,i (0 for b_K = 8, whose codes are centred on load).
-__global__ __launch_bounds__(kD) void qprep_kernel(DevSide K, const uint16_t* __restrict__ q, int G,
-                                                   int8_t* __restrict__ qlimb, float* __restrict__ qscale,
-                                                   int32_t* __restrict__ qcorr) {
-    __shared__ float qsh[16][kD];
+// Per unit: q~_g = (step_K log2(e) / sqrt(d)) P_K q_g, sigma_g = max|q~_g| / 127 and three int8
+// limbs with q~ ~ sigma (L0 + L1/254 + L2/254^2). The limbs are written as the logit MFMA's A
+// operand of every lane: qa[u][ks][lm][lane] = 16 bytes, lane (grp, row = 4 (h % 4) + limb), lm = h / 4,
+// operand byte m <-> coordinate 16 (4 ks + grp) + pos_b(m) (zero outside the rank, for limb 3 and for
+// heads >= G). qk[u][h] = (sigma, sigma / 254, sigma / 254^2, bias) with
+// bias = -2^(b-1) sum_limb k_limb sum_i L_limb,i (0 for b = 8, whose codes are centred on load).
+__global__ __launch_bounds__(kD) void qprep_kernel(DevSide K, const uint16_t* __restrict__ q, int G, int LM,
+                                                   v4i* __restrict__ qa, float4* __restrict__ qk) {
+    extern __shared__ float qsm[];
+    float* qsh = qsm;                                                  // [G][128]
+    uint8_t* img = reinterpret_cast<uint8_t*>(qsh + G * kD);           // [2][LM][64][16] operand image
     __shared__ float fred[kD / 64];
     __shared__ int ired[kLimbs][kD / 64];
     const int u = blockIdx.x, i = threadIdx.x, lane = i & 63, wv = i >> 6;
-    for (int g = 0; g < G; ++g) qsh[g][i] = h2f(q[((int64_t)u * G + g) * kD + i]);
+    for (int g = 0; g < G; ++g) qsh[g * kD + i] = h2f(q[((int64_t)u * G + g) * kD + i]);
+    const int img_words = 2 * LM * 64 * 4;
+    for (int k = i; k < img_words; k += kD) reinterpret_cast<uint32_t*>(img)[k] = 0u;
     __syncthreads();
     const int r = K.r[u], b = K.b[u];
     const int hk = b == 8 ? 0 : (1 << (b - 1));
     const float scale0 = K.delta[u] * 1.4426950408889634f * 0.08838834764831845f;  // log2(e) / sqrt(128)
-    // basis row i, read once with 16-byte loads
+    // destination of coordinate i in the operand image
+    const int g16 = r >> 4;
+    const int cg = i < 16 * g16 ? (i >> 4) : g16;
+    const int jpos = i - 16 * cg;
+    const int ks = cg >> 2, grp = cg & 3;
+    int kidx = 0;
+    KVC_SWITCH_B(b, kidx = kidx_b(B_, jpos));
     float prow[kD];
     {
         const uint4* P4 = reinterpret_cast<const uint4*>(K.basis + K.basis_off[u] + (int64_t)(i < r ? i : 0) * kD);
@@ -157,7 +500,7 @@ __global__ __launch_bounds__(kD) void qprep_kernel(DevSide K, const uint16_t* __
     for (int g = 0; g < G; ++g) {
         float acc = 0.f;
 #pragma unroll
-        for (int j = 0; j < kD; ++j) acc = fmaf(prow[j], qsh[g][j], acc);
+        for (int j = 0; j < kD; ++j) acc = fmaf(prow[j], qsh[g * kD + j], acc);
         const float qt = acc * scale0;
         float m = fabsf(qt);
         for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
@@ -174,88 +517,339 @@ __global__ __launch_bounds__(kD) void qprep_kernel(DevSide K, const uint16_t* __
         const int L[kLimbs] = {(int)l0, (int)l1, (int)l2};
 #pragma unroll
         for (int k = 0; k < kLimbs; ++k) {
-            qlimb[(((int64_t)u * kLimbs + k) * G + g) * kD + i] = (int8_t)L[k];
+            if (i < r) {
+                const int row_lane = 16 * grp + 4 * (g & 3) + k;
+                img[(((ks * LM + (g >> 2)) * 64 + row_lane) << 4) + kidx] = (uint8_t)(int8_t)L[k];
+            }
             int s = L[k];
             for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
             if (lane == 0) ired[k][wv] = s;
         }
         __syncthreads();
-        if (i < kLimbs) qcorr[((int64_t)u * kLimbs + i) * G + g] = hk * (ired[i][0] + ired[i][1]);
-        if (i == 0) qscale[(int64_t)u * G + g] = sigma;
+        if (i == 0) {
+            const float k0 = sigma, k1 = sigma * (1.f / 254.f), k2 = sigma * (1.f / 64516.f);
+            const float bias = -(float)hk * ((float)(ired[0][0] + ired[0][1]) * k0 + (float)(ired[1][0] + ired[1][1]) * k1 +
+                                             (float)(ired[2][0] + ired[2][1]) * k2);
+            qk[(int64_t)u * G + g] = float4{k0, k1, k2, bias};
+        }
         __syncthreads();
     }
+    v4i* dst = qa + (int64_t)u * 2 * LM * 64;
+    for (int k = i; k < 2 * LM * 64; k += kD) dst[k] = reinterpret_cast<const v4i*>(img)[k];
 }
 
 // ---------------------------------------------------------------- partials
 
 template <int G> struct Shape {
-    static constexpr int LM = (4 * G + 15) / 16;       // logit M-tiles: row 4 h + limb (limb 3 is zero)
-    static constexpr int PM = (kLimbs * G + 15) / 16;  // PV M-tiles: row limb * G + h
-    static constexpr int NV = kD / 16 + 1;             // V N-tiles incl. the all-ones coordinate
+    static constexpr int LM = (G + 3) / 4;  // M-tiles of 16 rows = 4 heads x 4 limb slots (logits and PV)
     // Wavefronts per SIMD the register budget is cut for (512 / W registers per lane, no spills).
-    static constexpr int W = G == 1 || G == 4 ? 4 : (G == 2 ? 3 : (G == 8 ? 2 : 1));
+    static constexpr int W = G <= 4 ? 3 : (G == 8 ? 2 : 1);
 };
 
-// Token of logit column col in sub-tile st. With this order a lane's four tokens (st = 0..3) sit at
-// the consecutive V slots 4 col + st of the token permutation psi, so its probability limbs go to
-// LDS as one dword per limb.
-__device__ __forceinline__ int tok_of(int st, int col) { return 16 * (col & 3) + 4 * (col >> 2) + st; }
+// Runs a KVC_SWITCH_B-style CALL with B_ = the compile-time width BKc (BVc), or switches on the
+// runtime width when it is 0.
+#define KVC_SW_K(CALL)                                          \
+    if constexpr (BKc != 0) {                                   \
+        constexpr int B_ = BKc;                                 \
+        CALL;                                                   \
+    } else {                                                    \
+        KVC_SWITCH_B(bk, CALL);                                 \
+    }
+#define KVC_SW_V(CALL)                                          \
+    if constexpr (BVc != 0) {                                   \
+        constexpr int B_ = BVc;                                 \
+        CALL;                                                   \
+    } else {                                                    \
+        KVC_SWITCH_B(bv, CALL);                                 \
+    }
 
-// K tail group (r_K % 16 coordinates) of the staged tile, transposed to [token][16] bytes in LDS.
-template <int BK>
-__device__ __forceinline__ void k_tail(const uint8_t* __restrict__ ktile, int rk, uint8_t* __restrict__ tail, int lane) {
+// One work item (unit u, context chunk [start, end)) with the K and V bit widths fixed at compile
+// time (BKc, BVc in 1..4), or switched per tile (0: the general path for widths above 4).
+extern __shared__ __attribute__((aligned(16))) uint8_t kvc_dsm[];
+
+// K-step structure of a rank: 0: two K-steps, no tail group; 1: two K-steps, the tail group in the
+// second; 2: one K-step, no tail group; 3: one K-step holding the tail group.
+__host__ __device__ constexpr int k_mode(int r) {
+    return r > 64 ? ((r & 15) ? 1 : 0) : ((r & 15) ? 3 : 2);
+}
+
+// Wave-uniform copies (a non-inlined function receives its arguments in vector registers).
+__device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
+__device__ __forceinline__ const uint8_t* uni(const uint8_t* p) {
+    const uint64_t a = reinterpret_cast<uint64_t>(p);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a), hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
+    return reinterpret_cast<const uint8_t*>(((uint64_t)hi << 32) | lo);
+}
+
+template <int G, int BKc, int BVc, int KM>
+__device__ __noinline__ void run_item(const DevSide& K, const DevSide& V, const v4i* __restrict__ qa_ws,
+                                         const float4* __restrict__ qk_ws, int k_cap_tiles, int v_cap_tiles, int u,
+                                         int start, int end, float* __restrict__ out, int lane) {
+    constexpr int LM = Shape<G>::LM;
+    uint8_t* pmat = kvc_dsm;                            // [16 LM][kPRowBytes] probability limbs
+    uint8_t* stage = kvc_dsm + 16 * LM * kPRowBytes;    // staged tail K-step
+    const int col = lane & 15, grp = lane >> 4;
+    u = uni(u);
+    start = uni(start);
+    end = uni(end);
+    k_cap_tiles = uni(k_cap_tiles);
+    v_cap_tiles = uni(v_cap_tiles);
+    const int rk = uni(K.r[u]), bk = uni(K.b[u]), rv = uni(V.r[u]), bv = uni(V.b[u]);
+    const int hv = bv == 8 ? 0 : (1 << (bv - 1));
+    const int nk = (rk + 63) >> 6, nv = (rv + 15) >> 4;
     const int g16 = rk >> 4, rho = rk & 15;
-    const float inv_rho = 1.f / (float)rho;
-    const int base_sd = g16 << 8;  // first sub-dword of the tail (slot 1024 g16)
-    for (int sd = lane; sd < 16 * rho; sd += 64) {
-        const uint32_t cw = code_subdword<BK>(ktile, rk, base_sd + sd);
-        const int q0 = 4 * sd, q1 = q0 + 2;
-        // q / rho for q < 64 rho: (q + 1/2) / rho sits >= 1/(2 rho) away from an integer, far above fp32 error
-        const int t0i = (int)(((float)q0 + 0.5f) * inv_rho), t1i = (int)(((float)q1 + 0.5f) * inv_rho);
-        *reinterpret_cast<uint16_t*>(tail + t0i * 16 + (q0 - t0i * rho)) = (uint16_t)(cw & 0xffff);
-        *reinterpret_cast<uint16_t*>(tail + t1i * 16 + (q1 - t1i * rho)) = (uint16_t)(cw >> 16);
+    const int ks_t = rho ? (g16 >> 2) : 2;  // K-step holding the tail group (2: none)
+    const int ktb = 8 * rk * bk, vtb = 8 * rv * bv;
+    const int tile0 = start / kTile, tile_last = (end - 1) / kTile;
+    const uint8_t* kstream = uni(K.codes + K.code_off[u]);
+    const uint8_t* vstream = uni(V.codes + V.code_off[u]);
+    // Descriptor of tile t of a stream (bounds: the stream's end); none past the chunk.
+    auto k_rs = [&](int t) {
+        const bool ok = t <= tile_last;
+        return __builtin_amdgcn_make_buffer_rsrc((void*)(kstream + (int64_t)t * ktb), (short)0,
+                                                 ok ? (k_cap_tiles - t) * ktb : 0, kRsrcWord3);
+    };
+    auto v_rs = [&](int t) {
+        const bool ok = t <= tile_last;
+        return __builtin_amdgcn_make_buffer_rsrc((void*)(vstream + (int64_t)t * vtb), (short)0,
+                                                 ok ? (v_cap_tiles - t) * vtb : 0, kRsrcWord3);
+    };
+
+    // lane constants (plane-width units): direct K fields of K-step ks (group 4 ks + grp, tokens 4 col ..),
+    // value fields (coordinate col of the N-tile, quarter grp), staged tail positions.
+    uint32_t LK[2];
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+        const int cg = 4 * ks + grp;
+        LK[ks] = ks == ks_t ? (uint32_t)(512 * ks + 8 * lane) : (cg < g16 ? (uint32_t)(128 * cg + 8 * col) : kLaneOOB);
+    }
+    const uint32_t LV = (uint32_t)(8 * col + 2 * grp);
+    uint32_t XB = 0, XS = 0;  // staged token fields start at plane-width units XB + st XS
+    {
+        const int nf = g16 - 4 * (ks_t < 2 ? ks_t : 0);  // full groups in the staged K-step
+        if (grp < nf) { XB = (uint32_t)((64 * grp + 4 * col) * 16); XS = 16; }
+        else if (grp == nf) { XB = (uint32_t)(nf * 1024 + 4 * col * rho); XS = (uint32_t)rho; }
+    }
+
+    // q~ limbs (A operands of the logits) and per-head scale factors
+    v4i qa[2][LM];
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+        for (int lm = 0; lm < LM; ++lm) qa[ks][lm] = qa_ws[(((int64_t)u * 2 + ks) * LM + lm) * 64 + lane];
+    float k0[LM], k1[LM], k2[LM], bias[LM], mrun[LM], mb[LM];
+#pragma unroll
+    for (int lm = 0; lm < LM; ++lm) {
+        const int h = 4 * lm + grp;
+        const float4 v = h < G ? qk_ws[(int64_t)u * G + h] : float4{0.f, 0.f, 0.f, 0.f};
+        k0[lm] = v.x; k1[lm] = v.y; k2[lm] = v.z; bias[lm] = v.w;
+        mrun[lm] = -INFINITY;
+        mb[lm] = 0.f;  // bias - mrun once the first tile has set mrun
+    }
+    for (int k = lane; k < 16 * LM * kPRowBytes / 4; k += 64) reinterpret_cast<uint32_t*>(pmat)[k] = 0u;
+    wave_lds_sync();
+
+    v4i C[LM][9];
+#pragma unroll
+    for (int pm = 0; pm < LM; ++pm)
+#pragma unroll
+        for (int nt = 0; nt < 9; ++nt) C[pm][nt] = v4i{0, 0, 0, 0};
+    const uint32_t one = col == 0 ? 0x01010101u : 0u;
+    const v4i ones = v4i{(int)one, (int)one, (int)one, (int)one};
+
+    // Prefetch registers: with a depth of 2, tile t is processed from set t % 2 while the loads of
+    // tile t + 1 (the other set) are in flight, and set t % 2 is refilled with tile t + 2 as it is
+    // consumed; with a depth of 1 there is one set, refilled with tile t + 1.
+    uint32_t kbA[kKBufWords], vbA[kVBufWords], kbB[kKBufWords], vbB[kVBufWords];
+#pragma unroll
+    for (int k = 0; k < kKBufWords; ++k) kbA[k] = kbB[k] = 0u;
+#pragma unroll
+    for (int k = 0; k < kVBufWords; ++k) vbA[k] = vbB[k] = 0u;
+    {
+        // issued in the loop's own order (K-steps, then value N-tiles, per set), so that the waits at
+        // the loop head count the same younger loads on entry as on the back edge
+        const auto krs = k_rs(tile0), vrs = v_rs(tile0);
+        KVC_SW_K(k_prefetch<B_>(kbA, krs, rk, nk, ks_t, LK, lane));
+        __builtin_amdgcn_sched_barrier(0);
+        KVC_SW_V(v_prefetch<B_>(vbA, vrs, rv, LV, nv));
+        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (kPrefetchDepth == 2) {
+            const auto krs1 = k_rs(tile0 + 1), vrs1 = v_rs(tile0 + 1);
+            KVC_SW_K(k_prefetch<B_>(kbB, krs1, rk, nk, ks_t, LK, lane));
+            __builtin_amdgcn_sched_barrier(0);
+            KVC_SW_V(v_prefetch<B_>(vbB, vrs1, rv, LV, nv));
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+
+    auto step = [&](const int tile, uint32_t (&kb)[kKBufWords], uint32_t (&vb)[kVBufWords],
+                    uint32_t (&kb_next)[kKBufWords], const bool stage_next) {
+        const int tok0 = tile * kTile;
+        const bool first = tile == tile0;
+        const auto krs = k_rs(tile), vrs = v_rs(tile);
+        const auto krs_n = k_rs(tile + kPrefetchDepth), vrs_n = v_rs(tile + kPrefetchDepth);
+        // Opaque per-tile copies of the lane and rank constants: the offsets every bit width derives
+        // from them are recomputed inside the loop instead of being hoisted and kept live across it
+        // for all eight widths at once.
+        uint32_t LKt[2] = {LK[0], LK[1]}, XBt = XB, XSt = XS, LVt = LV;
+        int rkt = rk, rvt = rv;
+        if constexpr (BKc == 0 || BVc == 0) {
+            asm volatile("" : "+v"(LKt[0]), "+v"(LKt[1]), "+v"(LVt), "+v"(XBt), "+v"(XSt));
+            asm volatile("" : "+s"(rkt), "+s"(rvt));
+        }
+        const int nkt = nk, nvt = nv, kst = ks_t;
+
+        // ---- logits, log2 domain, less the running max (the raw logits on the first tile)
+        float s[LM][4];
+        {
+            float off[LM];
+#pragma unroll
+            for (int lm = 0; lm < LM; ++lm) off[lm] = first ? bias[lm] : mb[lm];
+            KVC_SW_K((k_tile<B_, LM, KM>(kb, kb_next, stage_next, krs, krs_n, rkt, nkt, kst, LKt, XBt, XSt, lane, stage, qa, k0, k1, k2, off, s)));
+        }
+
+        // ---- online softmax
+        float mx[LM];
+        const bool last = tok0 + kTile > end;
+        bool raise = first;
+        if (last) {  // tokens past the end of the chunk
+#pragma unroll
+            for (int lm = 0; lm < LM; ++lm)
+#pragma unroll
+                for (int st = 0; st < 4; ++st)
+                    if (tok0 + 4 * col + st >= end) s[lm][st] = -INFINITY;
+        }
+        if constexpr (G % 4 != 0) {  // rows of heads past G
+#pragma unroll
+            for (int lm = 0; lm < LM; ++lm)
+                if (4 * lm + grp >= G) s[lm][0] = s[lm][1] = s[lm][2] = s[lm][3] = -INFINITY;
+        }
+#pragma unroll
+        for (int lm = 0; lm < LM; ++lm) {
+            mx[lm] = row_max(fmaxf(fmaxf(s[lm][0], s[lm][1]), fmaxf(s[lm][2], s[lm][3])));
+            raise = raise || mx[lm] > kLazy;
+        }
+        if (__any(raise)) {
+            // Raise the max of each head whose tile beats it by more than 2^kLazy (every head on the
+            // first tile) to the tile's own max, and rescale that head's accumulators exactly (every
+            // limb of a (head, coordinate) sits in this lane): value = C0 + 2^8 C1 + 2^16 C2 ->
+            // rint(value alpha), split again.
+#pragma unroll
+            for (int lm = 0; lm < LM; ++lm) {
+                if ((first && mx[lm] > -INFINITY) || mx[lm] > kLazy) {
+                    const float mold = mrun[lm];
+                    const float shift = first ? 0.f : mold;  // s + shift = the raw logit
+                    const float mnew = mx[lm] + shift;
+                    const float alpha = first ? 0.f : exp2f(mold - mnew);
+                    mrun[lm] = mnew;
+                    mb[lm] = bias[lm] - mnew;
+#pragma unroll
+                    for (int st = 0; st < 4; ++st) s[lm][st] = (s[lm][st] + shift) - mnew;
+                    if (!first) {
+                        const double a = (double)alpha;
+#pragma unroll
+                        for (int nt = 0; nt < 9; ++nt) {
+                            const double v = (double)C[lm][nt][0] + 256.0 * (double)C[lm][nt][1] + 65536.0 * (double)C[lm][nt][2];
+                            const double vs = rint(v * a);
+                            const double c2 = floor(vs * (1.0 / 65536.0));
+                            const double rem = vs - 65536.0 * c2;
+                            const double c1 = floor(rem * (1.0 / 256.0));
+                            C[lm][nt][2] = (int)c2;
+                            C[lm][nt][1] = (int)c1;
+                            C[lm][nt][0] = (int)(rem - 256.0 * c1);
+                        }
+                    }
+                }
+            }
+        }
+
+        // ---- probability limbs: P'' = round(p kPScale) + 0x8080; bytes 0, 1 (xor 0x80) and 2 are
+        // the signed limbs S0, S1, S2 with P = S0 + 2^8 S1 + 2^16 S2. Row 4 h + limb, bytes 4 col + st.
+#pragma unroll
+        for (int lm = 0; lm < LM; ++lm) {
+            uint32_t P[4];
+#pragma unroll
+            for (int st = 0; st < 4; ++st)
+                P[st] = (uint32_t)fmaf(__builtin_amdgcn_exp2f(s[lm][st]), kPScale, kPBias);
+            const uint32_t q01 = perm(P[1], P[0], 0x05010400u), q23 = perm(P[3], P[2], 0x05010400u);
+            const uint32_t r01 = perm(P[1], P[0], 0x00000602u), r23 = perm(P[3], P[2], 0x00000602u);
+            const uint32_t L0 = perm(q23, q01, 0x05040100u) ^ 0x80808080u;
+            const uint32_t L1 = perm(q23, q01, 0x07060302u) ^ 0x80808080u;
+            const uint32_t L2 = perm(r23, r01, 0x05040100u);
+            // every lane writes (heads past G have -inf logits, so zero limbs): no divergent LDS writes
+            uint8_t* row = pmat + (16 * lm + 4 * grp) * kPRowBytes + 4 * col;
+            *reinterpret_cast<uint32_t*>(row) = L0;
+            *reinterpret_cast<uint32_t*>(row + kPRowBytes) = L1;
+            *reinterpret_cast<uint32_t*>(row + 2 * kPRowBytes) = L2;
+        }
+        wave_lds_sync();
+        v4i ap[LM];
+#pragma unroll
+        for (int pm = 0; pm < LM; ++pm)
+            ap[pm] = *reinterpret_cast<const v4i*>(pmat + (16 * pm + col) * kPRowBytes + 16 * grp);
+
+        // ---- PV (value N-tiles, then the all-ones column)
+        KVC_SW_V((v_tile<B_, LM>(vb, vrs, vrs_n, rvt, LVt, nvt, ap, C)));
+#pragma unroll
+        for (int pm = 0; pm < LM; ++pm) C[pm][8] = mfma_i8(ap[pm], ones, C[pm][8]);
+        wave_lds_sync();  // pmat is rewritten by the next tile
+    };
+    if constexpr (kPrefetchDepth == 2) {
+        // pairs of tiles in a straight-line body (the load-wait counts stay exact across the back edge)
+        // The staged (tail) K-step of tile t + 1 goes to LDS at the end of tile t's logits (the first
+        // tile's before the loop); the general path stages each tile itself.
+        constexpr bool kAhead = KM >= 0;
+        if constexpr (kAhead) {
+            if (ks_t == 0) k_write_stage<BKc>(kbA, stage, lane);
+            else if (ks_t == 1) k_write_stage<BKc>(kbA + k_step_words(BKc), stage, lane);
+            wave_lds_sync();
+        }
+        int tile = tile0;
+        for (; tile + 1 <= tile_last; tile += 2) {
+            step(tile, kbA, vbA, kbB, kAhead);
+            step(tile + 1, kbB, vbB, kbA, kAhead);
+        }
+        if (tile <= tile_last) step(tile, kbA, vbA, kbB, kAhead);
+    } else {
+        for (int tile = tile0; tile <= tile_last; ++tile) step(tile, kbA, vbA, kbA, false);
+    }
+
+    // Partial of each head: m, l = sum of P (all-ones column), centred accumulator. Lane (grp, col)
+    // holds every limb of head 4 pm + grp at coordinate 16 nt + col; the all-ones column is col 0.
+#pragma unroll
+    for (int pm = 0; pm < LM; ++pm) {
+        const int h = 4 * pm + grp;
+        const int o0 = __shfl(C[pm][8][0], lane & 48), o1 = __shfl(C[pm][8][1], lane & 48),
+                  o2 = __shfl(C[pm][8][2], lane & 48);
+        if (G % 4 == 0 || h < G) {
+            float* o = out + h * kPartStride;
+            if (col == 0) {
+                o[0] = mrun[pm];
+                o[1] = (float)o0 + 256.f * (float)o1 + 65536.f * (float)o2;
+            }
+#pragma unroll
+            for (int nt = 0; nt < 8; ++nt) {
+                const int cc = 16 * nt + col;
+                if (nt < nv) {
+                    const int a0 = C[pm][nt][0] - hv * o0, a1 = C[pm][nt][1] - hv * o1, a2 = C[pm][nt][2] - hv * o2;
+                    o[4 + cc] = cc < rv ? (float)a0 + 256.f * (float)a1 + 65536.f * (float)a2 : 0.f;
+                }
+            }
+        }
     }
 }
 
-// K operand fragments of K-step ks for the 4 sub-tiles (logit B operand): lane (grp, col) = token
-// tok_of(st, col), coordinates 64 ks + 16 grp + [0, 16), read in the grouped layout without bounds:
-// groups past r_K read stale LDS bytes, which meet zero q~ limbs, and the lanes of the tail group are
-// replaced from the transposed tail by the caller. All reads stay below 1024 b_K bytes.
-template <int BK>
-__device__ __forceinline__ void k_frags(const uint8_t* __restrict__ ktile, int rk, int ks, int lane, v4i (&Bk)[4]) {
-    const int col = lane & 15, grp = lane >> 4;
-    const int cg = 4 * ks + grp;
-#pragma unroll
-    for (int st = 0; st < 4; ++st) Bk[st] = code_frag16<BK>(ktile, rk, (cg << 10) + (tok_of(st, col) << 4));
-}
+#undef KVC_SW_K
+#undef KVC_SW_V
 
-// V operand fragments of N-tiles nt0 .. nt0 + 4: lane (grp, col) = coordinate 16 nt + col, tokens
-// 16 st + 4 grp + i at slot 4 st + i. Coordinates >= r_V read stale LDS bytes (below 1024 b_V bytes
-// past the tile start) into accumulator columns that are never used; N-tile 8 is the all-ones column.
-template <int BV>
-__device__ __forceinline__ void v_frags(const uint8_t* __restrict__ vtile, int rv, int nt0, int lane, v4i ones,
-                                        v4i (&Bf)[5]) {
-    const int col = lane & 15, grp = lane >> 4;
-#pragma unroll
-    for (int k = 0; k < 5; ++k) {
-        const int nt = nt0 + k;
-        Bf[k] = nt == kD / 16 ? ones : code_frag16<BV>(vtile, rv, ((16 * nt + col) << 6) + (grp << 4));
-    }
-}
-
+// Token of logit column col in sub-tile st is 4 col + st: a lane's four tokens are consecutive, so
+// its K fields are one contiguous load, and its probability limbs are one dword per limb in LDS.
 template <int G>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(Shape<G>::W, Shape<G>::W))) void decode_mfma_kernel(DevSide K, DevSide V, const int8_t* __restrict__ qlimb,
-                                                         const float* __restrict__ qscale,
-                                                         const int32_t* __restrict__ qcorr,
-                                                         const int32_t* __restrict__ seq_len, int max_seq, int chunk,
-                                                         int n_chunks, float* __restrict__ part, int raw_bytes) {
-    constexpr int LM = Shape<G>::LM, PM = Shape<G>::PM, NV = Shape<G>::NV;
-    extern __shared__ float smem[];
-    float* accs = smem;                                                   // [G][kAccStride] fp32: coords 0..127, 128 = sum P
-    float* alph = smem + G * kAccStride;                                  // [16] per-head rescale factors
-    uint8_t* pmat = reinterpret_cast<uint8_t*>(alph + 16);               // [16 PM][64] probability limbs, V slot order
-    uint8_t* tail = pmat + 16 * PM * kTile;                               // [64][16] K tail codes
-    uint4* raw = reinterpret_cast<uint4*>(tail + kTile * 16);            // raw K tile, then V tile
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(Shape<G>::W, Shape<G>::W))) void decode_partial_kernel(
+    DevSide K, DevSide V, const v4i* __restrict__ qa_ws, const float4* __restrict__ qk_ws,
+    const int32_t* __restrict__ seq_len, int max_seq, int chunk, int n_chunks, int k_cap_tiles, int v_cap_tiles,
+    float* __restrict__ part) {
+    constexpr int LM = Shape<G>::LM;
 
     const int u = blockIdx.y, c = blockIdx.x, lane = threadIdx.x;
     const int col = lane & 15, grp = lane >> 4;
@@ -268,343 +862,104 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(Shape<G>::W,
         if (lane < G) { out[lane * kPartStride] = -INFINITY; out[lane * kPartStride + 1] = 0.f; }
         return;
     }
-    const int rk = K.r[u], bk = K.b[u], rv = V.r[u], bv = V.b[u];
-    const int hv = bv == 8 ? 0 : (1 << (bv - 1));
-    const int nk = (rk + 63) >> 6;
-    const int nv = (rv + 15) >> 4;  // V N-tiles holding coordinates (N-tile 8 = all-ones column)
-    const uint8_t* __restrict__ kstream = K.codes + K.code_off[u];
-    const uint8_t* __restrict__ vstream = V.codes + V.code_off[u];
-
-    // Logit A operands: lane (grp, col) = row 16 lm + col = (head 4 lm + col / 4, limb col % 4),
-    // coordinates 64 ks + 16 grp + [0, 16). The logit of (head 4 lm + grp, token) is
-    // sum_limb S_limb kq[lm][limb] + bq[lm] in the log2 domain (bq holds the centring correction).
-    v4i qA[2][LM];
-    float kq[LM][kLimbs], bq[LM];
-#pragma unroll
-    for (int lm = 0; lm < LM; ++lm) {
-        const int h = 4 * lm + (col >> 2), limb = col & 3;
-        const bool ok = h < G && limb < kLimbs;
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-            v4i v = {0, 0, 0, 0};
-            if (ok && ks < nk)
-                v = *reinterpret_cast<const v4i*>(qlimb + (((int64_t)u * kLimbs + limb) * G + h) * kD + 64 * ks + 16 * grp);
-            qA[ks][lm] = v;
-        }
-        const int hs = 4 * lm + grp;
-        float bsum = 0.f;
-#pragma unroll
-        for (int l = 0; l < kLimbs; ++l) {
-            const float ls = l == 0 ? 1.f : (l == 1 ? (1.f / 254.f) : (1.f / 64516.f));
-            kq[lm][l] = hs < G ? qscale[(int64_t)u * G + hs] * ls : 0.f;
-            if (hs < G) bsum = fmaf(-(float)qcorr[((int64_t)u * kLimbs + l) * G + hs], kq[lm][l], bsum);
-        }
-        bq[lm] = bsum;
-    }
-    for (int k = lane; k < G * kAccStride; k += 64) accs[k] = 0.f;
-    for (int k = lane; k < 16 * PM * kTile / 4; k += 64) reinterpret_cast<uint32_t*>(pmat)[k] = 0u;
-    __syncthreads();
-
-    v4i Cpv[PM][NV];
-#pragma unroll
-    for (int pm = 0; pm < PM; ++pm)
-#pragma unroll
-        for (int nt = 0; nt < NV; ++nt) Cpv[pm][nt] = v4i{0, 0, 0, 0};
-    float m_run[LM];  // running max (log2 domain) of head 4 lm + grp
-#pragma unroll
-    for (int lm = 0; lm < LM; ++lm) m_run[lm] = -INFINITY;
-
-    // When a head's running max grows (by more than 2^kLazy, so alpha <= 2^-kLazy) its int32
-    // accumulator rows are rescaled in place: C <- rint(C alpha). The rounding adds at most about one
-    // quantum of P per rescale, the size of one token's quantisation error; rows of heads that kept
-    // their max are left untouched. Rare (a few tiles per chunk), so it is written for size.
-    auto rescale = [&](const float (&alpha)[LM]) {
-        int ln = threadIdx.x;
-        asm volatile("" : "+v"(ln));
-        const int gr = ln >> 4;
-#pragma unroll
-        for (int lm = 0; lm < LM; ++lm)
-            if ((ln & 15) == 0 && 4 * lm + gr < G) alph[4 * lm + gr] = alpha[lm];
-        __syncthreads();
-#pragma unroll
-        for (int pm = 0; pm < PM; ++pm)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int row = 16 * pm + 4 * gr + i;
-                const float a = row < kLimbs * G ? alph[row % G] : 1.f;
-                const bool keep = a == 1.f;
-#pragma unroll
-                for (int nt = 0; nt < NV; ++nt) {
-                    const int cur = Cpv[pm][nt][i];
-                    const int scaled = (int)rintf((float)cur * a);
-                    Cpv[pm][nt][i] = keep ? cur : scaled;
-                }
-            }
-        __syncthreads();
-    };
-
-    const v4i ones = col == 0 ? v4i{0x01010101, 0x01010101, 0x01010101, 0x01010101} : v4i{0, 0, 0, 0};
-    const int kch = (8 * rk * bk) >> 4, vch = (8 * rv * bv) >> 4;  // 16-byte chunks per K / V tile
-    const uint8_t* ktile = reinterpret_cast<const uint8_t*>(raw);
-    const uint8_t* vtile = reinterpret_cast<const uint8_t*>(raw + kch);
-    // The packed K and V tiles are staged in LDS with coalesced 16-byte loads: chunk cc < kch of
-    // the K tile, then the V tile's, 64 chunks per round. The first 4 rounds of the next tile are
-    // loaded into registers while the current tile is computed; further rounds (tiles of more than
-    // 4 KiB) are loaded when their tile is staged. Lanes past the last chunk reload the V tile's last.
-    const int nch = kch + vch;
-    const int64_t ktb = 8 * rk * bk, vtb = 8 * rv * bv;  // tile bytes
-    auto chunk_src = [&](int tile, int cc) -> const uint4* {
-        const uint4* kb = reinterpret_cast<const uint4*>(kstream + tile * ktb);
-        const uint4* vb = reinterpret_cast<const uint4*>(vstream + tile * vtb) - kch;
-        return (cc < kch ? kb : vb) + min(cc, nch - 1);
-    };
-    uint4 pf0, pf1, pf2, pf3;
-    {
-        const int tile = start / kTile;
-        pf0 = *chunk_src(tile, lane);
-        pf1 = *chunk_src(tile, 64 + lane);
-        pf2 = *chunk_src(tile, 128 + lane);
-        pf3 = *chunk_src(tile, 192 + lane);
-    }
-    for (int tok0 = start; tok0 < end; tok0 += kTile) {
-        // An opaque per-tile copy of the lane id: lane-dependent fragment offsets are recomputed
-        // inside the loop instead of being hoisted and kept live in registers across it.
-        int lane_it = lane;
-        asm volatile("" : "+v"(lane_it));
-        const int col_it = lane_it & 15, grp_it = lane_it >> 4;
-        const int tile = tok0 / kTile;
-        if (lane_it < nch) raw[lane_it] = pf0;
-        if (64 + lane_it < nch) raw[64 + lane_it] = pf1;
-        if (128 + lane_it < nch) raw[128 + lane_it] = pf2;
-        if (192 + lane_it < nch) raw[192 + lane_it] = pf3;
-        for (int c0 = 256; c0 < nch; c0 += 64)
-            if (c0 + lane_it < nch) raw[c0 + lane_it] = *chunk_src(tile, c0 + lane_it);
-        __syncthreads();
-        if (tok0 + kTile < end) {
-            pf0 = *chunk_src(tile + 1, lane_it);
-            pf1 = *chunk_src(tile + 1, 64 + lane_it);
-            pf2 = *chunk_src(tile + 1, 128 + lane_it);
-            pf3 = *chunk_src(tile + 1, 192 + lane_it);
-        }
-        // Logits: S[lm][st] = q~ limbs (rows) . codes (64 coords x 16 tokens), summed over K-steps.
-        if (rk & 15) {
-            KVC_SWITCH_B(bk, k_tail<B_>(ktile, rk, tail, lane_it));
-            __syncthreads();
-        }
-        v4i S[LM][4];
-#pragma unroll
-        for (int lm = 0; lm < LM; ++lm)
-#pragma unroll
-            for (int st = 0; st < 4; ++st) S[lm][st] = v4i{0, 0, 0, 0};
-        // All MFMAs are issued unconditionally (absent coordinates contribute zero fragments), which
-        // keeps the accumulator code straight-line.
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-            v4i Bk[4];
-            KVC_SWITCH_B(bk, k_frags<B_>(ktile, rk, ks, lane_it, Bk));
-            if ((rk & 15) && (rk >> 6) == ks) {  // this K-step holds the tail group: its lanes read the transposed copy
-#pragma unroll
-                for (int st = 0; st < 4; ++st) {
-                    const v4i tv = *reinterpret_cast<const v4i*>(tail + tok_of(st, col_it) * 16);
-                    if (grp_it == ((rk >> 4) & 3)) Bk[st] = tv;
-                }
-            }
-#pragma unroll
-            for (int st = 0; st < 4; ++st)
-#pragma unroll
-                for (int lm = 0; lm < LM; ++lm) S[lm][st] = mfma_i8(qA[ks][lm], Bk[st], S[lm][st]);
-        }
-        // Lane (grp, col) holds the three limbs of head 4 lm + grp for token tok_of(st, col).
-        float s[LM][4];
-#pragma unroll
-        for (int lm = 0; lm < LM; ++lm)
-#pragma unroll
-            for (int st = 0; st < 4; ++st) {
-                float v = fmaf((float)S[lm][st][0], kq[lm][0], bq[lm]);
-                v = fmaf((float)S[lm][st][1], kq[lm][1], v);
-                s[lm][st] = fmaf((float)S[lm][st][2], kq[lm][2], v);
-            }
-        if (tok0 + kTile > end) {  // last tile of the chunk: tokens past the end get zero weight
-#pragma unroll
-            for (int st = 0; st < 4; ++st)
-                if (tok0 + tok_of(st, col_it) >= end) {
-#pragma unroll
-                    for (int lm = 0; lm < LM; ++lm) s[lm][st] = -INFINITY;
-                }
-        }
-
-        // Online softmax: running max per head over the 16 lanes of its row; the int32
-        // accumulators are rescaled when it grows past the lazy margin.
-        float alpha[LM];
-        bool grow = false;
-#pragma unroll
-        for (int lm = 0; lm < LM; ++lm) {
-            float m = fmaxf(fmaxf(s[lm][0], s[lm][1]), fmaxf(s[lm][2], s[lm][3]));
-            m = fmaxf(m, row_ror<8>(m));
-            m = fmaxf(m, row_ror<4>(m));
-            m = fmaxf(m, row_ror<2>(m));
-            m = fmaxf(m, row_ror<1>(m));
-            // lazy: keep the stale max while the tile stays within 2^kLazy of it (p <= 2^kLazy then)
-            const float mn = m > m_run[lm] + kLazy ? m : m_run[lm];
-            alpha[lm] = mn > m_run[lm] ? __builtin_amdgcn_exp2f(m_run[lm] - mn) : 1.f;
-            grow = grow || (mn > m_run[lm] && m_run[lm] > -INFINITY);
-            m_run[lm] = mn;
-        }
-        if (__any(grow)) rescale(alpha);
-
-        // Probability limbs: P = round(p (2^21 - 1) / 2^kLazy) = L0 2^14 + L1 2^7 + L2 (p <= 2^kLazy).
-        // Row limb * G + h of pmat, bytes 4 col .. 4 col + 3 = tokens tok_of(0..3, col).
-#pragma unroll
-        for (int lm = 0; lm < LM; ++lm) {
-            const int h = 4 * lm + grp_it;
-            uint32_t P[4];
-#pragma unroll
-            for (int st = 0; st < 4; ++st)
-                P[st] = (uint32_t)fmaf(__builtin_amdgcn_exp2f(s[lm][st] - m_run[lm]), kPScale, 0.5f);
-            if (G >= 4 * (lm + 1) || h < G) {
-#pragma unroll
-                for (int l = 0; l < kLimbs; ++l) {
-                    const uint32_t sh = 14 - 7 * l;
-                    uint32_t w = (P[0] >> sh) & 0x7fu;
-#pragma unroll
-                    for (int st = 1; st < 4; ++st) w |= ((P[st] >> sh) & 0x7fu) << (8 * st);
-                    *reinterpret_cast<uint32_t*>(pmat + (l * G + h) * kTile + 4 * col_it) = w;
-                }
+    const int bk = K.b[u], bv = V.b[u];
+    // Compiled per (b_K, b_V, K-step structure) for the common widths and group sizes; the general
+    // path switches on the widths per tile.
+    if constexpr (G == 4 || G == 8) {
+        if (bk <= 4 && bv <= 4) {
+            switch (((bk - 1) * 4 + (bv - 1)) * 4 + k_mode(K.r[u])) {
+#define KVC_ITEM(BK, BV, KM)                                                                                      \
+    case ((BK - 1) * 4 + (BV - 1)) * 4 + KM:                                                                    \
+        run_item<G, BK, BV, KM>(K, V, qa_ws, qk_ws, k_cap_tiles, v_cap_tiles, u, start, end, out, lane);        \
+        return;
+#define KVC_ITEM4(BK, BV) KVC_ITEM(BK, BV, 0) KVC_ITEM(BK, BV, 1) KVC_ITEM(BK, BV, 2) KVC_ITEM(BK, BV, 3)
+                KVC_ITEM4(1, 1) KVC_ITEM4(1, 2) KVC_ITEM4(1, 3) KVC_ITEM4(1, 4)
+                KVC_ITEM4(2, 1) KVC_ITEM4(2, 2) KVC_ITEM4(2, 3) KVC_ITEM4(2, 4)
+                KVC_ITEM4(3, 1) KVC_ITEM4(3, 2) KVC_ITEM4(3, 3) KVC_ITEM4(3, 4)
+                KVC_ITEM4(4, 1) KVC_ITEM4(4, 2) KVC_ITEM4(4, 3) KVC_ITEM4(4, 4)
+#undef KVC_ITEM4
+#undef KVC_ITEM
+                default: break;
             }
         }
-        __syncthreads();
-        v4i Ap[PM];
-#pragma unroll
-        for (int pm = 0; pm < PM; ++pm)
-            Ap[pm] = *reinterpret_cast<const v4i*>(pmat + (16 * pm + col_it) * kTile + 16 * grp_it);
-
-        // PV: Cpv[pm][nt] += P limbs (rows x 64 tokens) . V codes (64 tokens x 16 coords).
-#pragma unroll
-        for (int half = 0; half < 2; ++half) {
-            const int nt0 = 5 * half;
-            v4i Bf[5];
-            KVC_SWITCH_B(bv, v_frags<B_>(vtile, rv, nt0, lane_it, ones, Bf));
-#pragma unroll
-            for (int k = 0; k < 5; ++k)
-                if (nt0 + k < NV)
-#pragma unroll
-                    for (int pm = 0; pm < PM; ++pm) Cpv[pm][nt0 + k] = mfma_i8(Ap[pm], Bf[k], Cpv[pm][nt0 + k]);
-        }
-        __syncthreads();  // raw and pmat are rewritten by the next tile
     }
-    // Centre (exact, in integers, with the all-ones column O) and combine the three P limbs of each
-    // head into the fp32 LDS accumulator: accs[g][c] = sum_limb ls (C - 2^(b-1) O), accs[g][128] = sum_limb ls O.
-    {
-#pragma unroll
-        for (int pm = 0; pm < PM; ++pm)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int row = 16 * pm + 4 * grp + i;
-                const int plimb = row / G, g = row - plimb * G;
-                const int O = __shfl(Cpv[pm][NV - 1][i], lane & 48);
-                const float ls = plimb == 0 ? 16384.f : (plimb == 1 ? 128.f : 1.f);
-                float* arow = accs + g * kAccStride;
-                if (plimb < kLimbs) {
-#pragma unroll
-                    for (int nt = 0; nt < NV - 1; ++nt) {
-                        const int coord = 16 * nt + col;
-                        if (nt < nv && coord < rv) atomicAdd(arow + coord, (float)(Cpv[pm][nt][i] - hv * O) * ls);
-                    }
-                    if (col == 0) atomicAdd(arow + kD, (float)O * ls);
-                }
-            }
-    }
-    __syncthreads();
-
-    // Partial of each head: m, l = sum of P (all-ones column), centred accumulator.
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-        const float mg = __shfl(m_run[g / 4], 16 * (g % 4));
-        float* o = out + g * kPartStride;
-        const float* arow = accs + g * kAccStride;
-        if (lane == 0) { o[0] = mg; o[1] = arow[kD]; }
-        o[4 + lane] = lane < rv ? arow[lane] : 0.f;
-        o[4 + 64 + lane] = lane + 64 < rv ? arow[lane + 64] : 0.f;
-    }
+    run_item<G, 0, 0, -1>(K, V, qa_ws, qk_ws, k_cap_tiles, v_cap_tiles, u, start, end, out, lane);
 }
 
 // ---------------------------------------------------------------- combine
 
-__global__ __launch_bounds__(kD) void combine_kernel(DevSide V, int G, int n_chunks, const float* __restrict__ part,
-                                                     float* __restrict__ out) {
-    constexpr int kMaxG = 16;
+// One block per unit, one wavefront per query head; lane l handles coordinates l and l + 64.
+// The chunks' partials merge in the log2 domain (M = max m_c, L = sum l_c 2^(m_c - M),
+// A_j = sum acc_c,j 2^(m_c - M)), z_j = step_V (A_j / L + 1/2) is the dequantised rank-space
+// average, and o = P_V^T z (the V reconstruction of Lemma lem:head-dist applied after the
+// softmax average, which is linear).
+constexpr int kMaxG = 16;
+__global__ __launch_bounds__(64 * kMaxG) void combine_kernel(DevSide V, int G, int n_chunks, const float* __restrict__ part,
+                                                             float* __restrict__ out) {
     __shared__ float zs[kMaxG][kD];
-    __shared__ float lsum[kMaxG];
-    const int u = blockIdx.x, j = threadIdx.x;
+    const int u = blockIdx.x, g = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int rv = V.r[u];
     const float step = V.delta[u];
-    const float* __restrict__ pu = part + (int64_t)u * n_chunks * G * kPartStride;
-    for (int g = 0; g < G; ++g) {
-        const float* pg = pu + g * kPartStride;
-        float M = -INFINITY;
-        for (int c = 0; c < n_chunks; ++c) M = fmaxf(M, pg[(int64_t)c * G * kPartStride]);
-        float L = 0.f, A = 0.f;
-        for (int c = 0; c < n_chunks; ++c) {
-            const float* pc = pg + (int64_t)c * G * kPartStride;
-            const float lc = pc[1];
-            if (lc > 0.f) {
-                const float w = exp2f(pc[0] - M);
-                L = fmaf(lc, w, L);
-                if (j < rv) A = fmaf(pc[4 + j], w, A);
-            }
+    const float* __restrict__ pg = part + (int64_t)u * n_chunks * G * kPartStride + g * kPartStride;
+    const int64_t cs = (int64_t)G * kPartStride;
+    float M = -INFINITY;
+    for (int c = 0; c < n_chunks; ++c) M = fmaxf(M, pg[c * cs]);
+    float L = 0.f, A0 = 0.f, A1 = 0.f;
+    for (int c = 0; c < n_chunks; ++c) {
+        const float* pc = pg + c * cs;
+        const float lc = pc[1];
+        if (lc > 0.f) {  // an empty chunk writes only m and l
+            const float w = exp2f(pc[0] - M);
+            L = fmaf(lc, w, L);
+            if (lane < rv) A0 = fmaf(pc[4 + lane], w, A0);
+            if (lane + 64 < rv) A1 = fmaf(pc[4 + 64 + lane], w, A1);
         }
-        zs[g][j] = (L > 0.f && j < rv) ? step * (A / L + 0.5f) : 0.f;
-        if (j == 0) lsum[g] = L;
     }
+    const float inv = L > 0.f ? 1.f / L : 0.f;
+    zs[g][lane] = (L > 0.f && lane < rv) ? step * fmaf(A0, inv, 0.5f) : 0.f;
+    zs[g][lane + 64] = (L > 0.f && lane + 64 < rv) ? step * fmaf(A1, inv, 0.5f) : 0.f;
     __syncthreads();
-    // o_g = P_V^T z_g for every head in one pass over the basis (coalesced rows of P)
     const uint16_t* __restrict__ P = V.basis + V.basis_off[u];
-    float o[kMaxG];
-#pragma unroll
-    for (int g = 0; g < kMaxG; ++g) o[g] = 0.f;
+    float o0 = 0.f, o1 = 0.f;
     for (int i = 0; i < rv; ++i) {
-        const float p = h2f(P[(int64_t)i * kD + j]);
-#pragma unroll
-        for (int g = 0; g < kMaxG; ++g)
-            if (g < G) o[g] = fmaf(p, zs[g][i], o[g]);
+        const float z = zs[g][i];
+        o0 = fmaf(h2f(P[(int64_t)i * kD + lane]), z, o0);
+        o1 = fmaf(h2f(P[(int64_t)i * kD + lane + 64]), z, o1);
     }
-#pragma unroll
-    for (int g = 0; g < kMaxG; ++g)
-        if (g < G) out[((int64_t)u * G + g) * kD + j] = lsum[g] > 0.f ? o[g] : 0.f;
+    out[((int64_t)u * G + g) * kD + lane] = o0;
+    out[((int64_t)u * G + g) * kD + lane + 64] = o1;
 }
 
 // ---------------------------------------------------------------- host side
 
 namespace {
 
-// Raw LDS bytes for the staged tiles: fragment reads run past the staged tiles (up to 1024 b bytes
-// from each tile start), so the region covers max(1024 b_K, 8 r_K b_K + 1024 b_V) over the units.
-int raw_tile_bytes(const kvc_stream_desc* k, const kvc_stream_desc* v) {
-    int raw = 16;
-    for (int u = 0; u < k->n_units; ++u) {
-        const int kb = 8 * k->r_host[u] * k->b_host[u];
-        raw = std::max(raw, std::max(1024 * k->b_host[u], kb + 1024 * v->b_host[u]));
-    }
-    return raw;
+
+// LDS bytes of the staged tail K-step: the largest over units whose rank has a tail group.
+int stage_lds_bytes(const kvc_stream_desc* k) {
+    int m = 0;
+    for (int u = 0; u < k->n_units; ++u)
+        if (k->r_host[u] & 15) m = std::max(m, 512 * k->b_host[u]);
+    return m == 0 ? 0 : m + 32;  // funnel reads may look one word past a plane's region
 }
 
-size_t partial_smem(int G, int raw_bytes) {
-    const int PM = (kLimbs * G + 15) / 16;
-    return (size_t)G * kAccStride * 4 + 16 * 4 + (size_t)16 * PM * kTile + kTile * 16 + (size_t)raw_bytes;
+size_t partial_smem(int G, int stage_bytes_) {
+    const int LM = (G + 3) / 4;
+    return (size_t)16 * LM * kPRowBytes + (size_t)stage_bytes_;
 }
 
 template <int G>
 int resident_blocks(size_t smem) {
     int nb = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, decode_mfma_kernel<G>, 64, smem) != hipSuccess || nb <= 0) {
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, decode_partial_kernel<G>, 64, smem) != hipSuccess || nb <= 0) {
         (void)hipGetLastError();
-        nb = 8;
+        nb = 16;
     }
     return nb;
 }
 
 // Work items (wavefronts) the device holds at once for this launch; without a device, the
-// MI355X figures (256 CUs, 8 resident wavefronts each).
+// MI355X figures (256 CUs, 16 resident wavefronts each).
 int64_t resident_slots(int G, size_t smem) {
     int dev = 0, ncu = 0;
     if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
@@ -623,36 +978,34 @@ int64_t resident_slots(int G, size_t smem) {
     return (int64_t)ncu * nb;
 }
 
-// Split of each unit's context into n_chunks equal chunks of whole tiles. Among counts that give
-// at least one work item per resident slot, the count minimises
+// Split of each unit's context into n_chunks equal chunks of whole tiles (at most kMaxChunkTiles
+// each). Among counts that give at least one work item per resident slot, the count minimises
 //   rounds x (tiles per item + per-item overhead) + (straggler share) x tiles per item,
 // rounds = ceil(items / resident slots): whole rounds with no short remainder, and items short
-// enough that units of different cost even out (measured on the 32-layer 32k-token workload:
-// 9 chunks of 57 tiles beat 3 chunks of 171 by 11 % and 24 chunks of 22 by 12 %).
+// enough that units of different cost even out.
 constexpr int kItemOverheadTiles = 4;
 constexpr double kStragglerShare = 0.5;
 
 struct WsLayout {
-    int chunk, n_chunks, raw_bytes;
-    int64_t qlimb, qscale, qcorr, part, total;  // byte offsets
+    int chunk, n_chunks, stage_bytes;
+    int64_t qa, qk, part, total;  // byte offsets
 };
 
-WsLayout ws_layout(const kvc_stream_desc* k, const kvc_stream_desc* v, int G, int max_seq) {
+WsLayout ws_layout(const kvc_stream_desc* k, int G, int max_seq) {
     WsLayout L;
     const int U = k->n_units;
-    L.raw_bytes = raw_tile_bytes(k, v);
-    const int64_t slots = resident_slots(G, partial_smem(G, L.raw_bytes));
+    const int LM = (G + 3) / 4;
+    L.stage_bytes = stage_lds_bytes(k);
+    const int64_t slots = resident_slots(G, partial_smem(G, L.stage_bytes));
     const int tpu = (max_seq + kTile - 1) / kTile;
-    // Candidates that fill every resident slot rank by cost; if none can (few units, short
-    // contexts), the one with the most items wins.
     bool best_full = false;
     double best_cost = 0.0;
     int64_t best_items = -1;
-    L.chunk = tpu * kTile;
-    L.n_chunks = 1;
-    for (int n = 1; n <= tpu && n <= 1024; ++n) {
+    L.chunk = std::min(tpu, kMaxChunkTiles) * kTile;
+    L.n_chunks = (tpu + kMaxChunkTiles - 1) / kMaxChunkTiles;
+    for (int n = 1; n <= tpu && n <= 4096; ++n) {
         const int c = (tpu + n - 1) / n;
-        if ((tpu + c - 1) / c != n) continue;
+        if ((tpu + c - 1) / c != n || c > kMaxChunkTiles) continue;
         const int64_t items = (int64_t)U * n;
         const bool full = items >= slots;
         const int64_t rounds = (items + slots - 1) / slots;
@@ -668,10 +1021,9 @@ WsLayout ws_layout(const kvc_stream_desc* k, const kvc_stream_desc* v, int G, in
         }
     }
     auto up = [](int64_t x) { return (x + 255) / 256 * 256; };
-    L.qlimb = 0;
-    L.qscale = up(L.qlimb + (int64_t)U * kLimbs * G * kD);
-    L.qcorr = up(L.qscale + (int64_t)U * G * 4);
-    L.part = up(L.qcorr + (int64_t)U * kLimbs * G * 4);
+    L.qa = 0;
+    L.qk = up(L.qa + (int64_t)U * 2 * LM * 64 * 16);
+    L.part = up(L.qk + (int64_t)U * G * 16);
     L.total = L.part + (int64_t)U * L.n_chunks * G * kPartStride * 4;
     return L;
 }
@@ -686,21 +1038,27 @@ int decode_check(const kvc_stream_desc* k, const kvc_stream_desc* v, int32_t G, 
     if (max_seq_len < 1) return set_error(KVC_EINVAL, "kvc_decode_attn: max_seq_len < 1");
     if (max_seq_len > k->capacity || max_seq_len > v->capacity)
         return set_error(KVC_ENOSPACE, "kvc_decode_attn: max_seq_len exceeds capacity");
+    // per-unit streams must lie inside their arenas (the kernels bound their loads by the stream)
+    const int64_t kct = ((int64_t)k->capacity + kTile - 1) / kTile, vct = ((int64_t)v->capacity + kTile - 1) / kTile;
+    for (int u = 0; u < k->n_units; ++u) {
+        if (kct * 8 * k->r_host[u] * k->b_host[u] > INT32_MAX || vct * 8 * v->r_host[u] * v->b_host[u] > INT32_MAX)
+            return set_error(KVC_EUNSUPPORTED, "kvc_decode_attn: a unit's stream exceeds 2 GiB");
+    }
     return KVC_OK;
 }
 
 template <int G>
-int launch_partials(dim3 grid, hipStream_t st, const DevSide& K, const DevSide& V, const int8_t* ql, const float* qs,
-                    const int32_t* qc, const int32_t* seq_len, int max_seq, int chunk, int n_chunks, float* part,
-                    int raw_bytes) {
-    const size_t smem = partial_smem(G, raw_bytes);
+int launch_partials(dim3 grid, hipStream_t st, const DevSide& K, const DevSide& V, const v4i* qa, const float4* qk,
+                    const int32_t* seq_len, int max_seq, int chunk, int n_chunks, int kct, int vct, float* part,
+                    int stage_bytes_) {
+    const size_t smem = partial_smem(G, stage_bytes_);
     if (smem > 64 * 1024) {
-        const hipError_t e = hipFuncSetAttribute((const void*)decode_mfma_kernel<G>,
+        const hipError_t e = hipFuncSetAttribute((const void*)decode_partial_kernel<G>,
                                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
         if (e != hipSuccess) return set_error(KVC_EDEVICE, "hipFuncSetAttribute: %s", hipGetErrorString(e));
     }
-    hipLaunchKernelGGL(decode_mfma_kernel<G>, grid, dim3(64), smem, st, K, V, ql, qs, qc, seq_len, max_seq, chunk,
-                       n_chunks, part, raw_bytes);
+    hipLaunchKernelGGL(decode_partial_kernel<G>, grid, dim3(64), smem, st, K, V, qa, qk, seq_len, max_seq, chunk,
+                       n_chunks, kct, vct, part);
     return KVC_OK;
 }
 
@@ -713,7 +1071,7 @@ extern "C" size_t kvc_decode_attn_workspace(const kvc_stream_desc* k, const kvc_
                                             int32_t max_seq_len) {
     clear_error();
     if (decode_check(k, v, G, max_seq_len)) return 0;
-    return (size_t)ws_layout(k, v, G, max_seq_len).total;
+    return (size_t)ws_layout(k, G, max_seq_len).total;
 }
 
 extern "C" int kvc_decode_attn(const kvc_stream_desc* k, const kvc_stream_desc* v, const uint16_t* q, int32_t G,
@@ -725,28 +1083,29 @@ extern "C" int kvc_decode_attn(const kvc_stream_desc* k, const kvc_stream_desc* 
     if (!q || !seq_len || !out || !ws) return set_error(KVC_EINVAL, "kvc_decode_attn: null pointer");
     if (reinterpret_cast<uintptr_t>(ws) & 255) return set_error(KVC_EINVAL, "kvc_decode_attn: workspace not 256-byte aligned");
     const int U = k->n_units;
-    const WsLayout L = ws_layout(k, v, G, max_seq_len);
+    const WsLayout L = ws_layout(k, G, max_seq_len);
     if ((int64_t)ws_bytes < L.total)
         return set_error(KVC_ENOSPACE, "kvc_decode_attn: workspace %zu < %lld bytes", ws_bytes, (long long)L.total);
     char* w = reinterpret_cast<char*>(ws);
-    int8_t* ql = reinterpret_cast<int8_t*>(w + L.qlimb);
-    float* qs = reinterpret_cast<float*>(w + L.qscale);
-    int32_t* qc = reinterpret_cast<int32_t*>(w + L.qcorr);
+    v4i* qa = reinterpret_cast<v4i*>(w + L.qa);
+    float4* qk = reinterpret_cast<float4*>(w + L.qk);
     float* part = reinterpret_cast<float*>(w + L.part);
     hipStream_t st = (hipStream_t)stream;
     const DevSide K = dev_side(k), V = dev_side(v);
-    hipLaunchKernelGGL(qprep_kernel, dim3(U), dim3(kD), 0, st, K, q, G, ql, qs, qc);
-    const int raw_bytes = L.raw_bytes;
+    const int LM = (G + 3) / 4;
+    const size_t qsm = (size_t)G * kD * 4 + (size_t)2 * LM * 64 * 16;
+    hipLaunchKernelGGL(qprep_kernel, dim3(U), dim3(kD), qsm, st, K, q, G, LM, qa, qk);
+    const int kct = (k->capacity + kTile - 1) / kTile, vct = (v->capacity + kTile - 1) / kTile;
     const dim3 grid(L.n_chunks, U);
     int e = KVC_OK;
     switch (G) {
-        case 1: e = launch_partials<1>(grid, st, K, V, ql, qs, qc, seq_len, max_seq_len, L.chunk, L.n_chunks, part, raw_bytes); break;
-        case 2: e = launch_partials<2>(grid, st, K, V, ql, qs, qc, seq_len, max_seq_len, L.chunk, L.n_chunks, part, raw_bytes); break;
-        case 4: e = launch_partials<4>(grid, st, K, V, ql, qs, qc, seq_len, max_seq_len, L.chunk, L.n_chunks, part, raw_bytes); break;
-        case 8: e = launch_partials<8>(grid, st, K, V, ql, qs, qc, seq_len, max_seq_len, L.chunk, L.n_chunks, part, raw_bytes); break;
-        default: e = launch_partials<16>(grid, st, K, V, ql, qs, qc, seq_len, max_seq_len, L.chunk, L.n_chunks, part, raw_bytes); break;
+        case 1: e = launch_partials<1>(grid, st, K, V, qa, qk, seq_len, max_seq_len, L.chunk, L.n_chunks, kct, vct, part, L.stage_bytes); break;
+        case 2: e = launch_partials<2>(grid, st, K, V, qa, qk, seq_len, max_seq_len, L.chunk, L.n_chunks, kct, vct, part, L.stage_bytes); break;
+        case 4: e = launch_partials<4>(grid, st, K, V, qa, qk, seq_len, max_seq_len, L.chunk, L.n_chunks, kct, vct, part, L.stage_bytes); break;
+        case 8: e = launch_partials<8>(grid, st, K, V, qa, qk, seq_len, max_seq_len, L.chunk, L.n_chunks, kct, vct, part, L.stage_bytes); break;
+        default: e = launch_partials<16>(grid, st, K, V, qa, qk, seq_len, max_seq_len, L.chunk, L.n_chunks, kct, vct, part, L.stage_bytes); break;
     }
     if (e) return e;
-    hipLaunchKernelGGL(combine_kernel, dim3(U), dim3(kD), 0, st, V, G, L.n_chunks, part, out);
+    hipLaunchKernelGGL(combine_kernel, dim3(U), dim3(64 * G), 0, st, V, G, L.n_chunks, part, out);
     return check_launch("kvc_decode_attn");
 }

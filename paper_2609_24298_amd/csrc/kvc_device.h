@@ -22,10 +22,21 @@ struct DevSide {
     const uint16_t* basis;
 };
 
+// Position inside a run of 16 slots given to the m-th item, and its inverse. The V side stores
+// each quarter of 16 tokens in this order; in the decode kernels position j of a 16-slot run is
+// operand byte kidx_b(j) (byte k of dword d at 4d + k), which is where the unpacking of a field of
+// that width puts it. b = 8: identity; b = 4: nibble pairs; other b: 4 x 4 transpose.
+__host__ __device__ constexpr int pos_b(int b, int m) {
+    return b == 8 ? m : (b == 4 ? 8 * (m >> 3) + 2 * (m & 3) + ((m >> 2) & 1) : 4 * (m & 3) + (m >> 2));
+}
+__host__ __device__ constexpr int kidx_b(int b, int j) {
+    return b == 8 ? j : (b == 4 ? 8 * (j >> 3) + 4 * (j & 1) + ((j & 7) >> 1) : 4 * (j & 3) + (j >> 2));
+}
+
 // Slot of (token t in tile, coordinate i). K: token-major inside groups of 16
-// coordinates (so a token's 16 codes of a group are 16 aligned slots), the
-// r % 16 tail group token-major after them. V: coordinate-major with the 4x4
-// (a, c) transpose of the token index.
+// coordinates (a token's 16 codes of a group are 16 consecutive slots), the
+// r % 16 tail group token-major after them. V: coordinate-major, each quarter
+// of 16 tokens in the order pos_b.
 __device__ __forceinline__ int slot_k(int t, int i, int r) {
     const int g16 = r >> 4;
     if (i < 16 * g16) return ((i >> 4) << 10) + (t << 4) + (i & 15);
@@ -39,10 +50,14 @@ __device__ __forceinline__ void unslot_k(int phi, int r, int& t, int& i) {
     t = q / rho;
     i = 16 * g16 + (q - t * rho);
 }
-__device__ __forceinline__ int psi(int t) { return (t & 0x03) | ((t & 0x0c) << 2) | ((t & 0x30) >> 2); }
-__device__ __forceinline__ int slot_v(int t, int i) { return i * 64 + psi(t); }
+__device__ __forceinline__ int slot_v(int t, int i, int b) { return i * 64 + (t & 48) + pos_b(b, t & 15); }
+__device__ __forceinline__ void unslot_v(int phi, int b, int& t, int& i) {
+    i = phi >> 6;
+    t = (phi & 48) + kidx_b(b, phi & 15);
+}
 
-// Code stored in slot phi of the tile starting at `tile` (planes widest first).
+// Code stored in slot phi of the tile starting at `tile`: the p bits of each plane
+// (widest first) sit at bits [p phi, p phi + p) of the plane.
 __device__ __forceinline__ uint32_t load_code(const uint8_t* __restrict__ tile, int r, int b, int phi) {
     if (b == 8) return tile[phi];
     uint32_t c = 0;
@@ -51,12 +66,9 @@ __device__ __forceinline__ uint32_t load_code(const uint8_t* __restrict__ tile, 
 #pragma unroll
     for (int p = 4; p >= 1; p >>= 1) {
         if (b & p) {
-            const int per_word = 32 / p;
-            const int w = phi / per_word, iota = phi % per_word;
-            const int bit = 8 * (iota & 3) + p * (iota >> 2);
-            const uint32_t word = reinterpret_cast<const uint32_t*>(tile + off)[w];
+            const int bit = p * phi;
             rem -= p;
-            c |= ((word >> bit) & ((1u << p) - 1u)) << rem;
+            c |= ((uint32_t)(tile[off + (bit >> 3)] >> (bit & 7)) & ((1u << p) - 1u)) << rem;
             off += 8 * r * p;
         }
     }
@@ -71,10 +83,10 @@ __host__ __device__ constexpr int plane_w(int b, int k) {
     return b == 8 ? 8 : (k == 0 ? ((b & 4) ? 4 : ((b & 2) ? 2 : 1))
                                : (k == 1 ? ((b & 4) ? ((b & 2) ? 2 : 1) : 1) : 1));
 }
-__host__ __device__ constexpr int plane_sh(int b, int k) {
-    return k + 1 >= n_planes(b) ? 0 : plane_w(b, k + 1) + plane_sh(b, k + 1);
-}
-__host__ __device__ constexpr int plane_off(int b, int k) { return k == 0 ? 0 : plane_w(b, k - 1) + plane_off(b, k - 1); }
+// Bits below plane k (its shift) and plane widths before it (its offset): closed forms, so that
+// they fold to constants even where k is an unrolled loop index.
+__host__ __device__ constexpr int plane_sh(int b, int k) { return b == 8 ? 0 : (b & (plane_w(b, k) - 1)); }
+__host__ __device__ constexpr int plane_off(int b, int k) { return b == 8 ? 0 : (b & ~(2 * plane_w(b, k) - 1)); }
 
 // Runs CALL with the compile-time bit width B_ equal to the runtime value b.
 #define KVC_SWITCH_B(b, CALL)                                \

@@ -128,9 +128,26 @@ __device__ uint32_t resolve_code_wave(const uint16_t* __restrict__ Pl_row, const
     return exact_code(Pg_row, xrow, step, b);
 }
 
+// Four slots (one code per byte of v, already masked to P bits) packed into 4 P consecutive bits.
+template <int P>
+__device__ __forceinline__ uint32_t compact4(uint32_t v) {
+    if constexpr (P == 4) {
+        v = (v | (v >> 4)) & 0x00ff00ffu;
+        return (v | (v >> 8)) & 0xffffu;
+    } else if constexpr (P == 2) {
+        v = (v | (v >> 6)) & 0x000f000fu;
+        return (v | (v >> 12)) & 0xffu;
+    } else if constexpr (P == 1) {
+        v = (v | (v >> 7)) & 0x00030003u;
+        return (v | (v >> 14)) & 0xfu;
+    } else {
+        return v;
+    }
+}
+
 // Packs slots [sl0, sl0 + n_sl) of a tile (their codes are bytes sb[0 .. n_sl) in slot order)
-// into every bit plane of a B-bit code: word w of a plane of width p takes slots
-// [w 32/p, (w + 1) 32/p); dword m of those bytes holds slots 4m .. 4m + 3, shifted by p m.
+// into every bit plane of a B-bit code: slot phi of a plane of width p takes bits
+// [p phi, p phi + p), so word w of the plane holds slots [w 32/p, (w + 1) 32/p) in order.
 template <int B, int K>
 __device__ __forceinline__ void pack_plane(const uint8_t* __restrict__ sb, uint8_t* __restrict__ tbase, int r, int sl0,
                                            int n_sl, int lane) {
@@ -143,7 +160,7 @@ __device__ __forceinline__ void pack_plane(const uint8_t* __restrict__ sb, uint8
             const uint32_t* src = reinterpret_cast<const uint32_t*>(sb + wi * PPW);
             uint32_t word = 0;
 #pragma unroll
-            for (int m = 0; m < PPW / 4; ++m) word |= ((src[m] >> SH) & PM) << (P * m);
+            for (int m = 0; m < PPW / 4; ++m) word |= compact4<P>((src[m] >> SH) & PM) << (4 * P * m);
             pw[wi] = word;
         }
     }
@@ -283,8 +300,16 @@ __global__ __launch_bounds__(kEncMmaThreads) __attribute__((amdgpu_waves_per_eu(
                             if (4 * grp + i < rho) sb[(16 * nt + col) * rho + 4 * grp + i] = (uint8_t)(cw[nt] >> (8 * i));
                 }
             } else if (16 * mc + col < r) {
+                // tokens 16 nt + 4 grp + i of coordinate row col; quarter nt holds them in the order pos_b
+                if (b == 8) {
 #pragma unroll
-                for (int nt = 0; nt < 4; ++nt) *reinterpret_cast<uint32_t*>(sb + 64 * col + 16 * grp + 4 * nt) = cw[nt];
+                    for (int nt = 0; nt < 4; ++nt) *reinterpret_cast<uint32_t*>(sb + 64 * col + 16 * nt + 4 * grp) = cw[nt];
+                } else {
+#pragma unroll
+                    for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) sb[64 * col + 16 * nt + pos_b(b, 4 * grp + i)] = (uint8_t)(cw[nt] >> (8 * i));
+                }
             }
             // undecided elements (rare): flag them again per lane, then the whole wavefront settles
             // them one by one
@@ -318,7 +343,7 @@ __global__ __launch_bounds__(kEncMmaThreads) __attribute__((amdgpu_waves_per_eu(
                         } else {
                             tkn = 16 * nt + 4 * Lgrp + i;
                             c = 16 * mc + Lcol;
-                            sl = 64 * Lcol + 16 * Lgrp + 4 * nt + i;
+                            sl = 64 * Lcol + 16 * nt + pos_b(b, 4 * Lgrp + i);
                         }
                         const uint16_t* xrow = xu + (int64_t)(tok0 + tkn - t0) * kD;
                         const uint32_t code = resolve_code_wave(Pl + c * kPRow, Pg + (int64_t)c * kD, xrow, step, b,
@@ -347,10 +372,10 @@ __global__ __launch_bounds__(kEncMmaThreads) __attribute__((amdgpu_waves_per_eu(
                             const int ph = sl0 + wi * ppw + io;
                             int t2, i2;
                             if constexpr (side == KVC_SIDE_K) unslot_k(ph, r, t2, i2);
-                            else { i2 = ph >> 6; t2 = psi(ph & 63); }
+                            else unslot_v(ph, b, t2, i2);
                             const int tk = tok0 + t2;
                             if (tk >= lo && tk < hi) {
-                                const int bit = 8 * (io & 3) + p * (io >> 2);
+                                const int bit = p * io;
                                 word |= (((uint32_t)sb[wi * ppw + io] >> sh) & vm) << bit;
                                 msk |= vm << bit;
                             }
@@ -431,7 +456,7 @@ __global__ __launch_bounds__(kAppThreads) void append_kernel(DevSide s, int side
     uint8_t* __restrict__ stream = s.codes + s.code_off[u];
     for (int t = 0; t < n_tok; ++t) {
         const int tok = t0 + t, tile = tok / kTile, tt = tok % kTile;
-        const int phi = side == KVC_SIDE_K ? slot_k(tt, i, r) : slot_v(tt, i);
+        const int phi = side == KVC_SIDE_K ? slot_k(tt, i, r) : slot_v(tt, i, b);
         uint8_t* __restrict__ tbase = stream + (int64_t)tile * 8 * r * b;
         for (int p = 8; p >= 1; p >>= 1) {
             if (b == 8 ? p != 8 : (p == 8 || !(b & p))) continue;
@@ -446,11 +471,11 @@ __global__ __launch_bounds__(kAppThreads) void append_kernel(DevSide s, int side
                 const int ph = lw * ppw + iota;
                 int t2, i2;
                 if (side == KVC_SIDE_K) unslot_k(ph, r, t2, i2);
-                else { i2 = ph >> 6; t2 = psi(ph & 63); }
+                else unslot_v(ph, b, t2, i2);
                 const int tk = tile * kTile + t2 - t0;
                 if (tk >= 0 && tk < n_tok) {
                     if (first) { leader = tk == t && i2 == i; first = false; }
-                    const int bit = 8 * (iota & 3) + p * (iota >> 2);
+                    const int bit = p * iota;
                     val |= ((uint32_t)(cs[tk][i2] >> sh) & vmask) << bit;
                     msk |= vmask << bit;
                 }
@@ -487,7 +512,7 @@ __global__ __launch_bounds__(kRecThreads) void reconstruct_kernel(DevSide s, int
         if (tok < t0 + n_tok) {
             const uint8_t* tile = stream + (int64_t)(tok / kTile) * 8 * r * b;
             const int tl = tok % kTile;
-            const int phi = side == KVC_SIDE_K ? slot_k(tl, i, r) : slot_v(tl, i);
+            const int phi = side == KVC_SIDE_K ? slot_k(tl, i, r) : slot_v(tl, i, b);
             z = ((float)load_code(tile, r, b, phi) - half) * step;
         }
         zh[tt * zs + i] = z;

@@ -69,26 +69,43 @@ def test_c_exact_encode_on_exact_thresholds():
 
 
 def test_layout_hand_derived_bit_positions():
-    # K side, r = 2, b = 1: slot(t=0, i=1) = 1 -> word 0, bit 8 * 1 + 1 * 0 = 8
+    # K side, r = 2, b = 1 (tail group only): slot(t=0, i=1) = 0*2 + 1 = 1 -> bit 1 of byte 0
     c = np.zeros((64, 2), dtype=np.uint8)
     c[0, 1] = 1
     s = onat.pack(c, 2, 1, ol.SIDE_K)
-    assert s.size == 16 and list(np.nonzero(s)[0]) == [1] and s[1] == 1
-    # K side, r = 2, b = 1: slot(t=2, i=0) = 4 -> iota 4 -> bit 8 * 0 + 1 * 1 = 1
+    assert s.size == 16 and list(np.nonzero(s)[0]) == [0] and s[0] == 2
+    # K side, r = 2, b = 1: slot(t=2, i=0) = 4 -> bit 4 of byte 0
     c[:] = 0
     c[2, 0] = 1
     s = onat.pack(c, 2, 1, ol.SIDE_K)
-    assert list(np.nonzero(s)[0]) == [0] and s[0] == 2
-    # V side, r = 2, b = 1: coord 1, token 0 -> slot 64 -> word 2, bit 0 -> byte 8
+    assert list(np.nonzero(s)[0]) == [0] and s[0] == 16
+    # V side, r = 2, b = 1: coord 1, token 0 -> slot 64 -> bit 64 -> byte 8
     c[:] = 0
     c[0, 1] = 1
     s = onat.pack(c, 2, 1, ol.SIDE_V)
     assert list(np.nonzero(s)[0]) == [8] and s[8] == 1
-    # V side: token 5 = 16*0 + 4*1 + 1 -> psi = 16*1 + 4*0 + 1 = 17 -> iota 17 -> bit 8*1 + 4 = 12 -> byte 1, bit 4
+    # V side, b = 1: token 6 (quarter 0, item 6) -> position 4*2 + 1 = 9 -> bit 9 -> byte 1, bit 1;
+    # token 17 (quarter 1, item 1) -> slot 16 + 4 = 20 -> byte 2, bit 4
     c[:] = 0
-    c[5, 0] = 1
+    c[6, 0] = 1
+    c[17, 0] = 1
     s = onat.pack(c, 2, 1, ol.SIDE_V)
-    assert list(np.nonzero(s)[0]) == [1] and s[1] == 16
+    assert list(np.nonzero(s)[0]) == [1, 2] and s[1] == 2 and s[2] == 16
+    # V side, b = 2: token 13 -> position 4*1 + 3 = 7 -> bits 14, 15 -> byte 1, value 3 << 6
+    c[:] = 0
+    c[13, 0] = 3
+    s = onat.pack(c, 2, 2, ol.SIDE_V)
+    assert list(np.nonzero(s)[0]) == [1] and s[1] == 0xC0
+    # V side, b = 4: token 5 -> position 8*0 + 2*1 + 1 = 3 -> bits 12..15 -> high nibble of byte 1
+    c[:] = 0
+    c[5, 0] = 0xA
+    s = onat.pack(c, 2, 4, ol.SIDE_V)
+    assert list(np.nonzero(s)[0]) == [1] and s[1] == 0xA0
+    # V side, b = 8: natural token order, one byte per slot: coord 1, token 37 -> slot 64 + 37
+    c8 = np.zeros((64, 2), dtype=np.uint8)
+    c8[37, 1] = 200
+    s = onat.pack(c8, 2, 8, ol.SIDE_V)
+    assert list(np.nonzero(s)[0]) == [101] and s[101] == 200
     # K side with a tail group, r = 18 (one group of 16 + 2 tail coordinates), b = 8 (plain bytes):
     # token 1, coordinate 3 -> slot 0*1024 + 1*16 + 3 = 19; token 1, coordinate 17 -> slot 1024 + 1*2 + 1 = 1027
     c18 = np.zeros((64, 18), dtype=np.uint8)
@@ -96,6 +113,12 @@ def test_layout_hand_derived_bit_positions():
     c18[1, 17] = 9
     s = onat.pack(c18, 18, 8, ol.SIDE_K)
     assert list(np.nonzero(s)[0]) == [19, 1027] and s[19] == 7 and s[1027] == 9
+    # K side, r = 18, b = 2: token 3, coordinate 17 -> tail slot 1024 + 3*2 + 1 = 1031 -> bits 2062, 2063
+    # -> byte 257, bits 6..7
+    c18[:] = 0
+    c18[3, 17] = 2
+    s = onat.pack(c18, 18, 2, ol.SIDE_K)
+    assert list(np.nonzero(s)[0]) == [257] and s[257] == 0x80
     # b = 8 on the K side with r < 16 is plain bytes in token-major order
     c = np.arange(64 * 2, dtype=np.uint8).reshape(64, 2)
     s = onat.pack(c, 2, 8, ol.SIDE_K)
@@ -105,6 +128,14 @@ def test_layout_hand_derived_bit_positions():
     c[0, 0] = 0b110
     s = onat.pack(c, 2, 3, ol.SIDE_K)
     assert s.size == 48 and s[0] == 0b11 and np.count_nonzero(s) == 1
+
+
+@pytest.mark.parametrize("b", range(1, 9))
+def test_v_token_order_is_a_permutation_of_each_quarter(b):
+    pos = [ol.pos_b(b, m) for m in range(16)]
+    assert sorted(pos) == list(range(16))
+    if b != 4:
+        assert all(ol.pos_b(b, ol.pos_b(b, m)) == m for m in range(16))
 
 
 @pytest.mark.parametrize("side", [ol.SIDE_K, ol.SIDE_V])
