@@ -709,7 +709,6 @@ __device__ __noinline__ void run_item(const DevSide& K, const DevSide& V, const 
         }
 
         // ---- online softmax
-        float mx[LM];
         const bool last = tok0 + kTile > end;
         bool raise = first;
         if (last) {  // tokens past the end of the chunk
@@ -724,12 +723,18 @@ __device__ __noinline__ void run_item(const DevSide& K, const DevSide& V, const 
             for (int lm = 0; lm < LM; ++lm)
                 if (4 * lm + grp >= G) s[lm][0] = s[lm][1] = s[lm][2] = s[lm][3] = -INFINITY;
         }
+        // A head's row max beats kLazy exactly when one of its lanes' own maxima does: the common
+        // path tests the lane maxima only and takes the cross-lane row max inside the rare branch.
+        float ml[LM];
 #pragma unroll
         for (int lm = 0; lm < LM; ++lm) {
-            mx[lm] = row_max(fmaxf(fmaxf(s[lm][0], s[lm][1]), fmaxf(s[lm][2], s[lm][3])));
-            raise = raise || mx[lm] > kLazy;
+            ml[lm] = fmaxf(fmaxf(s[lm][0], s[lm][1]), fmaxf(s[lm][2], s[lm][3]));
+            raise = raise || ml[lm] > kLazy;
         }
         if (__any(raise)) {
+            float mx[LM];
+#pragma unroll
+            for (int lm = 0; lm < LM; ++lm) mx[lm] = row_max(ml[lm]);
             // Raise the max of each head whose tile beats it by more than 2^kLazy (every head on the
             // first tile) to the tile's own max, and rescale that head's accumulators exactly (every
             // limb of a (head, coordinate) sits in this lane): value = C0 + 2^8 C1 + 2^16 C2 ->

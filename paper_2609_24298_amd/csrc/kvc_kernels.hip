@@ -8,9 +8,10 @@
 //                       codes decided against a rigorous error bound (undecided
 //                       elements settled in fp64, then exactly in 128-bit
 //                       integers), bit-packed from LDS group by group.
-//  append_kernel        1-4 new tokens per unit (a decode step's append): one
-//                       thread per coordinate, the same decision, and a merge of
-//                       the new bits into the packed words.
+//  append_kernel        1-4 new tokens per unit (a decode step's append): basis
+//                       rows read coalesced, the same bounded decision (undecided
+//                       elements settled by their wavefront), and the new fields
+//                       written in place (whole words where a token owns them).
 //  reconstruct_kernel   x_hat = P^T z for a 64-token block of one unit.
 #include <hip/hip_runtime.h>
 
@@ -57,24 +58,18 @@ __device__ __forceinline__ uint32_t exact_code(const uint16_t* __restrict__ Prow
     return (uint32_t)(first_fail - (1 - h));
 }
 
-// Code from the fp32 projection `acc` whose error is at most `err`
-// (|acc - y| <= err). Falls back to exact_code when a quantizer threshold
-// j * step, j in [1 - 2^(b-1), 2^(b-1) - 1], is not clearly separated.
-__device__ __forceinline__ uint32_t decide_code(float acc, float err, float step, int b,
-                                                const uint16_t* Prow, const uint16_t* xrow) {
+// Code from the fp32 projection `acc` whose error is at most `err` (|acc - y| <= err), when no
+// quantizer threshold j * step, j in [1 - 2^(b-1), 2^(b-1) - 1], lies within that error: returns
+// false (undecided) otherwise.
+__device__ __forceinline__ bool fast_code(float acc, float err, float step, int b, uint32_t& code) {
     const int h = 1 << (b - 1);
     const double st = step, yd = acc, ed = err;
     const double t = yd / st;
-    bool amb = !(ed < 0.25 * st);
-    if (!amb) {
-        const double jn = rint(t);
-        if (jn >= 1 - h && jn <= h - 1) amb = !(fabs(yd - jn * st) > ed + 0x1p-45 * fabs(yd));
-    }
-    if (!amb) {
-        const double kd = fmin(fmax(floor(t) + h, 0.0), (double)((1 << b) - 1));
-        return (uint32_t)kd;
-    }
-    return exact_code(Prow, xrow, step, b);
+    if (!(ed < 0.25 * st)) return false;
+    const double jn = rint(t);
+    if (jn >= 1 - h && jn <= h - 1 && !(fabs(yd - jn * st) > ed + 0x1p-45 * fabs(yd))) return false;
+    code = (uint32_t)fmin(fmax(floor(t) + h, 0.0), (double)((1 << b) - 1));
+    return true;
 }
 
 // ---------------------------------------------------------------- bulk encode on matrix cores
@@ -392,9 +387,19 @@ __global__ __launch_bounds__(kEncMmaThreads) __attribute__((amdgpu_waves_per_eu(
 
 // ---------------------------------------------------------------- append
 
-// Appending a few tokens (a decode step adds one per unit): one block per unit, thread i
-// computes coordinate i of every new token from its basis row, decides the code as
-// the bulk encoder does, and the new codes are merged into the packed words of their tiles.
+// Sum over the 16 lanes of a DPP row, returned in every lane of the row (row rotations).
+__device__ __forceinline__ float row_sum16(float v) {
+    v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x128, 0xf, 0xf, true));
+    v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x124, 0xf, 0xf, true));
+    v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x122, 0xf, 0xf, true));
+    v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x121, 0xf, 0xf, true));
+    return v;
+}
+
+// Appending a few tokens (a decode step adds one per unit): one block per unit; coordinate i of
+// every new token is projected from basis row i, its code decided against the fp32 error bound
+// (the wavefront settles the rare undecided ones as the bulk encoder does), and the new codes are
+// written into their tiles.
 constexpr int kAppThreads = kD;
 constexpr int kAppMaxTok = 4;
 
@@ -403,6 +408,8 @@ __global__ __launch_bounds__(kAppThreads) void append_kernel(DevSide s, int side
     __shared__ float xs[kAppMaxTok][kD];
     __shared__ float red[kAppMaxTok][kAppThreads / 64];
     __shared__ uint8_t cs[kAppMaxTok][kD];
+    __shared__ float ys[kAppMaxTok][kD];
+    __shared__ float pns[kD];
     const int u = blockIdx.x, i = threadIdx.x;
     const int r = s.r[u], b = s.b[u];
     const float step = s.delta[u];
@@ -416,73 +423,110 @@ __global__ __launch_bounds__(kAppThreads) void append_kernel(DevSide s, int side
         if ((i & 63) == 0) red[t][i >> 6] = s2;
     }
     __syncthreads();
-    if (i < r) {
-        float acc[kAppMaxTok] = {0.f, 0.f, 0.f, 0.f};
-        float pn2 = 0.f;
-        const uint4* Pr = reinterpret_cast<const uint4*>(P + (int64_t)i * kD);
-#pragma unroll 4
-        for (int q = 0; q < kD / 8; ++q) {
-            const uint4 w = Pr[q];
-            const uint32_t w4[4] = {w.x, w.y, w.z, w.w};
-            float pv[8];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                pv[2 * e] = h2f((uint16_t)(w4[e] & 0xffff));
-                pv[2 * e + 1] = h2f((uint16_t)(w4[e] >> 16));
-            }
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                pn2 = fmaf(pv[e], pv[e], pn2);
-#pragma unroll
-                for (int t = 0; t < kAppMaxTok; ++t)
-                    if (t < n_tok) acc[t] = fmaf(pv[e], xs[t][8 * q + e], acc[t]);
-            }
-        }
-        const float pn = sqrtf(pn2);
+    {
+        // Coalesced projection: in pass k, the 16 lanes (rr, c) of a row group read 16 bytes each of
+        // basis row 8 k + rr (the whole 256-byte row), form partial dot products over their 8 columns
+        // and sum them across the group with row rotations. Every row's loads are issued up front.
+        const int c = i & 15, rr = i >> 4;
+        float xr[kAppMaxTok][8];
 #pragma unroll
         for (int t = 0; t < kAppMaxTok; ++t)
-            if (t < n_tok) {
-                // |acc - y| <= 2^-17 ||P_i|| ||x|| for a 128-term fp32 sum, used with a 4x margin
-                const float xn = sqrtf(red[t][0] + red[t][1]);
-                cs[t][i] = (uint8_t)decide_code(acc[t], 0x1p-15f * pn * xn, step, b, P + (int64_t)i * kD,
-                                                xu + (int64_t)t * kD);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) xr[t][e] = t < n_tok ? xs[t][8 * c + e] : 0.f;
+        uint4 w[kD / 8];
+#pragma unroll
+        for (int k = 0; k < kD / 8; ++k) {
+            const int row = 8 * k + rr;
+            w[k] = row < r ? reinterpret_cast<const uint4*>(P + (int64_t)row * kD)[c] : uint4{0u, 0u, 0u, 0u};
+        }
+#pragma unroll
+        for (int k = 0; k < kD / 8; ++k) {
+            const uint32_t w4[4] = {w[k].x, w[k].y, w[k].z, w[k].w};
+            float pn = 0.f, acc[kAppMaxTok] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const float pv = h2f((uint16_t)(w4[e >> 1] >> (16 * (e & 1))));
+                pn = fmaf(pv, pv, pn);
+#pragma unroll
+                for (int t = 0; t < kAppMaxTok; ++t) acc[t] = fmaf(pv, xr[t][e], acc[t]);
             }
+            pn = row_sum16(pn);
+#pragma unroll
+            for (int t = 0; t < kAppMaxTok; ++t)
+                if (t < n_tok) acc[t] = row_sum16(acc[t]);
+            if (c == 0) {
+                const int row = 8 * k + rr;
+                pns[row] = pn;
+#pragma unroll
+                for (int t = 0; t < kAppMaxTok; ++t) ys[t][row] = acc[t];
+            }
+        }
+    }
+    __syncthreads();
+    {
+        // Codes decided in fp32 where the error bound allows; each undecided element is then
+        // resolved by its whole wavefront (fp64, then exact), one element at a time.
+        const int lane = i & 63;
+        const float pn = i < r ? sqrtf(pns[i]) : 0.f;
+        for (int t = 0; t < n_tok; ++t) {
+            // |acc - y| <= 2^-17 ||P_i|| ||x|| for a 128-term fp32 sum in any order, used with a 4x margin
+            const float xn = sqrtf(red[t][0] + red[t][1]);
+            uint32_t code = 0;
+            const bool amb = i < r && !fast_code(ys[t][i], 0x1p-15f * pn * xn, step, b, code);
+            uint64_t m = __ballot(amb);
+            while (m) {
+                const int l = __builtin_ctzll(m);
+                m &= m - 1;
+                const int il = (i & ~63) + l;
+                const uint16_t* Prow = P + (int64_t)il * kD;
+                const uint32_t cl = resolve_code_wave(Prow, Prow, xu + (int64_t)t * kD, step, b, sqrtf(pns[il]), xn, lane);
+                if (lane == l) code = cl;
+            }
+            if (i < r) cs[t][i] = (uint8_t)code;
+        }
     }
     __syncthreads();
     if (i >= r) return;
-    // Merge: thread (t, i) visits the word holding slot (t, i) in each plane. The word's first slot
-    // that belongs to a new token elects one thread per word, which rewrites the new tokens' bits
-    // of that word and keeps every other bit.
+    // Merge, per new token and plane. K: a token's 16 codes of a full coordinate group are 16
+    // consecutive slots, i.e. whole 16-bit (p = 1) or 32-bit words that belong to this token alone:
+    // the group's lanes OR their fields together and one lane per word stores it. The tail group's
+    // fields, and every V field (one slot of a coordinate row shared with other tokens), are written
+    // in place with an atomic clear and set of the field's bits (a field never straddles a word).
+    // One thread owns each coordinate, so the new tokens of a call are written in order.
     uint8_t* __restrict__ stream = s.codes + s.code_off[u];
+    const int g16 = r >> 4, rho = r & 15;
     for (int t = 0; t < n_tok; ++t) {
         const int tok = t0 + t, tile = tok / kTile, tt = tok % kTile;
-        const int phi = side == KVC_SIDE_K ? slot_k(tt, i, r) : slot_v(tt, i, b);
         uint8_t* __restrict__ tbase = stream + (int64_t)tile * 8 * r * b;
-        for (int p = 8; p >= 1; p >>= 1) {
-            if (b == 8 ? p != 8 : (p == 8 || !(b & p))) continue;
+        const uint32_t c = cs[t][i];
+        for (int k = 0; k < 4; ++k) {
+            const int p = b == 8 ? (k == 0 ? 8 : 0) : (k == 0 ? 4 : (k == 1 ? 2 : (k == 2 ? 1 : 0)));
+            if (p == 0 || (b != 8 && !(b & p))) continue;
             const int sh = b == 8 ? 0 : (b & (p - 1));
             const int off = b == 8 ? 0 : (b & ~(2 * p - 1));
-            const int ppw = 32 / p;
-            const uint32_t vmask = p == 8 ? 0xffu : ((1u << p) - 1u);
-            const int lw = phi / ppw;
-            uint32_t val = 0, msk = 0;
-            bool first = true, leader = false;
-            for (int iota = 0; iota < ppw; ++iota) {
-                const int ph = lw * ppw + iota;
-                int t2, i2;
-                if (side == KVC_SIDE_K) unslot_k(ph, r, t2, i2);
-                else unslot_v(ph, b, t2, i2);
-                const int tk = tile * kTile + t2 - t0;
-                if (tk >= 0 && tk < n_tok) {
-                    if (first) { leader = tk == t && i2 == i; first = false; }
-                    const int bit = p * iota;
-                    val |= ((uint32_t)(cs[tk][i2] >> sh) & vmask) << bit;
-                    msk |= vmask << bit;
+            const uint32_t pb = p == 8 ? c : (c >> sh) & ((1u << p) - 1u);
+            uint8_t* __restrict__ base = tbase + 8 * r * off;
+            if (side == KVC_SIDE_K && i < 16 * g16) {
+                const int lpw = p >= 4 ? 32 / p : 16;  // lanes whose fields share one stored word
+                const int fb = p * (i & 15);            // field bit within the group's run
+                uint32_t v = pb << (fb & 31);
+                for (int o = 1; o < lpw; o <<= 1) v |= __shfl_xor(v, o);
+                if ((i & (lpw - 1)) == 0) {
+                    uint8_t* w = base + p * (128 * (i >> 4) + 2 * tt) + (fb >> 3);
+                    if (p == 1) *reinterpret_cast<uint16_t*>(w) = (uint16_t)v;
+                    else *reinterpret_cast<uint32_t*>(w) = v;
                 }
-            }
-            if (leader) {
-                uint32_t* wp = reinterpret_cast<uint32_t*>(tbase + 8 * r * off) + lw;
-                *wp = (*wp & ~msk) | val;
+            } else {
+                const int phi = side == KVC_SIDE_K ? 1024 * g16 + tt * rho + (i - 16 * g16) : slot_v(tt, i, b);
+                const int bit = p * phi;
+                if (p == 8) {
+                    base[bit >> 3] = (uint8_t)pb;
+                } else {
+                    uint32_t* wp = reinterpret_cast<uint32_t*>(base) + (bit >> 5);
+                    const uint32_t m = ((1u << p) - 1u) << (bit & 31);
+                    atomicAnd(wp, ~m);
+                    atomicOr(wp, pb << (bit & 31));
+                }
             }
         }
     }
