@@ -461,19 +461,38 @@ __device__ __forceinline__ void v_tile(uint32_t* vb, const __amdgpu_buffer_rsrc_
 // operand byte m <-> coordinate 16 (4 ks + grp) + pos_b(m) (zero outside the rank, for limb 3 and for
 // heads >= G). qk[u][h] = (sigma, sigma / 254, sigma / 254^2, bias) with
 // bias = -2^(b-1) sum_limb k_limb sum_i L_limb,i (0 for b = 8, whose codes are centred on load).
+constexpr int kQpRow = kD / 2 + 1;  // LDS words per staged basis row (fp16 pairs, padded: no bank conflicts)
 __global__ __launch_bounds__(kD) void qprep_kernel(DevSide K, const uint16_t* __restrict__ q, int G, int LM,
                                                    v4i* __restrict__ qa, float4* __restrict__ qk) {
     extern __shared__ float qsm[];
-    float* qsh = qsm;                                                  // [G][128]
-    uint8_t* img = reinterpret_cast<uint8_t*>(qsh + G * kD);           // [2][LM][64][16] operand image
-    __shared__ float fred[kD / 64];
-    __shared__ int ired[kLimbs][kD / 64];
+    float* qsh = qsm;                                                        // [G][128]
+    uint8_t* img = reinterpret_cast<uint8_t*>(qsh + G * kD);                 // [2][LM][64][16] operand image
+    uint32_t* ps = reinterpret_cast<uint32_t*>(img + 2 * LM * 64 * 16);      // [r][kQpRow] basis rows
+    float* qts = reinterpret_cast<float*>(ps + kD * kQpRow);                 // [G][128] q~
+    __shared__ float fred[16][kD / 64];
+    __shared__ int ired[16][kLimbs][kD / 64];
     const int u = blockIdx.x, i = threadIdx.x, lane = i & 63, wv = i >> 6;
-    for (int g = 0; g < G; ++g) qsh[g * kD + i] = h2f(q[((int64_t)u * G + g) * kD + i]);
-    const int img_words = 2 * LM * 64 * 4;
-    for (int k = i; k < img_words; k += kD) reinterpret_cast<uint32_t*>(img)[k] = 0u;
-    __syncthreads();
     const int r = K.r[u], b = K.b[u];
+    // stage q, clear the image, stage the basis rows (coalesced 16-byte loads, all in flight)
+    {
+        const uint4* __restrict__ P4 = reinterpret_cast<const uint4*>(K.basis + K.basis_off[u]);
+        const int n4 = r * kD / 8;
+        uint4 w[kD / 8];
+#pragma unroll
+        for (int k = 0; k < kD / 8; ++k) w[k] = k * kD + i < n4 ? P4[k * kD + i] : uint4{0u, 0u, 0u, 0u};
+        for (int g = 0; g < G; ++g) qsh[g * kD + i] = h2f(q[((int64_t)u * G + g) * kD + i]);
+        const int img_words = 2 * LM * 64 * 4;
+        for (int k = i; k < img_words; k += kD) reinterpret_cast<uint32_t*>(img)[k] = 0u;
+#pragma unroll
+        for (int k = 0; k < kD / 8; ++k) {
+            const int c4 = k * kD + i;  // uint4 index: row c4 / 16, words 4 (c4 % 16) ..
+            if (c4 < n4) {
+                uint32_t* d = ps + (c4 >> 4) * kQpRow + 4 * (c4 & 15);
+                d[0] = w[k].x; d[1] = w[k].y; d[2] = w[k].z; d[3] = w[k].w;
+            }
+        }
+    }
+    __syncthreads();
     const int hk = b == 8 ? 0 : (1 << (b - 1));
     const float scale0 = K.delta[u] * 1.4426950408889634f * 0.08838834764831845f;  // log2(e) / sqrt(128)
     // destination of coordinate i in the operand image
@@ -483,32 +502,29 @@ __global__ __launch_bounds__(kD) void qprep_kernel(DevSide K, const uint16_t* __
     const int ks = cg >> 2, grp = cg & 3;
     int kidx = 0;
     KVC_SWITCH_B(b, kidx = kidx_b(B_, jpos));
-    float prow[kD];
-    {
-        const uint4* P4 = reinterpret_cast<const uint4*>(K.basis + K.basis_off[u] + (int64_t)(i < r ? i : 0) * kD);
-#pragma unroll
-        for (int c = 0; c < kD / 8; ++c) {
-            const uint4 w = P4[c];
-            const uint32_t w4[4] = {w.x, w.y, w.z, w.w};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                prow[8 * c + 2 * e] = i < r ? h2f((uint16_t)(w4[e] & 0xffff)) : 0.f;
-                prow[8 * c + 2 * e + 1] = i < r ? h2f((uint16_t)(w4[e] >> 16)) : 0.f;
-            }
-        }
-    }
+    // q~_g,i for every head (thread i: basis row i), then every head's max |q~| in one round
     for (int g = 0; g < G; ++g) {
         float acc = 0.f;
-#pragma unroll
-        for (int j = 0; j < kD; ++j) acc = fmaf(prow[j], qsh[g * kD + j], acc);
+        if (i < r) {
+            const uint32_t* row = ps + i * kQpRow;
+#pragma unroll 8
+            for (int j = 0; j < kD / 2; ++j) {
+                const uint32_t pw = row[j];
+                acc = fmaf(h2f((uint16_t)(pw & 0xffffu)), qsh[g * kD + 2 * j], acc);
+                acc = fmaf(h2f((uint16_t)(pw >> 16)), qsh[g * kD + 2 * j + 1], acc);
+            }
+        }
         const float qt = acc * scale0;
+        qts[g * kD + i] = qt;
         float m = fabsf(qt);
         for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
-        if (lane == 0) fred[wv] = m;
-        __syncthreads();
-        const float amax = fmaxf(fred[0], fred[1]);
+        if (lane == 0) fred[g][wv] = m;
+    }
+    __syncthreads();
+    for (int g = 0; g < G; ++g) {
+        const float amax = fmaxf(fred[g][0], fred[g][1]);
         const float sigma = amax > 0.f ? amax / 127.f : 1.f;
-        const float x = qt / sigma;
+        const float x = qts[g * kD + i] / sigma;
         const float l0 = fminf(fmaxf(rintf(x), -127.f), 127.f);
         const float r1 = (x - l0) * 254.f;
         const float l1 = fminf(fmaxf(rintf(r1), -127.f), 127.f);
@@ -521,18 +537,19 @@ __global__ __launch_bounds__(kD) void qprep_kernel(DevSide K, const uint16_t* __
                 const int row_lane = 16 * grp + 4 * (g & 3) + k;
                 img[(((ks * LM + (g >> 2)) * 64 + row_lane) << 4) + kidx] = (uint8_t)(int8_t)L[k];
             }
-            int s = L[k];
-            for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
-            if (lane == 0) ired[k][wv] = s;
+            int sm = L[k];
+            for (int o = 32; o > 0; o >>= 1) sm += __shfl_xor(sm, o);
+            if (lane == 0) ired[g][k][wv] = sm;
         }
-        __syncthreads();
-        if (i == 0) {
-            const float k0 = sigma, k1 = sigma * (1.f / 254.f), k2 = sigma * (1.f / 64516.f);
-            const float bias = -(float)hk * ((float)(ired[0][0] + ired[0][1]) * k0 + (float)(ired[1][0] + ired[1][1]) * k1 +
-                                             (float)(ired[2][0] + ired[2][1]) * k2);
-            qk[(int64_t)u * G + g] = float4{k0, k1, k2, bias};
-        }
-        __syncthreads();
+    }
+    __syncthreads();
+    if (i < G) {
+        const int g = i;
+        const float sigma = fmaxf(fred[g][0], fred[g][1]) > 0.f ? fmaxf(fred[g][0], fred[g][1]) / 127.f : 1.f;
+        const float k0 = sigma, k1 = sigma * (1.f / 254.f), k2 = sigma * (1.f / 64516.f);
+        const float bias = -(float)hk * ((float)(ired[g][0][0] + ired[g][0][1]) * k0 + (float)(ired[g][1][0] + ired[g][1][1]) * k1 +
+                                         (float)(ired[g][2][0] + ired[g][2][1]) * k2);
+        qk[(int64_t)u * G + g] = float4{k0, k1, k2, bias};
     }
     v4i* dst = qa + (int64_t)u * 2 * LM * 64;
     for (int k = i; k < 2 * LM * 64; k += kD) dst[k] = reinterpret_cast<const v4i*>(img)[k];
@@ -893,46 +910,67 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(Shape<G>::W,
 
 // ---------------------------------------------------------------- combine
 
-// One block per unit, one wavefront per query head; lane l handles coordinates l and l + 64.
-// The chunks' partials merge in the log2 domain (M = max m_c, L = sum l_c 2^(m_c - M),
-// A_j = sum acc_c,j 2^(m_c - M)), z_j = step_V (A_j / L + 1/2) is the dequantised rank-space
-// average, and o = P_V^T z (the V reconstruction of Lemma lem:head-dist applied after the
-// softmax average, which is linear).
+// One block per unit, one wavefront per query head; lane l handles rank coordinates l and l + 64 of
+// the merge and output columns 2 l, 2 l + 1. The chunks' partials merge in the log2 domain
+// (M = max m_c, L = sum l_c 2^(m_c - M), A_j = sum acc_c,j 2^(m_c - M)), z_j = step_V (A_j / L + 1/2)
+// is the dequantised rank-space average, and o = P_V^T z (the V reconstruction of Lemma
+// lem:head-dist applied after the softmax average, which is linear). The block stages P_V in LDS
+// with coalesced loads while its wavefronts merge; chunk loads are issued in batches.
 constexpr int kMaxG = 16;
+constexpr int kCombBatch = 8;  // chunks whose loads are in flight together
 __global__ __launch_bounds__(64 * kMaxG) void combine_kernel(DevSide V, int G, int n_chunks, const float* __restrict__ part,
                                                              float* __restrict__ out) {
     __shared__ float zs[kMaxG][kD];
-    const int u = blockIdx.x, g = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    __shared__ uint32_t ps[kD * kD / 2];  // P_V rows as fp16 pairs
+    const int u = blockIdx.x, g = threadIdx.x >> 6, lane = threadIdx.x & 63, nth = 64 * G;
     const int rv = V.r[u];
     const float step = V.delta[u];
+    {
+        const uint4* __restrict__ P4 = reinterpret_cast<const uint4*>(V.basis + V.basis_off[u]);
+        const int n4 = rv * kD / 8;
+        for (int k = threadIdx.x; k < n4; k += nth) reinterpret_cast<uint4*>(ps)[k] = P4[k];
+    }
     const float* __restrict__ pg = part + (int64_t)u * n_chunks * G * kPartStride + g * kPartStride;
     const int64_t cs = (int64_t)G * kPartStride;
+    // M and L: lane c < n_chunks reads chunk c's (m, l) (in rounds of 64 chunks)
     float M = -INFINITY;
-    for (int c = 0; c < n_chunks; ++c) M = fmaxf(M, pg[c * cs]);
+    for (int c0 = 0; c0 < n_chunks; c0 += 64)
+        if (c0 + lane < n_chunks) M = fmaxf(M, pg[(c0 + lane) * cs]);
+    for (int o = 32; o > 0; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
     float L = 0.f, A0 = 0.f, A1 = 0.f;
-    for (int c = 0; c < n_chunks; ++c) {
-        const float* pc = pg + c * cs;
-        const float lc = pc[1];
-        if (lc > 0.f) {  // an empty chunk writes only m and l
-            const float w = exp2f(pc[0] - M);
-            L = fmaf(lc, w, L);
-            if (lane < rv) A0 = fmaf(pc[4 + lane], w, A0);
-            if (lane + 64 < rv) A1 = fmaf(pc[4 + 64 + lane], w, A1);
+    for (int c0 = 0; c0 < n_chunks; c0 += kCombBatch) {
+        float mc[kCombBatch], lc[kCombBatch], a0[kCombBatch], a1[kCombBatch];
+#pragma unroll
+        for (int k = 0; k < kCombBatch; ++k) {
+            const int c = min(c0 + k, n_chunks - 1);
+            const float* pc = pg + c * cs;
+            mc[k] = pc[0];
+            lc[k] = c0 + k < n_chunks ? pc[1] : 0.f;
+            a0[k] = pc[4 + lane];
+            a1[k] = pc[4 + 64 + lane];
+        }
+#pragma unroll
+        for (int k = 0; k < kCombBatch; ++k) {
+            if (lc[k] > 0.f) {  // an empty chunk (or a batch slot past the last) has l = 0 and no accumulator
+                const float w = exp2f(mc[k] - M);
+                L = fmaf(lc[k], w, L);
+                A0 = fmaf(a0[k], w, A0);
+                A1 = fmaf(a1[k], w, A1);
+            }
         }
     }
     const float inv = L > 0.f ? 1.f / L : 0.f;
     zs[g][lane] = (L > 0.f && lane < rv) ? step * fmaf(A0, inv, 0.5f) : 0.f;
     zs[g][lane + 64] = (L > 0.f && lane + 64 < rv) ? step * fmaf(A1, inv, 0.5f) : 0.f;
     __syncthreads();
-    const uint16_t* __restrict__ P = V.basis + V.basis_off[u];
     float o0 = 0.f, o1 = 0.f;
     for (int i = 0; i < rv; ++i) {
         const float z = zs[g][i];
-        o0 = fmaf(h2f(P[(int64_t)i * kD + lane]), z, o0);
-        o1 = fmaf(h2f(P[(int64_t)i * kD + lane + 64]), z, o1);
+        const uint32_t pw = ps[i * (kD / 2) + lane];
+        o0 = fmaf(h2f((uint16_t)(pw & 0xffffu)), z, o0);
+        o1 = fmaf(h2f((uint16_t)(pw >> 16)), z, o1);
     }
-    out[((int64_t)u * G + g) * kD + lane] = o0;
-    out[((int64_t)u * G + g) * kD + lane + 64] = o1;
+    reinterpret_cast<float2*>(out + ((int64_t)u * G + g) * kD)[lane] = float2{o0, o1};
 }
 
 // ---------------------------------------------------------------- host side
@@ -1098,7 +1136,7 @@ extern "C" int kvc_decode_attn(const kvc_stream_desc* k, const kvc_stream_desc* 
     hipStream_t st = (hipStream_t)stream;
     const DevSide K = dev_side(k), V = dev_side(v);
     const int LM = (G + 3) / 4;
-    const size_t qsm = (size_t)G * kD * 4 + (size_t)2 * LM * 64 * 16;
+    const size_t qsm = (size_t)2 * G * kD * 4 + (size_t)2 * LM * 64 * 16 + (size_t)kD * kQpRow * 4;
     hipLaunchKernelGGL(qprep_kernel, dim3(U), dim3(kD), qsm, st, K, q, G, LM, qa, qk);
     const int kct = (k->capacity + kTile - 1) / kTile, vct = (v->capacity + kTile - 1) / kTile;
     const dim3 grid(L.n_chunks, U);
