@@ -590,7 +590,7 @@ __host__ __device__ constexpr int k_mode(int r) {
     return r > 64 ? ((r & 15) ? 1 : 0) : ((r & 15) ? 3 : 2);
 }
 
-// Wave-uniform copies (a non-inlined function receives its arguments in vector registers).
+// Wave-uniform copies of values the compiler cannot prove uniform (kept in scalar registers).
 __device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
 __device__ __forceinline__ const uint8_t* uni(const uint8_t* p) {
     const uint64_t a = reinterpret_cast<uint64_t>(p);
@@ -598,8 +598,10 @@ __device__ __forceinline__ const uint8_t* uni(const uint8_t* p) {
     return reinterpret_cast<const uint8_t*>(((uint64_t)hi << 32) | lo);
 }
 
+// Inlined into the kernel: each instantiation is a disjoint branch of the dispatch, so registers
+// are allocated per branch, and no call frame saves registers to scratch memory on every item.
 template <int G, int BKc, int BVc, int KM>
-__device__ __noinline__ void run_item(const DevSide& K, const DevSide& V, const v4i* __restrict__ qa_ws,
+__device__ __attribute__((always_inline)) void run_item(const DevSide& K, const DevSide& V, const v4i* __restrict__ qa_ws,
                                          const float4* __restrict__ qk_ws, int k_cap_tiles, int v_cap_tiles, int u,
                                          int start, int end, float* __restrict__ out, int lane) {
     constexpr int LM = Shape<G>::LM;
