@@ -196,8 +196,8 @@ int kvc_encode(const kvc_stream_desc* s, const uint16_t* x, int64_t x_unit_strid
  * undo the rotation in one fused pass).
  *
  *  k, v         descriptors of the K and V sides; same n_units, unit u pairs.
- *  q            device fp16 [n_units][G][d]: the G query heads sharing unit
- *               u's KV head.
+ *  q            device fp16 [n_units][G][d], 16-byte aligned: the G query
+ *               heads sharing unit u's KV head (KVC_EINVAL if misaligned).
  *  seq_len      device int32 [n_units]: tokens attended per unit (each in
  *               [1, max_seq_len]).
  *  max_seq_len  host: upper bound of seq_len, <= both capacities.

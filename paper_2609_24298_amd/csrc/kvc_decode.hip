@@ -461,98 +461,110 @@ __device__ __forceinline__ void v_tile(uint32_t* vb, const __amdgpu_buffer_rsrc_
 // operand byte m <-> coordinate 16 (4 ks + grp) + pos_b(m) (zero outside the rank, for limb 3 and for
 // heads >= G). qk[u][h] = (sigma, sigma / 254, sigma / 254^2, bias) with
 // bias = -2^(b-1) sum_limb k_limb sum_i L_limb,i (0 for b = 8, whose codes are centred on load).
-constexpr int kQpRow = kD / 2 + 1;  // LDS words per staged basis row (fp16 pairs, padded: no bank conflicts)
-__global__ __launch_bounds__(kD) void qprep_kernel(DevSide K, const uint16_t* __restrict__ q, int G, int LM,
+typedef _Float16 qp_h8 __attribute__((ext_vector_type(8)));
+typedef float qp_f4 __attribute__((ext_vector_type(4)));
+
+// One wavefront per unit. The projection Y = P_K Q (rank rows x query-head columns) runs on
+// v_mfma_f32_16x16x32_f16 (exact fp16 products, fp32 accumulation): A = 16 basis rows x 32
+// coordinates, B = 32 coordinates x 16 heads, eight row blocks x four k-steps, every operand
+// loaded straight from global memory with all loads in flight. Lane (kq, col) then holds rows
+// 16 rb + 4 kq + v of head col; a head's max and limb sums reduce over its four lanes.
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void qprep_kernel(DevSide K, const uint16_t* __restrict__ q, int G, int LM,
                                                    v4i* __restrict__ qa, float4* __restrict__ qk) {
-    extern __shared__ float qsm[];
-    float* qsh = qsm;                                                        // [G][128]
-    uint8_t* img = reinterpret_cast<uint8_t*>(qsh + G * kD);                 // [2][LM][64][16] operand image
-    uint32_t* ps = reinterpret_cast<uint32_t*>(img + 2 * LM * 64 * 16);      // [r][kQpRow] basis rows
-    float* qts = reinterpret_cast<float*>(ps + kD * kQpRow);                 // [G][128] q~
-    __shared__ float fred[16][kD / 64];
-    __shared__ int ired[16][kLimbs][kD / 64];
-    const int u = blockIdx.x, i = threadIdx.x, lane = i & 63, wv = i >> 6;
+    extern __shared__ uint8_t img[];  // [2][LM][64][16] operand image
+    const int u = blockIdx.x, lane = threadIdx.x, col = lane & 15, kq = lane >> 4;
     const int r = K.r[u], b = K.b[u];
-    // stage q, clear the image, stage the basis rows (coalesced 16-byte loads, all in flight)
-    {
-        const uint4* __restrict__ P4 = reinterpret_cast<const uint4*>(K.basis + K.basis_off[u]);
-        const int n4 = r * kD / 8;
-        uint4 w[kD / 8];
+    const uint16_t* __restrict__ P = K.basis + K.basis_off[u];
+    const int img_words = 2 * LM * 64 * 4;
+    for (int k = lane; k < img_words; k += 64) reinterpret_cast<uint32_t*>(img)[k] = 0u;
+    qp_f4 C[8];
 #pragma unroll
-        for (int k = 0; k < kD / 8; ++k) w[k] = k * kD + i < n4 ? P4[k * kD + i] : uint4{0u, 0u, 0u, 0u};
-        for (int g = 0; g < G; ++g) qsh[g * kD + i] = h2f(q[((int64_t)u * G + g) * kD + i]);
-        const int img_words = 2 * LM * 64 * 4;
-        for (int k = i; k < img_words; k += kD) reinterpret_cast<uint32_t*>(img)[k] = 0u;
+    for (int rb = 0; rb < 8; ++rb) C[rb] = qp_f4{0.f, 0.f, 0.f, 0.f};
+    for (int h0 = 0; h0 < G; h0 += 16) {  // heads in groups of 16 columns
+        const int g = h0 + col;
+        qp_h8 B[4];
 #pragma unroll
-        for (int k = 0; k < kD / 8; ++k) {
-            const int c4 = k * kD + i;  // uint4 index: row c4 / 16, words 4 (c4 % 16) ..
-            if (c4 < n4) {
-                uint32_t* d = ps + (c4 >> 4) * kQpRow + 4 * (c4 & 15);
-                d[0] = w[k].x; d[1] = w[k].y; d[2] = w[k].z; d[3] = w[k].w;
+        for (int k4 = 0; k4 < 4; ++k4) {
+            const uint4 w = g < G ? reinterpret_cast<const uint4*>(q + ((int64_t)u * G + g) * kD + 32 * k4 + 8 * kq)[0]
+                                  : uint4{0u, 0u, 0u, 0u};
+            B[k4] = __builtin_bit_cast(qp_h8, w);
+        }
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {  // four row blocks' loads in flight at a time
+            uint4 A[4][4];
+#pragma unroll
+            for (int rq = 0; rq < 4; ++rq)
+#pragma unroll
+                for (int k4 = 0; k4 < 4; ++k4) {
+                    const int row = 16 * (4 * half + rq) + col;
+                    A[rq][k4] = row < r ? reinterpret_cast<const uint4*>(P + (int64_t)row * kD + 32 * k4 + 8 * kq)[0]
+                                        : uint4{0u, 0u, 0u, 0u};
+                }
+#pragma unroll
+            for (int rq = 0; rq < 4; ++rq) {
+                qp_f4 c = qp_f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int k4 = 0; k4 < 4; ++k4)
+                    c = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(qp_h8, A[rq][k4]), B[k4], c, 0, 0, 0);
+                C[4 * half + rq] = c;
             }
         }
-    }
-    __syncthreads();
-    const int hk = b == 8 ? 0 : (1 << (b - 1));
-    const float scale0 = K.delta[u] * 1.4426950408889634f * 0.08838834764831845f;  // log2(e) / sqrt(128)
-    // destination of coordinate i in the operand image
-    const int g16 = r >> 4;
-    const int cg = i < 16 * g16 ? (i >> 4) : g16;
-    const int jpos = i - 16 * cg;
-    const int ks = cg >> 2, grp = cg & 3;
-    int kidx = 0;
-    KVC_SWITCH_B(b, kidx = kidx_b(B_, jpos));
-    // q~_g,i for every head (thread i: basis row i), then every head's max |q~| in one round
-    for (int g = 0; g < G; ++g) {
-        float acc = 0.f;
-        if (i < r) {
-            const uint32_t* row = ps + i * kQpRow;
-#pragma unroll 8
-            for (int j = 0; j < kD / 2; ++j) {
-                const uint32_t pw = row[j];
-                acc = fmaf(h2f((uint16_t)(pw & 0xffffu)), qsh[g * kD + 2 * j], acc);
-                acc = fmaf(h2f((uint16_t)(pw >> 16)), qsh[g * kD + 2 * j + 1], acc);
+        const int hk = b == 8 ? 0 : (1 << (b - 1));
+        const float scale0 = K.delta[u] * 1.4426950408889634f * 0.08838834764831845f;  // log2(e) / sqrt(128)
+        float m = 0.f;
+#pragma unroll
+        for (int rb = 0; rb < 8; ++rb)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                C[rb][v] *= scale0;
+                m = fmaxf(m, fabsf(C[rb][v]));
             }
-        }
-        const float qt = acc * scale0;
-        qts[g * kD + i] = qt;
-        float m = fabsf(qt);
-        for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
-        if (lane == 0) fred[g][wv] = m;
-    }
-    __syncthreads();
-    for (int g = 0; g < G; ++g) {
-        const float amax = fmaxf(fred[g][0], fred[g][1]);
-        const float sigma = amax > 0.f ? amax / 127.f : 1.f;
-        const float x = qts[g * kD + i] / sigma;
-        const float l0 = fminf(fmaxf(rintf(x), -127.f), 127.f);
-        const float r1 = (x - l0) * 254.f;
-        const float l1 = fminf(fmaxf(rintf(r1), -127.f), 127.f);
-        const float r2 = (r1 - l1) * 254.f;
-        const float l2 = fminf(fmaxf(rintf(r2), -127.f), 127.f);
-        const int L[kLimbs] = {(int)l0, (int)l1, (int)l2};
+        m = fmaxf(m, __shfl_xor(m, 16));
+        m = fmaxf(m, __shfl_xor(m, 32));
+        const float sigma = m > 0.f ? m / 127.f : 1.f;
+        const int g16 = r >> 4;
+        int lsum[kLimbs] = {0, 0, 0};
+#pragma unroll
+        for (int rb = 0; rb < 8; ++rb)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int i = 16 * rb + 4 * kq + v;  // rank coordinate
+                if (i < r && g < G) {
+                    const float x = C[rb][v] / sigma;
+                    const float l0 = fminf(fmaxf(rintf(x), -127.f), 127.f);
+                    const float r1 = (x - l0) * 254.f;
+                    const float l1 = fminf(fmaxf(rintf(r1), -127.f), 127.f);
+                    const float r2 = (r1 - l1) * 254.f;
+                    const float l2 = fminf(fmaxf(rintf(r2), -127.f), 127.f);
+                    const int L[kLimbs] = {(int)l0, (int)l1, (int)l2};
+                    // destination of coordinate i in the operand image
+                    const int cg = i < 16 * g16 ? (i >> 4) : g16;
+                    const int jpos = i - 16 * cg;
+                    const int ks = cg >> 2, grp = cg & 3;
+                    const int kidx = kidx_b(b, jpos);
+#pragma unroll
+                    for (int k = 0; k < kLimbs; ++k) {
+                        img[(((ks * LM + (g >> 2)) * 64 + 16 * grp + 4 * (g & 3) + k) << 4) + kidx] = (uint8_t)(int8_t)L[k];
+                        lsum[k] += L[k];
+                    }
+                }
+            }
 #pragma unroll
         for (int k = 0; k < kLimbs; ++k) {
-            if (i < r) {
-                const int row_lane = 16 * grp + 4 * (g & 3) + k;
-                img[(((ks * LM + (g >> 2)) * 64 + row_lane) << 4) + kidx] = (uint8_t)(int8_t)L[k];
-            }
-            int sm = L[k];
-            for (int o = 32; o > 0; o >>= 1) sm += __shfl_xor(sm, o);
-            if (lane == 0) ired[g][k][wv] = sm;
+            lsum[k] += __shfl_xor(lsum[k], 16);
+            lsum[k] += __shfl_xor(lsum[k], 32);
+        }
+        if (kq == 0 && g < G) {
+            const float k0 = sigma, k1 = sigma * (1.f / 254.f), k2 = sigma * (1.f / 64516.f);
+            const float bias = -(float)hk * ((float)lsum[0] * k0 + (float)lsum[1] * k1 + (float)lsum[2] * k2);
+            qk[(int64_t)u * G + g] = float4{k0, k1, k2, bias};
         }
     }
-    __syncthreads();
-    if (i < G) {
-        const int g = i;
-        const float sigma = fmaxf(fred[g][0], fred[g][1]) > 0.f ? fmaxf(fred[g][0], fred[g][1]) / 127.f : 1.f;
-        const float k0 = sigma, k1 = sigma * (1.f / 254.f), k2 = sigma * (1.f / 64516.f);
-        const float bias = -(float)hk * ((float)(ired[g][0][0] + ired[g][0][1]) * k0 + (float)(ired[g][1][0] + ired[g][1][1]) * k1 +
-                                         (float)(ired[g][2][0] + ired[g][2][1]) * k2);
-        qk[(int64_t)u * G + g] = float4{k0, k1, k2, bias};
-    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
     v4i* dst = qa + (int64_t)u * 2 * LM * 64;
-    for (int k = i; k < 2 * LM * 64; k += kD) dst[k] = reinterpret_cast<const v4i*>(img)[k];
+    for (int k = lane; k < 2 * LM * 64; k += 64) dst[k] = reinterpret_cast<const v4i*>(img)[k];
 }
 
 // ---------------------------------------------------------------- partials
@@ -1126,6 +1138,7 @@ extern "C" int kvc_decode_attn(const kvc_stream_desc* k, const kvc_stream_desc* 
     if (int e = decode_check(k, v, G, max_seq_len)) return e;
     if (k->n_units == 0) return KVC_OK;
     if (!q || !seq_len || !out || !ws) return set_error(KVC_EINVAL, "kvc_decode_attn: null pointer");
+    if (reinterpret_cast<uintptr_t>(q) & 15) return set_error(KVC_EINVAL, "kvc_decode_attn: q not 16-byte aligned");
     if (reinterpret_cast<uintptr_t>(ws) & 255) return set_error(KVC_EINVAL, "kvc_decode_attn: workspace not 256-byte aligned");
     const int U = k->n_units;
     const WsLayout L = ws_layout(k, G, max_seq_len);
@@ -1138,8 +1151,8 @@ extern "C" int kvc_decode_attn(const kvc_stream_desc* k, const kvc_stream_desc* 
     hipStream_t st = (hipStream_t)stream;
     const DevSide K = dev_side(k), V = dev_side(v);
     const int LM = (G + 3) / 4;
-    const size_t qsm = (size_t)2 * G * kD * 4 + (size_t)2 * LM * 64 * 16 + (size_t)kD * kQpRow * 4;
-    hipLaunchKernelGGL(qprep_kernel, dim3(U), dim3(kD), qsm, st, K, q, G, LM, qa, qk);
+    const size_t qsm = (size_t)2 * LM * 64 * 16;
+    hipLaunchKernelGGL(qprep_kernel, dim3(U), dim3(64), qsm, st, K, q, G, LM, qa, qk);
     const int kct = (k->capacity + kTile - 1) / kTile, vct = (v->capacity + kTile - 1) / kTile;
     const dim3 grid(L.n_chunks, U);
     int e = KVC_OK;

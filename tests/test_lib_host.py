@@ -211,3 +211,21 @@ def test_descriptor_validation_ranges_without_gpu():
     dl[0] = 0.5
     assert L.kvc_reconstruct(ctypes.byref(desc()), 0, 65, fake, None) == kvc.KVC_ENOSPACE
     assert L.kvc_reconstruct(ctypes.byref(desc()), -1, 1, fake, None) == kvc.KVC_EINVAL
+
+
+def test_decode_rejects_misaligned_query_without_gpu():
+    # q is read as 16-byte operand fragments; a misaligned pointer is refused before any launch
+    L = kvc.lib()
+    r = np.array([4], dtype=np.int32)
+    b = np.array([3], dtype=np.int32)
+    off = np.array([0], dtype=np.int64)
+    boff = np.array([0], dtype=np.int64)
+    dl = np.array([0.5], dtype=np.float32)
+    fake = ctypes.c_void_p(256)          # never dereferenced
+    dk, dv = (kvc.StreamDesc(n_units=1, d=128, capacity=64, side=side, r_host=r.ctypes.data, b_host=b.ctypes.data,
+                             code_off_host=off.ctypes.data, basis_off_host=boff.ctypes.data,
+                             delta_host=dl.ctypes.data, r=fake, b=fake, code_off=fake, basis_off=fake, delta=fake,
+                             codes=fake, codes_bytes=8 * 4 * 3, basis=fake, basis_elems=4 * 128) for side in (0, 1))
+    rc = L.kvc_decode_attn(ctypes.byref(dk), ctypes.byref(dv), ctypes.c_void_p(258), 4, fake, 1, fake, fake, 1 << 20, None)
+    assert rc == kvc.KVC_EINVAL
+    assert b"16-byte" in L.kvc_last_error()
