@@ -928,22 +928,17 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(Shape<G>::W,
 // the merge and output columns 2 l, 2 l + 1. The chunks' partials merge in the log2 domain
 // (M = max m_c, L = sum l_c 2^(m_c - M), A_j = sum acc_c,j 2^(m_c - M)), z_j = step_V (A_j / L + 1/2)
 // is the dequantised rank-space average, and o = P_V^T z (the V reconstruction of Lemma
-// lem:head-dist applied after the softmax average, which is linear). The block stages P_V in LDS
-// with coalesced loads while its wavefronts merge; chunk loads are issued in batches.
+// lem:head-dist applied after the softmax average, which is linear). Chunk and basis loads are
+// issued in batches.
 constexpr int kMaxG = 16;
 constexpr int kCombBatch = 8;  // chunks whose loads are in flight together
+constexpr int kCombRows = 16;  // basis rows whose loads are in flight together
 __global__ __launch_bounds__(64 * kMaxG) void combine_kernel(DevSide V, int G, int n_chunks, const float* __restrict__ part,
                                                              float* __restrict__ out) {
     __shared__ float zs[kMaxG][kD];
-    __shared__ uint32_t ps[kD * kD / 2];  // P_V rows as fp16 pairs
-    const int u = blockIdx.x, g = threadIdx.x >> 6, lane = threadIdx.x & 63, nth = 64 * G;
+    const int u = blockIdx.x, g = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int rv = V.r[u];
     const float step = V.delta[u];
-    {
-        const uint4* __restrict__ P4 = reinterpret_cast<const uint4*>(V.basis + V.basis_off[u]);
-        const int n4 = rv * kD / 8;
-        for (int k = threadIdx.x; k < n4; k += nth) reinterpret_cast<uint4*>(ps)[k] = P4[k];
-    }
     const float* __restrict__ pg = part + (int64_t)u * n_chunks * G * kPartStride + g * kPartStride;
     const int64_t cs = (int64_t)G * kPartStride;
     // M and L: lane c < n_chunks reads chunk c's (m, l) (in rounds of 64 chunks)
@@ -977,12 +972,20 @@ __global__ __launch_bounds__(64 * kMaxG) void combine_kernel(DevSide V, int G, i
     zs[g][lane] = (L > 0.f && lane < rv) ? step * fmaf(A0, inv, 0.5f) : 0.f;
     zs[g][lane + 64] = (L > 0.f && lane + 64 < rv) ? step * fmaf(A1, inv, 0.5f) : 0.f;
     __syncthreads();
+    // o = P_V^T z: lane l takes output columns 2 l, 2 l + 1; basis rows read 16 at a time (the
+    // block's wavefronts read the same rows, served by the cache after the first)
+    const uint32_t* __restrict__ P32 = reinterpret_cast<const uint32_t*>(V.basis + V.basis_off[u]);
     float o0 = 0.f, o1 = 0.f;
-    for (int i = 0; i < rv; ++i) {
-        const float z = zs[g][i];
-        const uint32_t pw = ps[i * (kD / 2) + lane];
-        o0 = fmaf(h2f((uint16_t)(pw & 0xffffu)), z, o0);
-        o1 = fmaf(h2f((uint16_t)(pw >> 16)), z, o1);
+    for (int i0 = 0; i0 < rv; i0 += kCombRows) {
+        uint32_t pw[kCombRows];
+#pragma unroll
+        for (int k = 0; k < kCombRows; ++k) pw[k] = i0 + k < rv ? P32[(i0 + k) * (kD / 2) + lane] : 0u;
+#pragma unroll
+        for (int k = 0; k < kCombRows; ++k) {
+            const float z = zs[g][(i0 + k) & (kD - 1)];  // zero past the rank
+            o0 = fmaf(h2f((uint16_t)(pw[k] & 0xffffu)), z, o0);
+            o1 = fmaf(h2f((uint16_t)(pw[k] >> 16)), z, o1);
+        }
     }
     reinterpret_cast<float2*>(out + ((int64_t)u * G + g) * kD)[lane] = float2{o0, o1};
 }
