@@ -172,6 +172,31 @@ class Side:
         return self.codes[off: off + self.stream_bytes(u, n_tok)]
 
 
+class SideRange:
+    """Units [u0, u0 + n) of a Side as a descriptor of their own: the per-unit tables are offset into
+    the parent's, the code and basis arenas are shared (a layer of a cache, for per-layer calls)."""
+
+    def __init__(self, parent: Side, u0: int, n: int):
+        assert 0 <= u0 and n >= 0 and u0 + n <= parent.n_units
+        self.parent = parent
+        self.side, self.capacity, self.n_units = parent.side, parent.capacity, n
+        self.r_h, self.b_h = parent.r_h[u0:u0 + n], parent.b_h[u0:u0 + n]
+        self.delta_h, self.basis_off_h = parent.delta_h[u0:u0 + n], parent.basis_off_h[u0:u0 + n]
+        self.code_off_h = parent.code_off_h[u0:u0 + n]
+        self.codes, self.basis = parent.codes, parent.basis
+        d = parent.desc
+        self.desc = StreamDesc(
+            n_units=n, d=d.d, capacity=d.capacity, side=d.side,
+            r_host=_np_ptr(self.r_h), b_host=_np_ptr(self.b_h), code_off_host=_np_ptr(self.code_off_h),
+            basis_off_host=_np_ptr(self.basis_off_h), delta_host=_np_ptr(self.delta_h),
+            r=d.r + 4 * u0, b=d.b + 4 * u0, code_off=d.code_off + 8 * u0, basis_off=d.basis_off + 8 * u0,
+            delta=d.delta + 4 * u0, codes=d.codes, codes_bytes=d.codes_bytes, basis=d.basis,
+            basis_elems=d.basis_elems)
+
+    def stream_bytes(self, u: int, n_tok: int) -> int:
+        return ((n_tok + TILE - 1) // TILE) * 8 * int(self.r_h[u]) * int(self.b_h[u])
+
+
 def _stream_ptr(stream):
     import torch
     if stream is None:

@@ -106,6 +106,12 @@ class Cache:
     def decode(self, q, seq_len, max_seq_len: int, out, ws, stream=None):
         kvc.kvc_decode_attn(self.K, self.V, q, self.w.group, seq_len, max_seq_len, out, ws, stream)
 
+    def layer_sides(self, layer: int):
+        """Descriptors of one layer's units (u = (layer * batch + sequence) * kv_heads + head is
+        layer-major, so they are one contiguous range) for per-layer calls."""
+        upl = self.w.batch * self.w.kv_heads
+        return kvc.SideRange(self.K, layer * upl, upl), kvc.SideRange(self.V, layer * upl, upl)
+
     def code_bytes(self, n_tok: int) -> int:
         """Algorithmic bytes of the K and V code streams holding n_tok tokens per unit."""
         return int(sum(self.K.stream_bytes(u, n_tok) + self.V.stream_bytes(u, n_tok) for u in range(self.w.n_units)))
