@@ -924,70 +924,125 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(Shape<G>::W,
 
 // ---------------------------------------------------------------- combine
 
-// One block per unit, one wavefront per query head; lane l handles rank coordinates l and l + 64 of
-// the merge and output columns 2 l, 2 l + 1. The chunks' partials merge in the log2 domain
-// (M = max m_c, L = sum l_c 2^(m_c - M), A_j = sum acc_c,j 2^(m_c - M)), z_j = step_V (A_j / L + 1/2)
-// is the dequantised rank-space average, and o = P_V^T z (the V reconstruction of Lemma
-// lem:head-dist applied after the softmax average, which is linear). Chunk and basis loads are
-// issued in batches.
-constexpr int kMaxG = 16;
-constexpr int kCombBatch = 8;  // chunks whose loads are in flight together
-constexpr int kCombRows = 16;  // basis rows whose loads are in flight together
-__global__ __launch_bounds__(64 * kMaxG) void combine_kernel(DevSide V, int G, int n_chunks, const float* __restrict__ part,
-                                                             float* __restrict__ out) {
-    __shared__ float zs[kMaxG][kD];
-    const int u = blockIdx.x, g = threadIdx.x >> 6, lane = threadIdx.x & 63;
+// One block of Wc wavefronts per unit (Wc = blockDim.x / 64: one for a few chunks, more when the
+// context is split into many). Lane l handles rank coordinates l and l + 64 of the merge and output
+// columns 2 l, 2 l + 1, for all G query heads. The chunks' partials merge in the log2 domain
+// (M = max m_c, L = sum l_c 2^(m_c - M), A_j = sum acc_c,j 2^(m_c - M)): wavefront w merges chunks
+// w, w + Wc, ... (a batch of chunks in flight at once, the running sums rescaled when a batch raises
+// M), the wavefronts' merges meet in LDS, and z_j = step_V (A_j / L + 1/2) is the dequantised
+// rank-space average. Then o = P_V^T z (the V reconstruction of Lemma lem:head-dist applied after the
+// softmax average, which is linear), computed by the first wavefront, which loads its two columns
+// of every basis row at the start.
+constexpr int kCombMaxRed = 32;  // Wc x G at most (LDS of the cross-wavefront merge)
+template <int G>
+__global__ __launch_bounds__(64 * (kCombMaxRed / G < 8 ? kCombMaxRed / G : 8)) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void combine_kernel(DevSide V, int n_chunks, const float* __restrict__ part, float* __restrict__ out) {
+    constexpr int kCombBatch = 16 / G > 0 ? 16 / G : 1;  // chunks whose partials are in flight together (per wavefront)
+    __shared__ float zs[G][kD];
+    extern __shared__ float comb_dsm[];  // [Wc * G][kPartStride] per (wavefront, head): M, L, -, -, A[128]
+    const int u = blockIdx.x, lane = threadIdx.x & 63, wv = threadIdx.x >> 6, Wc = blockDim.x >> 6;
+    float(*red)[kPartStride] = reinterpret_cast<float(*)[kPartStride]>(comb_dsm);
     const int rv = V.r[u];
     const float step = V.delta[u];
-    const float* __restrict__ pg = part + (int64_t)u * n_chunks * G * kPartStride + g * kPartStride;
-    const int64_t cs = (int64_t)G * kPartStride;
-    // M and L: lane c < n_chunks reads chunk c's (m, l) (in rounds of 64 chunks)
-    float M = -INFINITY;
-    for (int c0 = 0; c0 < n_chunks; c0 += 64)
-        if (c0 + lane < n_chunks) M = fmaxf(M, pg[(c0 + lane) * cs]);
-    for (int o = 32; o > 0; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
-    float L = 0.f, A0 = 0.f, A1 = 0.f;
-    for (int c0 = 0; c0 < n_chunks; c0 += kCombBatch) {
-        float mc[kCombBatch], lc[kCombBatch], a0[kCombBatch], a1[kCombBatch];
+    // the lane's two columns of every basis row, in flight while the chunks merge
+    const uint32_t* __restrict__ P32 = reinterpret_cast<const uint32_t*>(V.basis + V.basis_off[u]);
+    uint32_t pw[kD];
+#pragma unroll
+    for (int i = 0; i < kD; ++i) pw[i] = (wv == 0 && i < rv) ? P32[i * (kD / 2) + lane] : 0u;
+    const float* __restrict__ pu = part + (int64_t)u * n_chunks * G * kPartStride;
+    float M[G], L[G], A0[G], A1[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) { M[g] = -INFINITY; L[g] = A0[g] = A1[g] = 0.f; }
+    for (int c0 = wv; c0 < n_chunks; c0 += kCombBatch * Wc) {
+        float mc[kCombBatch][G], lc[kCombBatch][G], a0[kCombBatch][G], a1[kCombBatch][G];
 #pragma unroll
         for (int k = 0; k < kCombBatch; ++k) {
-            const int c = min(c0 + k, n_chunks - 1);
-            const float* pc = pg + c * cs;
-            mc[k] = pc[0];
-            lc[k] = c0 + k < n_chunks ? pc[1] : 0.f;
-            a0[k] = pc[4 + lane];
-            a1[k] = pc[4 + 64 + lane];
+            const int ck = c0 + k * Wc;
+            const int c = min(ck, n_chunks - 1);
+#pragma unroll
+            for (int g = 0; g < G; ++g) {
+                const float* pc = pu + ((int64_t)c * G + g) * kPartStride;
+                mc[k][g] = pc[0];
+                lc[k][g] = ck < n_chunks ? pc[1] : 0.f;
+                a0[k][g] = pc[4 + lane];
+                a1[k][g] = pc[4 + 64 + lane];
+            }
         }
 #pragma unroll
-        for (int k = 0; k < kCombBatch; ++k) {
-            if (lc[k] > 0.f) {  // an empty chunk (or a batch slot past the last) has l = 0 and no accumulator
-                const float w = exp2f(mc[k] - M);
-                L = fmaf(lc[k], w, L);
-                A0 = fmaf(a0[k], w, A0);
-                A1 = fmaf(a1[k], w, A1);
+        for (int g = 0; g < G; ++g) {
+            float mb = M[g];
+#pragma unroll
+            for (int k = 0; k < kCombBatch; ++k)
+                if (lc[k][g] > 0.f) mb = fmaxf(mb, mc[k][g]);
+            if (mb > M[g]) {  // M[g] = -inf before the first non-empty chunk: the sums are still zero
+                const float sc = M[g] == -INFINITY ? 0.f : exp2f(M[g] - mb);
+                L[g] *= sc; A0[g] *= sc; A1[g] *= sc;
+                M[g] = mb;
+            }
+#pragma unroll
+            for (int k = 0; k < kCombBatch; ++k) {
+                if (lc[k][g] > 0.f) {  // an empty chunk (or a batch slot past the last) has l = 0 and no accumulator
+                    const float w = exp2f(mc[k][g] - M[g]);
+                    L[g] = fmaf(lc[k][g], w, L[g]);
+                    A0[g] = fmaf(a0[k][g], w, A0[g]);
+                    A1[g] = fmaf(a1[k][g], w, A1[g]);
+                }
             }
         }
     }
-    const float inv = L > 0.f ? 1.f / L : 0.f;
-    zs[g][lane] = (L > 0.f && lane < rv) ? step * fmaf(A0, inv, 0.5f) : 0.f;
-    zs[g][lane + 64] = (L > 0.f && lane + 64 < rv) ? step * fmaf(A1, inv, 0.5f) : 0.f;
-    __syncthreads();
-    // o = P_V^T z: lane l takes output columns 2 l, 2 l + 1; basis rows read 16 at a time (the
-    // block's wavefronts read the same rows, served by the cache after the first)
-    const uint32_t* __restrict__ P32 = reinterpret_cast<const uint32_t*>(V.basis + V.basis_off[u]);
-    float o0 = 0.f, o1 = 0.f;
-    for (int i0 = 0; i0 < rv; i0 += kCombRows) {
-        uint32_t pw[kCombRows];
 #pragma unroll
-        for (int k = 0; k < kCombRows; ++k) pw[k] = i0 + k < rv ? P32[(i0 + k) * (kD / 2) + lane] : 0u;
-#pragma unroll
-        for (int k = 0; k < kCombRows; ++k) {
-            const float z = zs[g][(i0 + k) & (kD - 1)];  // zero past the rank
-            o0 = fmaf(h2f((uint16_t)(pw[k] & 0xffffu)), z, o0);
-            o1 = fmaf(h2f((uint16_t)(pw[k] >> 16)), z, o1);
-        }
+    for (int g = 0; g < G; ++g) {
+        float* rd = red[wv * G + g];
+        if (lane == 0) { rd[0] = M[g]; rd[1] = L[g]; }
+        rd[4 + lane] = A0[g];
+        rd[4 + 64 + lane] = A1[g];
     }
-    reinterpret_cast<float2*>(out + ((int64_t)u * G + g) * kD)[lane] = float2{o0, o1};
+    __syncthreads();
+    for (int g = wv; g < G; g += Wc) {  // the wavefronts' merges of head g, then z
+        float Mg = -INFINITY;
+        for (int w = 0; w < Wc; ++w)
+            if (red[w * G + g][1] > 0.f) Mg = fmaxf(Mg, red[w * G + g][0]);
+        float Lg = 0.f, B0 = 0.f, B1 = 0.f;
+        for (int w = 0; w < Wc; ++w) {
+            const float* rd = red[w * G + g];
+            if (rd[1] > 0.f) {
+                const float sc = exp2f(rd[0] - Mg);
+                Lg = fmaf(rd[1], sc, Lg);
+                B0 = fmaf(rd[4 + lane], sc, B0);
+                B1 = fmaf(rd[4 + 64 + lane], sc, B1);
+            }
+        }
+        const float inv = Lg > 0.f ? 1.f / Lg : 0.f;
+        zs[g][lane] = (Lg > 0.f && lane < rv) ? step * fmaf(B0, inv, 0.5f) : 0.f;
+        zs[g][lane + 64] = (Lg > 0.f && lane + 64 < rv) ? step * fmaf(B1, inv, 0.5f) : 0.f;
+    }
+    __syncthreads();
+    if (wv == 0) {
+        float o0[G], o1[G];
+#pragma unroll
+        for (int g = 0; g < G; ++g) o0[g] = o1[g] = 0.f;
+#pragma unroll
+        for (int i = 0; i < kD; ++i) {
+            const float p0 = h2f((uint16_t)(pw[i] & 0xffffu)), p1 = h2f((uint16_t)(pw[i] >> 16));
+#pragma unroll
+            for (int g = 0; g < G; ++g) {
+                const float z = zs[g][i];  // zero past the rank
+                o0[g] = fmaf(p0, z, o0[g]);
+                o1[g] = fmaf(p1, z, o1[g]);
+            }
+        }
+#pragma unroll
+        for (int g = 0; g < G; ++g)
+            reinterpret_cast<float2*>(out + ((int64_t)u * G + g) * kD)[lane] = float2{o0[g], o1[g]};
+    }
+}
+
+// Wavefronts of a combine block: enough that each merges about 8 chunks, within the LDS of the
+// cross-wavefront merge, at most one per query head, and few enough that every block is resident
+// at once (the kernel's register budget leaves two wavefronts per SIMD, eight per CU).
+inline int combine_waves(int G, int n_chunks, int U, int ncu) {
+    const int cap = std::min(std::min(std::max(kCombMaxRed / G, 1), std::min(G, 8)), std::max(1, 8 * ncu / std::max(U, 1)));
+    return std::max(1, std::min(cap, (n_chunks + 7) / 8));
 }
 
 // ---------------------------------------------------------------- host side
@@ -1018,15 +1073,20 @@ int resident_blocks(size_t smem) {
     return nb;
 }
 
-// Work items (wavefronts) the device holds at once for this launch; without a device, the
-// MI355X figures (256 CUs, 16 resident wavefronts each).
-int64_t resident_slots(int G, size_t smem) {
+// Compute units of the current device (256, the MI355X figure, without a device).
+int device_cus() {
     int dev = 0, ncu = 0;
     if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
         ncu <= 0) {
         (void)hipGetLastError();
         ncu = 256;
     }
+    return ncu;
+}
+
+// Work items (wavefronts) the device holds at once for this launch.
+int64_t resident_slots(int G, size_t smem) {
+    const int ncu = device_cus();
     int nb;
     switch (G) {
         case 1: nb = resident_blocks<1>(smem); break;
@@ -1167,6 +1227,15 @@ extern "C" int kvc_decode_attn(const kvc_stream_desc* k, const kvc_stream_desc* 
         default: e = launch_partials<16>(grid, st, K, V, qa, qk, seq_len, max_seq_len, L.chunk, L.n_chunks, kct, vct, part, L.stage_bytes); break;
     }
     if (e) return e;
-    hipLaunchKernelGGL(combine_kernel, dim3(U), dim3(64 * G), 0, st, V, G, L.n_chunks, part, out);
+    const int cw = combine_waves(G, L.n_chunks, U, device_cus());
+    const dim3 cblk(64 * cw);
+    const size_t csm = (size_t)cw * G * kPartStride * 4;
+    switch (G) {
+        case 1: hipLaunchKernelGGL(combine_kernel<1>, dim3(U), cblk, csm, st, V, L.n_chunks, part, out); break;
+        case 2: hipLaunchKernelGGL(combine_kernel<2>, dim3(U), cblk, csm, st, V, L.n_chunks, part, out); break;
+        case 4: hipLaunchKernelGGL(combine_kernel<4>, dim3(U), cblk, csm, st, V, L.n_chunks, part, out); break;
+        case 8: hipLaunchKernelGGL(combine_kernel<8>, dim3(U), cblk, csm, st, V, L.n_chunks, part, out); break;
+        default: hipLaunchKernelGGL(combine_kernel<16>, dim3(U), cblk, csm, st, V, L.n_chunks, part, out); break;
+    }
     return check_launch("kvc_decode_attn");
 }
