@@ -156,7 +156,8 @@ __host__ __device__ constexpr int v_words(int b) {
     return b == 8 ? 4 : ((b & 4 ? 2 : 0) + (b & 2 ? 1 : 0) + (b & 1 ? 1 : 0));
 }
 constexpr int kVBufWords = 16;  // value prefetch registers
-constexpr int kPrefetchDepth = 2;  // tiles of K and V loads in flight ahead of the one being processed
+constexpr int kPrefetchDepth = 2;  // tiles of K and V loads in flight ahead of the one being processed (the
+                                    // general path keeps one: its per-tile width switches need the registers)
 __host__ __device__ constexpr int v_prefetch_tiles(int b) { return kVBufWords / v_words(b) < 8 ? kVBufWords / v_words(b) : 8; }
 
 // Direct loads of one K-step's fields into w[0 .. 2B).
@@ -617,6 +618,7 @@ __device__ __attribute__((always_inline)) void run_item(const DevSide& K, const 
                                          const float4* __restrict__ qk_ws, int k_cap_tiles, int v_cap_tiles, int u,
                                          int start, int end, float* __restrict__ out, int lane) {
     constexpr int LM = Shape<G>::LM;
+    constexpr int kDepth = KM >= 0 ? kPrefetchDepth : 1;
     uint8_t* pmat = kvc_dsm;                            // [16 LM][kPRowBytes] probability limbs
     uint8_t* stage = kvc_dsm + 16 * LM * kPRowBytes;    // staged tail K-step
     const int col = lane & 15, grp = lane >> 4;
@@ -704,7 +706,7 @@ __device__ __attribute__((always_inline)) void run_item(const DevSide& K, const 
         __builtin_amdgcn_sched_barrier(0);
         KVC_SW_V(v_prefetch<B_>(vbA, vrs, rv, LV, nv));
         __builtin_amdgcn_sched_barrier(0);
-        if constexpr (kPrefetchDepth == 2) {
+        if constexpr (kDepth == 2) {
             const auto krs1 = k_rs(tile0 + 1), vrs1 = v_rs(tile0 + 1);
             KVC_SW_K(k_prefetch<B_>(kbB, krs1, rk, nk, ks_t, LK, lane));
             __builtin_amdgcn_sched_barrier(0);
@@ -718,7 +720,7 @@ __device__ __attribute__((always_inline)) void run_item(const DevSide& K, const 
         const int tok0 = tile * kTile;
         const bool first = tile == tile0;
         const auto krs = k_rs(tile), vrs = v_rs(tile);
-        const auto krs_n = k_rs(tile + kPrefetchDepth), vrs_n = v_rs(tile + kPrefetchDepth);
+        const auto krs_n = k_rs(tile + kDepth), vrs_n = v_rs(tile + kDepth);
         // Opaque per-tile copies of the lane and rank constants: the offsets every bit width derives
         // from them are recomputed inside the loop instead of being hoisted and kept live across it
         // for all eight widths at once.
@@ -830,7 +832,7 @@ __device__ __attribute__((always_inline)) void run_item(const DevSide& K, const 
         for (int pm = 0; pm < LM; ++pm) C[pm][8] = mfma_i8(ap[pm], ones, C[pm][8]);
         wave_lds_sync();  // pmat is rewritten by the next tile
     };
-    if constexpr (kPrefetchDepth == 2) {
+    if constexpr (kDepth == 2) {
         // pairs of tiles in a straight-line body (the load-wait counts stay exact across the back edge)
         // The staged (tail) K-step of tile t + 1 goes to LDS at the end of tile t's logits (the first
         // tile's before the loop); the general path stages each tile itself.
