@@ -187,6 +187,8 @@ def main():
     ap.add_argument("--workload", default="llama8b_b8_t32k_2bpd")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-per-layer", action="store_true",
+                    help="skip the per-layer loop (profiling runs that summarise the all-layers call)")
     ap.add_argument("--copy-calib", action="store_true",
                     help="after the timed region, run one plain 1 GiB device-to-device copy (the reference kernel "
                          "for scaling HBM byte counters)")
@@ -264,7 +266,7 @@ def main():
     t_dec = float(np.mean([a.elapsed_time(b) for a, b in evs])) / 1e3
     assert torch.isfinite(out).all().item()
 
-    per_layer = per_layer_loop(cache, w, q, seq, n_att, args.steps)
+    per_layer = None if args.no_per_layer else per_layer_loop(cache, w, q, seq, n_att, args.steps)
 
     dec_bytes = decode_alg_bytes(cache, n_att)
     # append: read the new token's fp16 K and V, write r*b bits per unit and side
