@@ -418,28 +418,28 @@ __device__ __forceinline__ v4i v_frag(const uint32_t* w) {
     return unpack16<B>(f, false);
 }
 
-template <int B>
+template <int B, int NV>
 __device__ __forceinline__ void v_prefetch(uint32_t (&vb)[kVBufWords], const __amdgpu_buffer_rsrc_t rs, int r,
                                            uint32_t lv, int nv) {
-    constexpr int VW = v_words(B);
+    constexpr int VW = v_words(B), NPF = v_prefetch_tiles(B) < NV ? v_prefetch_tiles(B) : NV;
     (void)nv;
 #pragma unroll
-    for (int nt = 0; nt < v_prefetch_tiles(B); ++nt) v_load<B>(rs, r, lv, nt, vb + nt * VW);
+    for (int nt = 0; nt < NPF; ++nt) v_load<B>(rs, r, lv, nt, vb + nt * VW);
 }
 
-// PV MFMAs of one tile (N-tiles nt < nv; the first v_prefetch_tiles come from the prefetched
-// words, the rest are loaded here), then the next tile's prefetch (rs_next; a zero-sized
-// descriptor when there is none).
-template <int B, int LM>
+// PV MFMAs of one tile (N-tiles nt < NV, a compile-time bound on the rank's N-tiles; the first
+// v_prefetch_tiles come from the prefetched words, the rest are loaded here), then the next tile's
+// prefetch (rs_next; a zero-sized descriptor when there is none).
+template <int B, int LM, int NV>
 __device__ __forceinline__ void v_tile(uint32_t* vb, const __amdgpu_buffer_rsrc_t rs, const __amdgpu_buffer_rsrc_t rs_next,
                                        int r, uint32_t lv, int nv, const v4i (&ap)[LM], v4i (&C)[LM][9]) {
-    constexpr int VW = v_words(B), NPF = v_prefetch_tiles(B);
-    // Every N-tile is processed, also those past the rank (their loads read beyond the plane, bounded
-    // by the stream, into accumulator columns that are never output): no branches, and every tile
-    // issues the same loads in the same order, so the waits for a tile's data stay exact.
+    constexpr int VW = v_words(B), NPF = v_prefetch_tiles(B) < NV ? v_prefetch_tiles(B) : NV;
+    // Every N-tile below NV is processed, also those past the rank (their loads read beyond the plane,
+    // bounded by the stream, into accumulator columns that are never output): no branches, and every
+    // tile issues the same loads in the same order, so the waits for a tile's data stay exact.
     (void)nv;
 #pragma unroll
-    for (int nt = 0; nt < 8; ++nt) {
+    for (int nt = 0; nt < NV; ++nt) {
         uint32_t w[4];
         if (nt < NPF) {
 #pragma unroll
@@ -613,7 +613,7 @@ __device__ __forceinline__ const uint8_t* uni(const uint8_t* p) {
 
 // Inlined into the kernel: each instantiation is a disjoint branch of the dispatch, so registers
 // are allocated per branch, and no call frame saves registers to scratch memory on every item.
-template <int G, int BKc, int BVc, int KM>
+template <int G, int BKc, int BVc, int KM, int NVc>
 __device__ __attribute__((always_inline)) void run_item(const DevSide& K, const DevSide& V, const v4i* __restrict__ qa_ws,
                                          const float4* __restrict__ qk_ws, int k_cap_tiles, int v_cap_tiles, int u,
                                          int start, int end, float* __restrict__ out, int lane) {
@@ -704,13 +704,13 @@ __device__ __attribute__((always_inline)) void run_item(const DevSide& K, const 
         const auto krs = k_rs(tile0), vrs = v_rs(tile0);
         KVC_SW_K(k_prefetch<B_>(kbA, krs, rk, nk, ks_t, LK, lane));
         __builtin_amdgcn_sched_barrier(0);
-        KVC_SW_V(v_prefetch<B_>(vbA, vrs, rv, LV, nv));
+        KVC_SW_V((v_prefetch<B_, NVc>(vbA, vrs, rv, LV, nv)));
         __builtin_amdgcn_sched_barrier(0);
         if constexpr (kDepth == 2) {
             const auto krs1 = k_rs(tile0 + 1), vrs1 = v_rs(tile0 + 1);
             KVC_SW_K(k_prefetch<B_>(kbB, krs1, rk, nk, ks_t, LK, lane));
             __builtin_amdgcn_sched_barrier(0);
-            KVC_SW_V(v_prefetch<B_>(vbB, vrs1, rv, LV, nv));
+            KVC_SW_V((v_prefetch<B_, NVc>(vbB, vrs1, rv, LV, nv)));
             __builtin_amdgcn_sched_barrier(0);
         }
     }
@@ -827,7 +827,7 @@ __device__ __attribute__((always_inline)) void run_item(const DevSide& K, const 
             ap[pm] = *reinterpret_cast<const v4i*>(pmat + (16 * pm + col) * kPRowBytes + 16 * grp);
 
         // ---- PV (value N-tiles, then the all-ones column)
-        KVC_SW_V((v_tile<B_, LM>(vb, vrs, vrs_n, rvt, LVt, nvt, ap, C)));
+        KVC_SW_V((v_tile<B_, LM, NVc>(vb, vrs, vrs_n, rvt, LVt, nvt, ap, C)));
 #pragma unroll
         for (int pm = 0; pm < LM; ++pm) C[pm][8] = mfma_i8(ap[pm], ones, C[pm][8]);
         wave_lds_sync();  // pmat is rewritten by the next tile
@@ -905,23 +905,27 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(Shape<G>::W,
     // path switches on the widths per tile.
     if constexpr (G == 4 || G == 8) {
         if (bk <= 4 && bv <= 4) {
-            switch (((bk - 1) * 4 + (bv - 1)) * 4 + k_mode(K.r[u])) {
-#define KVC_ITEM(BK, BV, KM)                                                                                      \
-    case ((BK - 1) * 4 + (BV - 1)) * 4 + KM:                                                                    \
-        run_item<G, BK, BV, KM>(K, V, qa_ws, qk_ws, k_cap_tiles, v_cap_tiles, u, start, end, out, lane);        \
+            // 3-bit values at rank <= 96 (six N-tiles) have their own instantiations
+            const int vm = bv == 3 && V.r[u] <= 96 ? 1 : 0;
+            switch ((((bk - 1) * 4 + (bv - 1)) * 4 + k_mode(K.r[u])) * 2 + vm) {
+#define KVC_ITEM(BK, BV, KM, NV)                                                                                  \
+    case (((BK - 1) * 4 + (BV - 1)) * 4 + KM) * 2 + (NV == 6):                                                  \
+        run_item<G, BK, BV, KM, NV>(K, V, qa_ws, qk_ws, k_cap_tiles, v_cap_tiles, u, start, end, out, lane);    \
         return;
-#define KVC_ITEM4(BK, BV) KVC_ITEM(BK, BV, 0) KVC_ITEM(BK, BV, 1) KVC_ITEM(BK, BV, 2) KVC_ITEM(BK, BV, 3)
-                KVC_ITEM4(1, 1) KVC_ITEM4(1, 2) KVC_ITEM4(1, 3) KVC_ITEM4(1, 4)
-                KVC_ITEM4(2, 1) KVC_ITEM4(2, 2) KVC_ITEM4(2, 3) KVC_ITEM4(2, 4)
-                KVC_ITEM4(3, 1) KVC_ITEM4(3, 2) KVC_ITEM4(3, 3) KVC_ITEM4(3, 4)
-                KVC_ITEM4(4, 1) KVC_ITEM4(4, 2) KVC_ITEM4(4, 3) KVC_ITEM4(4, 4)
+#define KVC_ITEM4(BK, BV) KVC_ITEM(BK, BV, 0, 8) KVC_ITEM(BK, BV, 1, 8) KVC_ITEM(BK, BV, 2, 8) KVC_ITEM(BK, BV, 3, 8)
+#define KVC_ITEM4S(BK) KVC_ITEM4(BK, 3) KVC_ITEM(BK, 3, 0, 6) KVC_ITEM(BK, 3, 1, 6) KVC_ITEM(BK, 3, 2, 6) KVC_ITEM(BK, 3, 3, 6)
+                KVC_ITEM4(1, 1) KVC_ITEM4(1, 2) KVC_ITEM4S(1) KVC_ITEM4(1, 4)
+                KVC_ITEM4(2, 1) KVC_ITEM4(2, 2) KVC_ITEM4S(2) KVC_ITEM4(2, 4)
+                KVC_ITEM4(3, 1) KVC_ITEM4(3, 2) KVC_ITEM4S(3) KVC_ITEM4(3, 4)
+                KVC_ITEM4(4, 1) KVC_ITEM4(4, 2) KVC_ITEM4S(4) KVC_ITEM4(4, 4)
+#undef KVC_ITEM4S
 #undef KVC_ITEM4
 #undef KVC_ITEM
                 default: break;
             }
         }
     }
-    run_item<G, 0, 0, -1>(K, V, qa_ws, qk_ws, k_cap_tiles, v_cap_tiles, u, start, end, out, lane);
+    run_item<G, 0, 0, -1, 8>(K, V, qa_ws, qk_ws, k_cap_tiles, v_cap_tiles, u, start, end, out, lane);
 }
 
 // ---------------------------------------------------------------- combine
