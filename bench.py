@@ -256,15 +256,43 @@ def main():
     ms_step = s0.elapsed_time(s1) / args.steps
     log(f"{args.steps} steps: {ms_step:.3f} ms/step")
 
-    # decode call alone, events on the launch stream, for the roofline entry
+    # decode call alone, events on the launch stream, for the roofline entry: back to back, and with the
+    # 256 MB MALL flushed (a 512 MB write) before each call, outside the events; the roofline takes the
+    # mean of the flushed calls
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
     for a, b in evs:
         a.record()
         cache.decode(q, seq, n_att, out, ws)
         b.record()
     torch.cuda.synchronize()
+    t_b2b = float(np.mean([a.elapsed_time(b) for a, b in evs])) / 1e3
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    for i, (a, b) in enumerate(evs):
+        flush.fill_(i & 0xFF)
+        a.record()
+        cache.decode(q, seq, n_att, out, ws)
+        b.record()
+    torch.cuda.synchronize()
     t_dec = float(np.mean([a.elapsed_time(b) for a, b in evs])) / 1e3
+    del flush
     assert torch.isfinite(out).all().item()
+
+    # achievable HBM read rate on this device: the library's streaming-read probe over 2 GiB (best of 5)
+    probe = torch.ones(2 << 30, dtype=torch.uint8, device=dev)
+    sink = torch.zeros(1, dtype=torch.int32, device=dev)
+    kvc.kvc_read_probe(probe, sink)
+    p_ms = []
+    for _ in range(5):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        kvc.kvc_read_probe(probe, sink)
+        b.record()
+        torch.cuda.synchronize()
+        p_ms.append(a.elapsed_time(b))
+    read_gbs = probe.numel() / (min(p_ms) / 1e3) / 1e9
+    del probe, sink
+    torch.cuda.empty_cache()
 
     per_layer = None if args.no_per_layer else per_layer_loop(cache, w, q, seq, n_att, args.steps)
 
@@ -275,7 +303,8 @@ def main():
     step_bytes = dec_bytes + append_bytes
     value = step_bytes / (ms_step / 1e3) / 1e9
     achieved = dec_bytes / t_dec / 1e9
-    log(f"decode call {t_dec * 1e3:.3f} ms, {achieved:.1f} GB/s algorithmic ({dec_bytes / 1e9:.3f} GB)")
+    log(f"decode call {t_dec * 1e3:.3f} ms, {achieved:.1f} GB/s algorithmic ({dec_bytes / 1e9:.3f} GB); "
+        f"back to back {t_b2b * 1e3:.3f} ms; read probe {read_gbs:.1f} GB/s")
 
     res = {
         "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
@@ -286,7 +315,9 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(dec_bytes),
                      "kernel": "kvc_decode_attn (qproj + decode_partial + combine)",
-                     "alg_bytes_per_launch": dec_bytes, "avg_launch_ms": round(t_dec * 1e3, 4)},
+                     "alg_bytes_per_launch": dec_bytes, "avg_launch_ms": round(t_dec * 1e3, 4),
+                     "launch_ms_back_to_back": round(t_b2b * 1e3, 4), "achievable_read_GBs": round(read_gbs, 1),
+                     "frac_of_achievable": round(achieved / read_gbs, 4)},
         "per_layer_decode": per_layer,
         "encode": {"vectors_per_s": round(enc_vectors / t_enc, 1), "model_tokens_per_s": round(w.batch * T / t_enc, 1),
                    "ms": round(t_enc * 1e3, 3), "hbm_read_GBs": round(enc_read / t_enc / 1e9, 2)},

@@ -226,6 +226,18 @@ size_t kvc_decode_attn_workspace(const kvc_stream_desc* k, const kvc_stream_desc
  */
 int kvc_reconstruct(const kvc_stream_desc* s, int32_t t0, int32_t n_tok, float* out, void* stream);
 
+/*
+ * kvc_read_probe - measurement utility, not a step of the method: streams `bytes` bytes of device
+ * memory with 16-byte non-temporal loads over the whole device. Its rate is the achievable HBM read
+ * bandwidth that the decode kernels are compared against (the paper's premise, Sec. 1, is that decode
+ * is bound by reading the KV cache).
+ *  buf    device memory, 16-byte aligned; bytes a multiple of 16 (0: no launch).
+ *  sink   one device uint32, 4-byte aligned, owned by the caller; written only when the folded value
+ *         of every loaded word equals a fixed constant (it exists to keep the loads live).
+ * KVC_EINVAL on a null or misaligned argument. Async on `stream`.
+ */
+int kvc_read_probe(const void* buf, size_t bytes, uint32_t* sink, void* stream);
+
 /* Message of the last failing call on this thread ("" if none). */
 const char* kvc_last_error(void);
 

@@ -1053,6 +1053,19 @@ inline int combine_waves(int G, int n_chunks, int U, int ncu) {
 
 // ---------------------------------------------------------------- host side
 
+// ---------------------------------------------------------------- read probe
+
+// Streaming read of n16 16-byte words (non-temporal loads, grid-stride). The words fold into one
+// value per lane, stored to sink only when it equals a constant, so that the loads stay live.
+__global__ __launch_bounds__(256) void read_probe_kernel(const v4u* __restrict__ p, size_t n16, uint32_t* __restrict__ sink) {
+    uint32_t acc = 0u;
+    for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n16; i += (size_t)gridDim.x * 256) {
+        const v4u v = __builtin_nontemporal_load(p + i);
+        acc ^= v[0] ^ v[1] ^ v[2] ^ v[3];
+    }
+    if (acc == 0x9e3779b9u) sink[0] = acc;
+}
+
 namespace {
 
 
@@ -1244,4 +1257,16 @@ extern "C" int kvc_decode_attn(const kvc_stream_desc* k, const kvc_stream_desc* 
         default: hipLaunchKernelGGL(combine_kernel<16>, dim3(U), cblk, csm, st, V, L.n_chunks, part, out); break;
     }
     return check_launch("kvc_decode_attn");
+}
+
+extern "C" int kvc_read_probe(const void* buf, size_t bytes, uint32_t* sink, void* stream) {
+    clear_error();
+    if (!buf || !sink || (reinterpret_cast<uintptr_t>(buf) & 15) || (bytes & 15) || (reinterpret_cast<uintptr_t>(sink) & 3))
+        return set_error(KVC_EINVAL, "kvc_read_probe: buf and bytes must be multiples of 16 bytes, sink a 4-byte aligned word");
+    if (bytes == 0) return KVC_OK;
+    const size_t n16 = bytes / 16;
+    const size_t blocks = std::min<size_t>((n16 + 255) / 256, (size_t)64 * device_cus());
+    hipLaunchKernelGGL(read_probe_kernel, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream,
+                       reinterpret_cast<const v4u*>(buf), n16, sink);
+    return check_launch("kvc_read_probe");
 }

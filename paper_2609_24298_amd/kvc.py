@@ -69,6 +69,7 @@ def lib():
                                                 ctypes.c_int32, ctypes.c_int32]
         L.kvc_decode_attn_workspace.restype = ctypes.c_size_t
         L.kvc_reconstruct.argtypes = [ctypes.POINTER(StreamDesc), ctypes.c_int32, ctypes.c_int32, _p, _p]
+        L.kvc_read_probe.argtypes = [_p, ctypes.c_size_t, _p, _p]
         L.kvc_last_error.restype = ctypes.c_char_p
         L.kvc_version.restype = ctypes.c_int32
         _lib = L
@@ -242,3 +243,13 @@ def kvc_reconstruct(side: Side, t0: int, n_tok: int, out, stream=None):
     assert out.device == side.codes.device
     _check(lib().kvc_reconstruct(ctypes.byref(side.desc), int(t0), int(n_tok), ctypes.c_void_p(out.data_ptr()),
                                  _stream_ptr(stream)))
+
+
+def kvc_read_probe(buf, sink, stream=None):
+    """Streaming read of a device buffer (uint8 tensor, 16-byte aligned, a multiple of 16 bytes); sink:
+    a device int32/uint32 tensor of at least one element. Measures the achievable HBM read rate."""
+    import torch
+    assert buf.is_contiguous() and sink.is_contiguous() and sink.numel() >= 1
+    assert sink.dtype in (torch.int32, torch.uint32) and buf.device == sink.device
+    _check(lib().kvc_read_probe(ctypes.c_void_p(buf.data_ptr()), buf.numel() * buf.element_size(),
+                                ctypes.c_void_p(sink.data_ptr()), _stream_ptr(stream)))

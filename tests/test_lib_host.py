@@ -229,3 +229,15 @@ def test_decode_rejects_misaligned_query_without_gpu():
     rc = L.kvc_decode_attn(ctypes.byref(dk), ctypes.byref(dv), ctypes.c_void_p(258), 4, fake, 1, fake, fake, 1 << 20, None)
     assert rc == kvc.KVC_EINVAL
     assert b"16-byte" in L.kvc_last_error()
+
+
+def test_read_probe_validates_arguments_without_gpu():
+    # the bandwidth probe refuses misaligned or null arguments before any launch; zero bytes launch nothing
+    L = kvc.lib()
+    fake = ctypes.c_void_p(256)          # never dereferenced
+    assert L.kvc_read_probe(ctypes.c_void_p(264), 1024, fake, None) == kvc.KVC_EINVAL
+    assert L.kvc_read_probe(fake, 1000, fake, None) == kvc.KVC_EINVAL
+    assert L.kvc_read_probe(fake, 1024, ctypes.c_void_p(258), None) == kvc.KVC_EINVAL
+    assert L.kvc_read_probe(None, 1024, fake, None) == kvc.KVC_EINVAL
+    assert b"16 bytes" in L.kvc_last_error()
+    assert L.kvc_read_probe(fake, 0, fake, None) == kvc.KVC_OK
