@@ -465,22 +465,31 @@ __device__ __forceinline__ void v_tile(uint32_t* vb, const __amdgpu_buffer_rsrc_
 typedef _Float16 qp_h8 __attribute__((ext_vector_type(8)));
 typedef float qp_f4 __attribute__((ext_vector_type(4)));
 
-// One wavefront per unit. The projection Y = P_K Q (rank rows x query-head columns) runs on
+// NW wavefronts per unit (1 when the units fill the device, 8 for a few units), wavefront w taking
+// row blocks [w 8/NW, (w + 1) 8/NW). The projection Y = P_K Q (rank rows x query-head columns) runs on
 // v_mfma_f32_16x16x32_f16 (exact fp16 products, fp32 accumulation): A = 16 basis rows x 32
-// coordinates, B = 32 coordinates x 16 heads, eight row blocks x four k-steps, every operand
-// loaded straight from global memory with all loads in flight. Lane (kq, col) then holds rows
-// 16 rb + 4 kq + v of head col; a head's max and limb sums reduce over its four lanes.
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void qprep_kernel(DevSide K, const uint16_t* __restrict__ q, int G, int LM,
+// coordinates, B = 32 coordinates x 16 heads, four k-steps per row block, every operand loaded
+// straight from global memory with up to four row blocks' loads in flight. Lane (kq, col) then holds
+// rows 16 rb + 4 kq + v of head col; a head's max and limb sums reduce over its four lanes, then over
+// the wavefronts through LDS.
+template <int NW>
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2, 2))) void qprep_kernel(DevSide K, const uint16_t* __restrict__ q, int G, int LM,
                                                    v4i* __restrict__ qa, float4* __restrict__ qk) {
+    constexpr int RB = 8 / NW;                 // row blocks per wavefront
+    constexpr int HALF = RB > 4 ? 2 : 1;       // rounds of at most four row blocks' loads
+    constexpr int RQ = RB / HALF;
     extern __shared__ uint8_t img[];  // [2][LM][64][16] operand image
-    const int u = blockIdx.x, lane = threadIdx.x, col = lane & 15, kq = lane >> 4;
+    __shared__ float red_m[NW][16];
+    __shared__ int red_l[NW][16][kLimbs];
+    const int u = blockIdx.x, wv = threadIdx.x >> 6, lane = threadIdx.x & 63, col = lane & 15, kq = lane >> 4;
     const int r = K.r[u], b = K.b[u];
     const uint16_t* __restrict__ P = K.basis + K.basis_off[u];
     const int img_words = 2 * LM * 64 * 4;
-    for (int k = lane; k < img_words; k += 64) reinterpret_cast<uint32_t*>(img)[k] = 0u;
-    qp_f4 C[8];
+    for (int k = threadIdx.x; k < img_words; k += 64 * NW) reinterpret_cast<uint32_t*>(img)[k] = 0u;
+    __syncthreads();
+    qp_f4 C[RB];
 #pragma unroll
-    for (int rb = 0; rb < 8; ++rb) C[rb] = qp_f4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < RB; ++j) C[j] = qp_f4{0.f, 0.f, 0.f, 0.f};
     for (int h0 = 0; h0 < G; h0 += 16) {  // heads in groups of 16 columns
         const int g = h0 + col;
         qp_h8 B[4];
@@ -491,47 +500,53 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
             B[k4] = __builtin_bit_cast(qp_h8, w);
         }
 #pragma unroll
-        for (int half = 0; half < 2; ++half) {  // four row blocks' loads in flight at a time
-            uint4 A[4][4];
+        for (int half = 0; half < HALF; ++half) {
+            uint4 A[RQ][4];
 #pragma unroll
-            for (int rq = 0; rq < 4; ++rq)
+            for (int rq = 0; rq < RQ; ++rq)
 #pragma unroll
                 for (int k4 = 0; k4 < 4; ++k4) {
-                    const int row = 16 * (4 * half + rq) + col;
+                    const int row = 16 * (RB * wv + RQ * half + rq) + col;
                     A[rq][k4] = row < r ? reinterpret_cast<const uint4*>(P + (int64_t)row * kD + 32 * k4 + 8 * kq)[0]
                                         : uint4{0u, 0u, 0u, 0u};
                 }
 #pragma unroll
-            for (int rq = 0; rq < 4; ++rq) {
+            for (int rq = 0; rq < RQ; ++rq) {
                 qp_f4 c = qp_f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int k4 = 0; k4 < 4; ++k4)
                     c = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(qp_h8, A[rq][k4]), B[k4], c, 0, 0, 0);
-                C[4 * half + rq] = c;
+                C[RQ * half + rq] = c;
             }
         }
         const int hk = b == 8 ? 0 : (1 << (b - 1));
         const float scale0 = K.delta[u] * 1.4426950408889634f * 0.08838834764831845f;  // log2(e) / sqrt(128)
         float m = 0.f;
 #pragma unroll
-        for (int rb = 0; rb < 8; ++rb)
+        for (int j = 0; j < RB; ++j)
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
-                C[rb][v] *= scale0;
-                m = fmaxf(m, fabsf(C[rb][v]));
+                C[j][v] *= scale0;
+                m = fmaxf(m, fabsf(C[j][v]));
             }
         m = fmaxf(m, __shfl_xor(m, 16));
         m = fmaxf(m, __shfl_xor(m, 32));
+        if constexpr (NW > 1) {
+            if (kq == 0) red_m[wv][col] = m;
+            __syncthreads();
+#pragma unroll
+            for (int w = 0; w < NW; ++w) m = fmaxf(m, red_m[w][col]);
+        }
         const float sigma = m > 0.f ? m / 127.f : 1.f;
         const int g16 = r >> 4;
         int lsum[kLimbs] = {0, 0, 0};
 #pragma unroll
-        for (int rb = 0; rb < 8; ++rb)
+        for (int j = 0; j < RB; ++j)
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
-                const int i = 16 * rb + 4 * kq + v;  // rank coordinate
+                const int i = 16 * (RB * wv + j) + 4 * kq + v;  // rank coordinate
                 if (i < r && g < G) {
-                    const float x = C[rb][v] / sigma;
+                    const float x = C[j][v] / sigma;
                     const float l0 = fminf(fmaxf(rintf(x), -127.f), 127.f);
                     const float r1 = (x - l0) * 254.f;
                     const float l1 = fminf(fmaxf(rintf(r1), -127.f), 127.f);
@@ -555,17 +570,28 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
             lsum[k] += __shfl_xor(lsum[k], 16);
             lsum[k] += __shfl_xor(lsum[k], 32);
         }
-        if (kq == 0 && g < G) {
+        if constexpr (NW > 1) {
+            if (kq == 0)
+#pragma unroll
+                for (int k = 0; k < kLimbs; ++k) red_l[wv][col][k] = lsum[k];
+            __syncthreads();
+#pragma unroll
+            for (int k = 0; k < kLimbs; ++k) {
+                lsum[k] = 0;
+#pragma unroll
+                for (int w = 0; w < NW; ++w) lsum[k] += red_l[w][col][k];
+            }
+        }
+        if (wv == 0 && kq == 0 && g < G) {
             const float k0 = sigma, k1 = sigma * (1.f / 254.f), k2 = sigma * (1.f / 64516.f);
             const float bias = -(float)hk * ((float)lsum[0] * k0 + (float)lsum[1] * k1 + (float)lsum[2] * k2);
             qk[(int64_t)u * G + g] = float4{k0, k1, k2, bias};
         }
+        if constexpr (NW > 1) __syncthreads();  // red_m, red_l are rewritten by the next head group
     }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+    __syncthreads();
     v4i* dst = qa + (int64_t)u * 2 * LM * 64;
-    for (int k = lane; k < 2 * LM * 64; k += 64) dst[k] = reinterpret_cast<const v4i*>(img)[k];
+    for (int k = threadIdx.x; k < 2 * LM * 64; k += 64 * NW) dst[k] = reinterpret_cast<const v4i*>(img)[k];
 }
 
 // ---------------------------------------------------------------- partials
@@ -930,23 +956,27 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(Shape<G>::W,
 
 // ---------------------------------------------------------------- combine
 
-// One block of Wc wavefronts per unit (Wc = blockDim.x / 64: one for a few chunks, more when the
-// context is split into many). Lane l handles rank coordinates l and l + 64 of the merge and output
-// columns 2 l, 2 l + 1, for all G query heads. The chunks' partials merge in the log2 domain
-// (M = max m_c, L = sum l_c 2^(m_c - M), A_j = sum acc_c,j 2^(m_c - M)): wavefront w merges chunks
-// w, w + Wc, ... (a batch of chunks in flight at once, the running sums rescaled when a batch raises
-// M), the wavefronts' merges meet in LDS, and z_j = step_V (A_j / L + 1/2) is the dequantised
-// rank-space average. Then o = P_V^T z (the V reconstruction of Lemma lem:head-dist applied after the
-// softmax average, which is linear), computed by the first wavefront, which loads its two columns
+// One block of WC wavefronts per unit (one for a few chunks, more when the context is split into
+// many). Lane l handles rank coordinates l and l + 64 of the merge and output columns 2 l, 2 l + 1.
+// The chunks' partials merge in the log2 domain (M = max m_c, L = sum l_c 2^(m_c - M),
+// A_j = sum acc_c,j 2^(m_c - M)): wavefront w merges chunks w, w + WC, ... (a batch of chunks in
+// flight at once, the running sums rescaled when a batch raises M), the wavefronts' merges meet in
+// LDS, and z_j = step_V (A_j / L + 1/2) is the dequantised rank-space average. Then o = P_V^T z (the
+// V reconstruction of Lemma lem:head-dist applied after the softmax average, which is linear), with
+// the heads shared among the wavefronts (G / WC each, at least one), each loading its two columns
 // of every basis row at the start.
-constexpr int kCombMaxRed = 32;  // Wc x G at most (LDS of the cross-wavefront merge)
-template <int G>
-__global__ __launch_bounds__(64 * (kCombMaxRed / G < 8 ? kCombMaxRed / G : 8)) __attribute__((amdgpu_waves_per_eu(2, 2)))
+constexpr int kCombMaxRed = 32;  // WC x G at most (LDS of the cross-wavefront merge)
+template <int G, int WC>
+__global__ __launch_bounds__(64 * WC) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void combine_kernel(DevSide V, int n_chunks, const float* __restrict__ part, float* __restrict__ out) {
+    static_assert(WC * G <= kCombMaxRed || WC == 1, "combine_kernel: cross-wavefront merge exceeds its LDS");
+    constexpr int Wc = WC;
+    constexpr int GH = G / WC > 0 ? G / WC : 1;          // heads whose output one wavefront computes
     constexpr int kCombBatch = 16 / G > 0 ? 16 / G : 1;  // chunks whose partials are in flight together (per wavefront)
     __shared__ float zs[G][kD];
-    extern __shared__ float comb_dsm[];  // [Wc * G][kPartStride] per (wavefront, head): M, L, -, -, A[128]
-    const int u = blockIdx.x, lane = threadIdx.x & 63, wv = threadIdx.x >> 6, Wc = blockDim.x >> 6;
+    extern __shared__ float comb_dsm[];  // [WC * G][kPartStride] per (wavefront, head): M, L, -, -, A[128]
+    const int u = blockIdx.x, lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int gb = wv * GH;  // first head of this wavefront's output (none when gb >= G)
     float(*red)[kPartStride] = reinterpret_cast<float(*)[kPartStride]>(comb_dsm);
     const int rv = V.r[u];
     const float step = V.delta[u];
@@ -954,7 +984,7 @@ void combine_kernel(DevSide V, int n_chunks, const float* __restrict__ part, flo
     const uint32_t* __restrict__ P32 = reinterpret_cast<const uint32_t*>(V.basis + V.basis_off[u]);
     uint32_t pw[kD];
 #pragma unroll
-    for (int i = 0; i < kD; ++i) pw[i] = (wv == 0 && i < rv) ? P32[i * (kD / 2) + lane] : 0u;
+    for (int i = 0; i < kD; ++i) pw[i] = (gb < G && i < rv) ? P32[i * (kD / 2) + lane] : 0u;
     const float* __restrict__ pu = part + (int64_t)u * n_chunks * G * kPartStride;
     float M[G], L[G], A0[G], A1[G];
 #pragma unroll
@@ -1023,35 +1053,66 @@ void combine_kernel(DevSide V, int n_chunks, const float* __restrict__ part, flo
         zs[g][lane + 64] = (Lg > 0.f && lane + 64 < rv) ? step * fmaf(B1, inv, 0.5f) : 0.f;
     }
     __syncthreads();
-    if (wv == 0) {
-        float o0[G], o1[G];
+    if (gb < G) {
+        float o0[GH], o1[GH];
 #pragma unroll
-        for (int g = 0; g < G; ++g) o0[g] = o1[g] = 0.f;
+        for (int j = 0; j < GH; ++j) o0[j] = o1[j] = 0.f;
 #pragma unroll
         for (int i = 0; i < kD; ++i) {
             const float p0 = h2f((uint16_t)(pw[i] & 0xffffu)), p1 = h2f((uint16_t)(pw[i] >> 16));
 #pragma unroll
-            for (int g = 0; g < G; ++g) {
-                const float z = zs[g][i];  // zero past the rank
-                o0[g] = fmaf(p0, z, o0[g]);
-                o1[g] = fmaf(p1, z, o1[g]);
+            for (int j = 0; j < GH; ++j) {
+                const float z = zs[gb + j][i];  // zero past the rank
+                o0[j] = fmaf(p0, z, o0[j]);
+                o1[j] = fmaf(p1, z, o1[j]);
             }
         }
 #pragma unroll
-        for (int g = 0; g < G; ++g)
-            reinterpret_cast<float2*>(out + ((int64_t)u * G + g) * kD)[lane] = float2{o0[g], o1[g]};
+        for (int j = 0; j < GH; ++j)
+            reinterpret_cast<float2*>(out + ((int64_t)u * G + gb + j) * kD)[lane] = float2{o0[j], o1[j]};
     }
 }
 
-// Wavefronts of a combine block: enough that each merges about 8 chunks, within the LDS of the
-// cross-wavefront merge, at most one per query head, and few enough that every block is resident
-// at once (the kernel's register budget leaves two wavefronts per SIMD, eight per CU).
+// Wavefronts of a combine block (1, 2, 4 or 8): enough that each merges about 8 chunks, within the
+// LDS of the cross-wavefront merge, and few enough that every block is resident at once (the
+// kernel's register budget leaves two wavefronts per SIMD, eight per CU).
 inline int combine_waves(int G, int n_chunks, int U, int ncu) {
-    const int cap = std::min(std::min(std::max(kCombMaxRed / G, 1), std::min(G, 8)), std::max(1, 8 * ncu / std::max(U, 1)));
-    return std::max(1, std::min(cap, (n_chunks + 7) / 8));
+    const int cap = std::min(std::min(std::max(kCombMaxRed / G, 1), 8), std::max(1, 8 * ncu / std::max(U, 1)));
+    int w = 1;
+    while (2 * w <= cap && 8 * w < n_chunks) w *= 2;
+    return w;
 }
 
 // ---------------------------------------------------------------- host side
+
+// Combine launch with cw (a power of two that combine_waves chose for this G) wavefronts per block.
+template <int G>
+void launch_combine(int cw, dim3 grid, dim3 blk, size_t smem, hipStream_t st, const DevSide& V, int n_chunks,
+                    const float* part, float* out) {
+    switch (cw) {
+        case 8:
+            if constexpr (8 * G <= kCombMaxRed) {
+                hipLaunchKernelGGL((combine_kernel<G, 8>), grid, blk, smem, st, V, n_chunks, part, out);
+                return;
+            }
+            break;
+        case 4:
+            if constexpr (4 * G <= kCombMaxRed) {
+                hipLaunchKernelGGL((combine_kernel<G, 4>), grid, blk, smem, st, V, n_chunks, part, out);
+                return;
+            }
+            break;
+        case 2:
+            if constexpr (2 * G <= kCombMaxRed) {
+                hipLaunchKernelGGL((combine_kernel<G, 2>), grid, blk, smem, st, V, n_chunks, part, out);
+                return;
+            }
+            break;
+        default:
+            break;
+    }
+    hipLaunchKernelGGL((combine_kernel<G, 1>), grid, dim3(64), (size_t)G * kPartStride * 4, st, V, n_chunks, part, out);
+}
 
 // ---------------------------------------------------------------- read probe
 
@@ -1234,7 +1295,11 @@ extern "C" int kvc_decode_attn(const kvc_stream_desc* k, const kvc_stream_desc* 
     const DevSide K = dev_side(k), V = dev_side(v);
     const int LM = (G + 3) / 4;
     const size_t qsm = (size_t)2 * LM * 64 * 16;
-    hipLaunchKernelGGL(qprep_kernel, dim3(U), dim3(64), qsm, st, K, q, G, LM, qa, qk);
+    // one wavefront per unit while the units fill the device, eight (one per row block) for a few units
+    if ((int64_t)U * 4 >= (int64_t)device_cus() * 8)
+        hipLaunchKernelGGL(qprep_kernel<1>, dim3(U), dim3(64), qsm, st, K, q, G, LM, qa, qk);
+    else
+        hipLaunchKernelGGL(qprep_kernel<8>, dim3(U), dim3(512), qsm, st, K, q, G, LM, qa, qk);
     const int kct = (k->capacity + kTile - 1) / kTile, vct = (v->capacity + kTile - 1) / kTile;
     const dim3 grid(L.n_chunks, U);
     int e = KVC_OK;
@@ -1250,11 +1315,11 @@ extern "C" int kvc_decode_attn(const kvc_stream_desc* k, const kvc_stream_desc* 
     const dim3 cblk(64 * cw);
     const size_t csm = (size_t)cw * G * kPartStride * 4;
     switch (G) {
-        case 1: hipLaunchKernelGGL(combine_kernel<1>, dim3(U), cblk, csm, st, V, L.n_chunks, part, out); break;
-        case 2: hipLaunchKernelGGL(combine_kernel<2>, dim3(U), cblk, csm, st, V, L.n_chunks, part, out); break;
-        case 4: hipLaunchKernelGGL(combine_kernel<4>, dim3(U), cblk, csm, st, V, L.n_chunks, part, out); break;
-        case 8: hipLaunchKernelGGL(combine_kernel<8>, dim3(U), cblk, csm, st, V, L.n_chunks, part, out); break;
-        default: hipLaunchKernelGGL(combine_kernel<16>, dim3(U), cblk, csm, st, V, L.n_chunks, part, out); break;
+        case 1: launch_combine<1>(cw, dim3(U), cblk, csm, st, V, L.n_chunks, part, out); break;
+        case 2: launch_combine<2>(cw, dim3(U), cblk, csm, st, V, L.n_chunks, part, out); break;
+        case 4: launch_combine<4>(cw, dim3(U), cblk, csm, st, V, L.n_chunks, part, out); break;
+        case 8: launch_combine<8>(cw, dim3(U), cblk, csm, st, V, L.n_chunks, part, out); break;
+        default: launch_combine<16>(cw, dim3(U), cblk, csm, st, V, L.n_chunks, part, out); break;
     }
     return check_launch("kvc_decode_attn");
 }
