@@ -81,6 +81,24 @@ def test_decode_every_group_size(G):
     _check_units(w, cache, ot, xk, xv, q, seq, out.cpu().numpy(), range(w.n_units), f"G={G}", w.tokens)
 
 
+@pytest.mark.parametrize("G", [1, 4, 8, 16])
+def test_decode_many_chunks_every_group_size(G):
+    # two units over 65 tiles: the context splits into more than 32 chunks, so the combine runs with
+    # its widest block for the group size (8 wavefronts for G <= 4, 4 for G = 8, 2 for G = 16) and the
+    # query projection on eight wavefronts per unit
+    w = synth.Workload(f"chunks_g{G}", layers=1, kv_heads=1, group=G, batch=2, tokens=4100, bpd=2.0)
+    log(f"[chunks G={G}] build")
+    cache, xk, xv = _build(w, w.tokens, w.tokens)
+    cache.encode(xk, xv, 0, w.tokens)
+    ot = OracleTables(w, cache.stats)
+    q = pipeline.draw_queries(w, cache.stats, 5, "cuda", scale=6.0)
+    seq = np.array([4100, 2345], dtype=np.int32)
+    ws, out = cache.decode_buffers(w.tokens)
+    cache.decode(q, torch.as_tensor(seq, device="cuda"), w.tokens, out, ws)
+    torch.cuda.synchronize()
+    _check_units(w, cache, ot, xk, xv, q, seq, out.cpu().numpy(), range(w.n_units), f"chunks G={G}", w.tokens)
+
+
 def _sampled_full(w, T, units, seed=0, qscale=1.0):
     """Bench launch configuration: encode T tokens, append one, decode over T + 1; check `units`."""
     log(f"[{w.name}] build cache + draw {2 * w.n_units * T} tokens")
