@@ -1179,10 +1179,11 @@ int64_t resident_slots(int G, size_t smem) {
 }
 
 // Split of each unit's context into n_chunks equal chunks of whole tiles (at most kMaxChunkTiles
-// each). Among counts that give at least one work item per resident slot, the count minimises
+// each). The count minimises
 //   rounds x (tiles per item + per-item overhead) + (straggler share) x tiles per item,
-// rounds = ceil(items / resident slots): whole rounds with no short remainder, and items short
-// enough that units of different cost even out.
+// rounds = ceil(items / resident slots): whole rounds with no short remainder, items short enough
+// that units of different cost even out, and no more items than that (one round of longer items
+// can beat two rounds of items half as long that would fill every slot).
 constexpr int kItemOverheadTiles = 4;
 constexpr double kStragglerShare = 0.5;
 
@@ -1198,24 +1199,17 @@ WsLayout ws_layout(const kvc_stream_desc* k, int G, int max_seq) {
     L.stage_bytes = stage_lds_bytes(k);
     const int64_t slots = resident_slots(G, partial_smem(G, L.stage_bytes));
     const int tpu = (max_seq + kTile - 1) / kTile;
-    bool best_full = false;
-    double best_cost = 0.0;
-    int64_t best_items = -1;
+    double best_cost = -1.0;
     L.chunk = std::min(tpu, kMaxChunkTiles) * kTile;
     L.n_chunks = (tpu + kMaxChunkTiles - 1) / kMaxChunkTiles;
     for (int n = 1; n <= tpu && n <= 4096; ++n) {
         const int c = (tpu + n - 1) / n;
         if ((tpu + c - 1) / c != n || c > kMaxChunkTiles) continue;
         const int64_t items = (int64_t)U * n;
-        const bool full = items >= slots;
         const int64_t rounds = (items + slots - 1) / slots;
         const double cost = (double)rounds * (c + kItemOverheadTiles) + kStragglerShare * c;
-        const bool better = best_items < 0 || (full && !best_full) ||
-                            (full && best_full && cost < best_cost) || (!full && !best_full && items > best_items);
-        if (better) {
-            best_full = full;
+        if (best_cost < 0.0 || cost < best_cost) {
             best_cost = cost;
-            best_items = items;
             L.chunk = c * kTile;
             L.n_chunks = n;
         }
