@@ -100,6 +100,23 @@ __device__ __forceinline__ double wave_sum(double v) {
     return v;
 }
 
+// Code from y ~ P_c . x (an fp64 sum of the 128 exact fp16 products, any order): true when y is far
+// enough from every threshold for the code to be certain. jn is a threshold index near y / step;
+// the sign of y - jn step is certain when |y - jn step| exceeds the bound, and then (for
+// e < step / 4) y lies between the jn - 1 and jn + 1 thresholds.
+__device__ __forceinline__ bool certain_code(double y, float step, int b, float pn, float xn, uint32_t& code) {
+    const double e = 0x1p-45 * (double)pn * (double)xn * 1.01;
+    const int h = 1 << (b - 1);
+    const double st = step;
+    const double jn = rint(y * (1.0 / st));
+    const double d = fma(-jn, st, y);
+    if (e < 0.25 * st && fabs(d) > e + 0x1p-50 * fabs(y) && fabs(d) < 0.75 * st) {
+        code = (uint32_t)fmin(fmax(jn - (d < 0.0 ? 1.0 : 0.0) + h, 0.0), (double)((1 << b) - 1));
+        return true;
+    }
+    return false;
+}
+
 // Code of coordinate c for token row `xrow`, decided by the whole wavefront: fp64 sum of the 128
 // exact products (lane takes j = 2 lane, 2 lane + 1), then the exact path if still undecided.
 // Uniform across the wavefront.
@@ -111,15 +128,8 @@ __device__ uint32_t resolve_code_wave(const uint16_t* __restrict__ Pl_row, const
     const double s = (double)h2f((uint16_t)(pw & 0xffff)) * (double)h2f((uint16_t)(xw & 0xffff)) +
                      (double)h2f((uint16_t)(pw >> 16)) * (double)h2f((uint16_t)(xw >> 16));
     const double y = wave_sum(s);
-    const double e = 0x1p-45 * (double)pn * (double)xn * 1.01;
-    const int h = 1 << (b - 1);
-    const double st = step;
-    // jn: a threshold index near y / step; the sign of y - jn step is certain when |y - jn step|
-    // exceeds the bound, and then (for e < step / 4) y lies between jn - 1 and jn + 1 thresholds.
-    const double jn = rint(y * (1.0 / st));
-    const double d = fma(-jn, st, y);
-    if (e < 0.25 * st && fabs(d) > e + 0x1p-50 * fabs(y) && fabs(d) < 0.75 * st)
-        return (uint32_t)fmin(fmax(jn - (d < 0.0 ? 1.0 : 0.0) + h, 0.0), (double)((1 << b) - 1));
+    uint32_t code;
+    if (certain_code(y, step, b, pn, xn, code)) return code;
     return exact_code(Pg_row, xrow, step, b);
 }
 
@@ -206,6 +216,8 @@ __global__ __launch_bounds__(kEncMmaThreads) __attribute__((amdgpu_waves_per_eu(
     float* __restrict__ etok = etoks + wv * kTile;
     const int h = 1 << (b - 1);
     const float fh = (float)h, fmax_code = (float)(2 * h - 1), inv = 1.f / step;
+    const float fh_lo = fh - 0.5f;                                       // t' = t - 1/2
+    const float half_amb = 0.5f - (float)(3 * h + 4) * 0x1p-22f;         // 1/2 - c_amb (exact in fp32)
     const int g16 = r >> 4, rho = r & 15, n_mc = (r + 15) >> 4;
     uint8_t* __restrict__ stream = s.codes + s.code_off[u];
     const uint16_t* __restrict__ xu = x + (int64_t)u * x_stride;
@@ -260,9 +272,12 @@ __global__ __launch_bounds__(kEncMmaThreads) __attribute__((amdgpu_waves_per_eu(
             }
             // K: lane holds coordinates 16 mc + 4 grp + i of token 16 nt + col.
             // V: lane holds tokens 16 nt + 4 grp + i of coordinate 16 mc + col.
-            // t = y / step + 2^(b-1): its floor, clamped, is the code; the element is undecided if an
-            // integer lies within the error bound (in step units) of t, which adds (|t| + 2^(b-1)) 2^-22
-            // for the rounding of 1 / step and of the fused multiply-add.
+            // t = y / step + 2^(b-1): its floor, clamped, is the code. With t' = t - 1/2 (one fused
+            // multiply-add) the floor is rint(t') wherever t is not within the error bound eps of an
+            // integer, i.e. wherever |t' - rint(t')| < 1/2 - eps; the other elements are undecided.
+            // eps = (the basis-product bound tb) + c_amb, c_amb covering the rounding of 1 / step and
+            // of the multiply-add, (|t| + 2^(b-1) + 1) 2^-22, for every |t| <= 2^b + 1 (beyond, the
+            // code is clamped to 0 or 2^b - 1 whatever the error).
             bool any_amb = false;
             uint32_t cw[4];
 #pragma unroll
@@ -270,13 +285,12 @@ __global__ __launch_bounds__(kEncMmaThreads) __attribute__((amdgpu_waves_per_eu(
                 uint32_t w = 0;
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    const float tb = side == KVC_SIDE_K ? et[nt] * tolc[16 * mc + 4 * grp + i]
-                                                        : etok[16 * nt + 4 * grp + i] * tolc[16 * mc + col];
-                    const float t = fmaf(acc[nt][i], inv, fh);
-                    const float f = floorf(t);
-                    const float fr = t - f;
-                    any_amb |= fminf(fr, 1.f - fr) <= fmaf(fabsf(t) + fh, 0x1p-22f, tb);
-                    w = __builtin_amdgcn_cvt_pk_u8_f32(__builtin_amdgcn_fmed3f(f, 0.f, fmax_code), i, w);
+                    const float thr = side == KVC_SIDE_K ? fmaf(-et[nt], tolc[16 * mc + 4 * grp + i], half_amb)
+                                                         : fmaf(-etok[16 * nt + 4 * grp + i], tolc[16 * mc + col], half_amb);
+                    const float tp = fmaf(acc[nt][i], inv, fh_lo);
+                    const float m = __builtin_rintf(tp);
+                    any_amb |= fabsf(tp - m) >= thr;
+                    w = __builtin_amdgcn_cvt_pk_u8_f32(__builtin_amdgcn_fmed3f(m, 0.f, fmax_code), i, w);
                 }
                 cw[nt] = w;
             }
@@ -314,11 +328,10 @@ __global__ __launch_bounds__(kEncMmaThreads) __attribute__((amdgpu_waves_per_eu(
                 for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
-                        const float tb = side == KVC_SIDE_K ? et[nt] * tolc[16 * mc + 4 * grp + i]
-                                                            : etok[16 * nt + 4 * grp + i] * tolc[16 * mc + col];
-                        const float t = fmaf(acc[nt][i], inv, fh);
-                        const float fr = t - floorf(t);
-                        if (fminf(fr, 1.f - fr) <= fmaf(fabsf(t) + fh, 0x1p-22f, tb)) ambm |= 1u << (4 * nt + i);
+                        const float thr = side == KVC_SIDE_K ? fmaf(-et[nt], tolc[16 * mc + 4 * grp + i], half_amb)
+                                                             : fmaf(-etok[16 * nt + 4 * grp + i], tolc[16 * mc + col], half_amb);
+                        const float tp = fmaf(acc[nt][i], inv, fh_lo);
+                        if (fabsf(tp - __builtin_rintf(tp)) >= thr) ambm |= 1u << (4 * nt + i);
                     }
                 uint64_t pend = __ballot(ambm != 0);
                 while (pend) {
