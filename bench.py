@@ -53,15 +53,16 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(per_launch_alg: int):
-    """HBM bytes per decode call from the committed rocprofv3 counter summary, if it is current."""
+def measured_traffic(per_launch_alg: int, workload: str):
+    """HBM bytes per decode call from the committed rocprofv3 counter summary, if it is current and of
+    this workload."""
     path = os.path.join(ROOT, "profiles", "decode_attn_llama8b_b8_t32k_2bpd_traffic.json")
     try:
         with open(path) as f:
             t = json.load(f)
     except (OSError, ValueError):
         return None
-    if t.get("kernel_source_sha") != kernel_source_hash():
+    if t.get("kernel_source_sha") != kernel_source_hash() or t.get("workload") != workload:
         return None
     return t.get("hbm_bytes_per_call")
 
@@ -189,6 +190,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-per-layer", action="store_true",
                     help="skip the per-layer loop (profiling runs that summarise the all-layers call)")
+    ap.add_argument("--uniform", type=int, nargs=4, metavar=("RK", "BK", "RV", "BV"), default=None,
+                    help="measurement case: one (r, b) pair per side for every head instead of the allocator's "
+                         "(the workload name gets the pairs appended; never the headline line)")
     ap.add_argument("--copy-calib", action="store_true",
                     help="after the timed region, run one plain 1 GiB device-to-device copy (the reference kernel "
                          "for scaling HBM byte counters)")
@@ -208,7 +212,7 @@ def main():
     torch.cuda.set_device(dev)
     log(f"workload {w}")
     t_setup = time.perf_counter()
-    cache = pipeline.Cache(w, seed=args.seed, device=dev, capacity=T + kvc.TILE)
+    cache = pipeline.Cache(w, seed=args.seed, device=dev, capacity=T + kvc.TILE, uniform=args.uniform)
     log(f"tables + bases in {time.perf_counter() - t_setup:.1f} s; "
         f"K (r,b) spread {len(set(zip(cache.k_tab.r.tolist(), cache.k_tab.b.tolist())))} pairs")
 
@@ -306,14 +310,16 @@ def main():
     log(f"decode call {t_dec * 1e3:.3f} ms, {achieved:.1f} GB/s algorithmic ({dec_bytes / 1e9:.3f} GB); "
         f"back to back {t_b2b * 1e3:.3f} ms; read probe {read_gbs:.1f} GB/s")
 
+    res_workload = w.name + ("" if args.uniform is None else "@uniform_k{}_{}_v{}_{}".format(*args.uniform))
     res = {
         "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "f32", "data": "synthetic",
-        "config": {"workload": w.name, "layers": w.layers, "kv_heads": w.kv_heads, "q_per_kv": w.group,
+        "config": {"workload": res_workload,
+                   "layers": w.layers, "kv_heads": w.kv_heads, "q_per_kv": w.group,
                    "batch": w.batch, "context": T, "bpd_per_side": w.bpd, "head_dim": w.d},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(dec_bytes),
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(dec_bytes, res_workload),
                      "kernel": "kvc_decode_attn (qproj + decode_partial + combine)",
                      "alg_bytes_per_launch": dec_bytes, "avg_launch_ms": round(t_dec * 1e3, 4),
                      "launch_ms_back_to_back": round(t_b2b * 1e3, 4), "achievable_read_GBs": round(read_gbs, 1),
@@ -331,7 +337,7 @@ def main():
         torch.cuda.synchronize()
         log(f"copy calibration: {n} bytes read and written")
         del src, dst
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and args.uniform is None:  # the oracle sample builds its own allocation
         log("cpu baseline (oracle) ...")
         try:
             res["cpu_baseline"] = cpu_baseline(w, cache.stats, args.seed, [0, w.n_units // 2 + 3], T)

@@ -23,14 +23,24 @@ class SideTables:
     delta: np.ndarray      # per head, float32
 
 
-def allocate_workload(w: synth.Workload, stats, bpd: float | None = None, solver: int = kvc.SOLVER_DAMPED):
-    """Joint K+V tables: K with attention-KL weights and C1+C2, V with MSE weights and C1 only."""
+def allocate_workload(w: synth.Workload, stats, bpd: float | None = None, solver: int = kvc.SOLVER_DAMPED,
+                      uniform=None):
+    """Joint K+V tables: K with attention-KL weights and C1+C2, V with MSE weights and C1 only.
+
+    uniform = (r_K, b_K, r_V, b_V) replaces the allocator's (r, b) by one pair per side for every head
+    (the coordinate order and the bases are still built per head): a measurement case that isolates
+    one code shape, not the method's allocation."""
     bpd = w.bpd if bpd is None else bpd
     lam_k = np.stack([s.lam_k for s in stats])
     sq = np.stack([s.sigma2_q for s in stats])
     lam_v = np.stack([s.lam_v for s in stats])
     ak = kvc.kvc_allocate(lam_k, sq, kvc.alloc_opts(bpd, solver))
     av = kvc.kvc_allocate(lam_v, None, kvc.alloc_opts(bpd, kvc.SOLVER_C1_ONLY))
+    if uniform is not None:
+        rk, bk, rv, bv = (int(x) for x in uniform)
+        for a, r, b in ((ak, rk, bk), (av, rv, bv)):
+            a["r"] = np.full_like(a["r"], r)
+            a["b"] = np.full_like(a["b"], b)
     sides = []
     for a, lam_key, U_key, sign_key in ((ak, "lam_k", "U_k", "sign_k"), (av, "lam_v", "U_v", "sign_v")):
         Ps, ds = [], []
@@ -81,13 +91,13 @@ class Cache:
     """A compressed K/V cache for a workload plus its decode buffers."""
 
     def __init__(self, w: synth.Workload, seed: int = 0, device="cuda", bpd: float | None = None,
-                 capacity: int | None = None, solver: int = kvc.SOLVER_DAMPED, stats=None):
+                 capacity: int | None = None, solver: int = kvc.SOLVER_DAMPED, stats=None, uniform=None):
         import torch
         self.w = w
         self.seed = seed
         self.device = torch.device(device)
         self.stats = synth.workload_stats(w, seed) if stats is None else stats
-        self.k_tab, self.v_tab = allocate_workload(w, self.stats, bpd, solver)
+        self.k_tab, self.v_tab = allocate_workload(w, self.stats, bpd, solver, uniform)
         self.capacity = w.tokens if capacity is None else capacity
         self.K = build_side(kvc.SIDE_K, self.k_tab, w, self.capacity, device)
         self.V = build_side(kvc.SIDE_V, self.v_tab, w, self.capacity, device)
