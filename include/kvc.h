@@ -220,6 +220,19 @@ size_t kvc_decode_attn_workspace(const kvc_stream_desc* k, const kvc_stream_desc
                                  int32_t G, int32_t max_seq_len);
 
 /*
+ * kvc_encode_kv - kvc_encode of the keys and the values of the same tokens in one call.
+ * Paper: table step 7-8 (a decode step caches the new token's key and value). For
+ * n_tok <= 4 (appending a decode step's tokens) both sides run in one launch; longer
+ * runs take the bulk encoder, one launch per side. Codes are those kvc_encode writes.
+ *  k, v          descriptors of the K (side 0) and V (side 1) streams, same n_units.
+ *  xk, xv        device fp16 tokens of each side, laid out as kvc_encode's x.
+ * Same requirements and errors as kvc_encode for each side, plus KVC_EINVAL for
+ * swapped sides or differing unit counts. Async on `stream`.
+ */
+int kvc_encode_kv(const kvc_stream_desc* k, const kvc_stream_desc* v, const uint16_t* xk, int64_t xk_unit_stride,
+                  const uint16_t* xv, int64_t xv_unit_stride, int32_t t0, int32_t n_tok, void* stream);
+
+/*
  * kvc_reconstruct - x_hat_t = P^T z_t for tokens [t0, t0 + n_tok) of every unit.
  * Paper: Appendix A, Lemma lem:head-dist (x_hat = U_r H_r^T Q(H_r U_r^T x)).
  *  out   device f32 [n_units][n_tok][d]. Async.

@@ -17,6 +17,7 @@
 
 #include <cmath>
 #include <cstdint>
+#include <utility>
 
 #include "kvc_device.h"
 #include "kvc_internal.h"
@@ -416,14 +417,14 @@ __device__ __forceinline__ float row_sum16(float v) {
 constexpr int kAppThreads = kD;
 constexpr int kAppMaxTok = 4;
 
-__global__ __launch_bounds__(kAppThreads) void append_kernel(DevSide s, int side, const uint16_t* __restrict__ x,
-                                                             int64_t x_stride, int t0, int n_tok) {
+__device__ __forceinline__ void append_unit(const DevSide& s, int side, const uint16_t* __restrict__ x,
+                                            int64_t x_stride, int t0, int n_tok, int u) {
     __shared__ float xs[kAppMaxTok][kD];
     __shared__ float red[kAppMaxTok][kAppThreads / 64];
     __shared__ uint8_t cs[kAppMaxTok][kD];
     __shared__ float ys[kAppMaxTok][kD];
     __shared__ float pns[kD];
-    const int u = blockIdx.x, i = threadIdx.x;
+    const int i = threadIdx.x;
     const int r = s.r[u], b = s.b[u];
     const float step = s.delta[u];
     const uint16_t* __restrict__ P = s.basis + s.basis_off[u];
@@ -545,6 +546,20 @@ __global__ __launch_bounds__(kAppThreads) void append_kernel(DevSide s, int side
     }
 }
 
+// One side: one block per unit.
+__global__ __launch_bounds__(kAppThreads) void append_kernel(DevSide s, int side, const uint16_t* __restrict__ x,
+                                                             int64_t x_stride, int t0, int n_tok) {
+    append_unit(s, side, x, x_stride, t0, n_tok, blockIdx.x);
+}
+
+// Both sides in one launch: block (u, 0) appends unit u's keys, block (u, 1) its values.
+__global__ __launch_bounds__(kAppThreads) void append_kv_kernel(DevSide k, DevSide v, const uint16_t* __restrict__ xk,
+                                                                int64_t xk_stride, const uint16_t* __restrict__ xv,
+                                                                int64_t xv_stride, int t0, int n_tok) {
+    if (blockIdx.y == 0) append_unit(k, KVC_SIDE_K, xk, xk_stride, t0, n_tok, blockIdx.x);
+    else append_unit(v, KVC_SIDE_V, xv, xv_stride, t0, n_tok, blockIdx.x);
+}
+
 // ---------------------------------------------------------------- reconstruct
 
 constexpr int kRecThreads = 256;
@@ -631,6 +646,30 @@ extern "C" int kvc_encode(const kvc_stream_desc* s, const uint16_t* x, int64_t x
         hipLaunchKernelGGL(encode_mfma_kernel<KVC_SIDE_V>, grid, dim3(kEncMmaThreads), smem, (hipStream_t)stream,
                            dev_side(s), x, x_unit_stride, t0, n_tok, tile_first, n_tiles);
     return check_launch("kvc_encode");
+}
+
+extern "C" int kvc_encode_kv(const kvc_stream_desc* k, const kvc_stream_desc* v, const uint16_t* xk,
+                             int64_t xk_unit_stride, const uint16_t* xv, int64_t xv_unit_stride, int32_t t0,
+                             int32_t n_tok, void* stream) {
+    clear_error();
+    if (int e = validate_desc(k, "kvc_encode_kv(k)")) return e;
+    if (int e = validate_desc(v, "kvc_encode_kv(v)")) return e;
+    if (k->side != KVC_SIDE_K || v->side != KVC_SIDE_V) return set_error(KVC_EINVAL, "kvc_encode_kv: descriptor sides");
+    if (k->n_units != v->n_units) return set_error(KVC_EINVAL, "kvc_encode_kv: K and V unit counts differ");
+    if (n_tok > kAppMaxTok) {  // runs of tiles: the bulk encoder, one launch per side
+        if (int e = kvc_encode(k, xk, xk_unit_stride, t0, n_tok, stream)) return e;
+        return kvc_encode(v, xv, xv_unit_stride, t0, n_tok, stream);
+    }
+    if (t0 < 0 || n_tok < 0) return set_error(KVC_EINVAL, "kvc_encode_kv: negative t0 or n_tok");
+    if ((int64_t)t0 + n_tok > k->capacity || (int64_t)t0 + n_tok > v->capacity)
+        return set_error(KVC_ENOSPACE, "kvc_encode_kv: t0 + n_tok > capacity");
+    if (n_tok == 0 || k->n_units == 0) return KVC_OK;
+    for (const auto& xs : {std::make_pair(xk, xk_unit_stride), std::make_pair(xv, xv_unit_stride)})
+        if (!xs.first || (reinterpret_cast<uintptr_t>(xs.first) & 15) || (xs.second & 7) || xs.second < (int64_t)n_tok * kD)
+            return set_error(KVC_EINVAL, "kvc_encode_kv: x must be 16-byte aligned with stride a multiple of 8 and >= n_tok*d");
+    hipLaunchKernelGGL(append_kv_kernel, dim3(k->n_units, 2), dim3(kAppThreads), 0, (hipStream_t)stream, dev_side(k),
+                       dev_side(v), xk, xk_unit_stride, xv, xv_unit_stride, t0, n_tok);
+    return check_launch("kvc_encode_kv");
 }
 
 extern "C" int kvc_reconstruct(const kvc_stream_desc* s, int32_t t0, int32_t n_tok, float* out, void* stream) {

@@ -70,6 +70,8 @@ def lib():
         L.kvc_decode_attn_workspace.restype = ctypes.c_size_t
         L.kvc_reconstruct.argtypes = [ctypes.POINTER(StreamDesc), ctypes.c_int32, ctypes.c_int32, _p, _p]
         L.kvc_read_probe.argtypes = [_p, ctypes.c_size_t, _p, _p]
+        L.kvc_encode_kv.argtypes = [ctypes.POINTER(StreamDesc), ctypes.POINTER(StreamDesc), _p, ctypes.c_int64, _p,
+                                    ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, _p]
         L.kvc_last_error.restype = ctypes.c_char_p
         L.kvc_version.restype = ctypes.c_int32
         _lib = L
@@ -213,6 +215,18 @@ def kvc_encode(side: Side, x, t0: int, n_tok: int, stream=None):
     assert x.device == side.codes.device
     _check(lib().kvc_encode(ctypes.byref(side.desc), ctypes.c_void_p(x.data_ptr()), int(x.stride(0)), int(t0),
                             int(n_tok), _stream_ptr(stream)))
+
+
+def kvc_encode_kv(k: Side, v: Side, xk, xv, t0: int, n_tok: int, stream=None):
+    """Keys and values of the same tokens: xk, xv fp16 tensors (n_units, >= n_tok, d) on the device."""
+    import torch
+    for side, x in ((k, xk), (v, xv)):
+        assert x.dtype == torch.float16 and x.is_contiguous() and x.dim() == 3
+        assert x.shape[0] == side.n_units and x.shape[1] >= n_tok and x.shape[2] == HEAD_DIM
+        assert x.device == side.codes.device
+    _check(lib().kvc_encode_kv(ctypes.byref(k.desc), ctypes.byref(v.desc), ctypes.c_void_p(xk.data_ptr()),
+                               int(xk.stride(0)), ctypes.c_void_p(xv.data_ptr()), int(xv.stride(0)), int(t0),
+                               int(n_tok), _stream_ptr(stream)))
 
 
 def kvc_decode_attn_workspace(k: Side, v: Side, G: int, max_seq_len: int) -> int:

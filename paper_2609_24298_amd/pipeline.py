@@ -103,8 +103,7 @@ class Cache:
         self.V = build_side(kvc.SIDE_V, self.v_tab, w, self.capacity, device)
 
     def encode(self, xk, xv, t0: int, n_tok: int, stream=None):
-        kvc.kvc_encode(self.K, xk, t0, n_tok, stream)
-        kvc.kvc_encode(self.V, xv, t0, n_tok, stream)
+        kvc.kvc_encode_kv(self.K, self.V, xk, xv, t0, n_tok, stream)
 
     def decode_buffers(self, max_seq_len: int):
         import torch

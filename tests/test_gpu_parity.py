@@ -212,6 +212,23 @@ def test_encode_append_ragged_pieces(small):
             assert np.array_equal(c1, c2)
 
 
+def test_encode_kv_equals_per_side_encode(small):
+    # both sides in one call (one launch for the append path, the bulk encoder beyond) write exactly the
+    # bytes of two per-side kvc_encode calls, piece by piece
+    w, cache, xk, xv, _ = small
+    T = 300
+    K1, V1 = (pipeline.build_side(s, t, w, T) for s, t in ((kvc.SIDE_K, cache.k_tab), (kvc.SIDE_V, cache.v_tab)))
+    K2, V2 = (pipeline.build_side(s, t, w, T) for s, t in ((kvc.SIDE_K, cache.k_tab), (kvc.SIDE_V, cache.v_tab)))
+    for a, e in ((0, 1), (1, 3), (3, 7), (7, 64), (64, 67), (67, 200), (200, 204), (204, 300)):
+        xs_k, xs_v = xk[:, a:e].contiguous(), xv[:, a:e].contiguous()
+        kvc.kvc_encode(K1, xs_k, a, e - a)
+        kvc.kvc_encode(V1, xs_v, a, e - a)
+        kvc.kvc_encode_kv(K2, V2, xs_k, xs_v, a, e - a)
+    torch.cuda.synchronize()
+    for S1, S2 in ((K1, K2), (V1, V2)):
+        assert torch.equal(S1.codes, S2.codes)
+
+
 def _custom_side(side, Ps, deltas, rs, bs, capacity):
     flat = np.concatenate([p.reshape(-1) for p in Ps])
     offs = np.concatenate([[0], np.cumsum([p.size for p in Ps])[:-1]]).astype(np.int64)

@@ -241,3 +241,22 @@ def test_read_probe_validates_arguments_without_gpu():
     assert L.kvc_read_probe(None, 1024, fake, None) == kvc.KVC_EINVAL
     assert b"16 bytes" in L.kvc_last_error()
     assert L.kvc_read_probe(fake, 0, fake, None) == kvc.KVC_OK
+
+
+def test_encode_kv_rejects_swapped_sides_without_gpu():
+    L = kvc.lib()
+    r = np.array([4], dtype=np.int32)
+    b = np.array([3], dtype=np.int32)
+    off = np.array([0], dtype=np.int64)
+    dl = np.array([0.5], dtype=np.float32)
+    fake = ctypes.c_void_p(256)          # never dereferenced
+    dk, dv = (kvc.StreamDesc(n_units=1, d=128, capacity=64, side=side, r_host=r.ctypes.data, b_host=b.ctypes.data,
+                             code_off_host=off.ctypes.data, basis_off_host=off.ctypes.data,
+                             delta_host=dl.ctypes.data, r=fake, b=fake, code_off=fake, basis_off=fake, delta=fake,
+                             codes=fake, codes_bytes=8 * 4 * 3, basis=fake, basis_elems=4 * 128) for side in (0, 1))
+    rc = L.kvc_encode_kv(ctypes.byref(dv), ctypes.byref(dk), fake, 128, fake, 128, 0, 1, None)
+    assert rc == kvc.KVC_EINVAL and b"sides" in L.kvc_last_error()
+    rc = L.kvc_encode_kv(ctypes.byref(dk), ctypes.byref(dv), ctypes.c_void_p(258), 128, fake, 128, 0, 1, None)
+    assert rc == kvc.KVC_EINVAL and b"16-byte" in L.kvc_last_error()
+    rc = L.kvc_encode_kv(ctypes.byref(dk), ctypes.byref(dv), fake, 128, fake, 128, 60, 5, None)
+    assert rc == kvc.KVC_ENOSPACE
