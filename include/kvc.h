@@ -199,7 +199,9 @@ int kvc_encode(const kvc_stream_desc* s, const uint16_t* x, int64_t x_unit_strid
  *  q            device fp16 [n_units][G][d], 16-byte aligned: the G query
  *               heads sharing unit u's KV head (KVC_EINVAL if misaligned).
  *  seq_len      device int32 [n_units]: tokens attended per unit (each in
- *               [1, max_seq_len]).
+ *               [1, max_seq_len]). Being device data it is not validated:
+ *               values are clamped to [0, max_seq_len] on the device, and a
+ *               unit with 0 tokens gets an all-zero output.
  *  max_seq_len  host: upper bound of seq_len, <= both capacities.
  *  out          device f32 [n_units][G][d]:
  *               out[u][g] = P_V^T sum_t p_t z_V,t,

@@ -156,6 +156,24 @@ def test_small_decode_ragged_lengths(small):
         assert normwise(got[u, g], v0) <= 1e-5
 
 
+def test_small_decode_clamps_lengths(small):
+    # seq_len is device data: 0 (or negative) attends to nothing and gives zeros, values past max_seq_len
+    # attend to max_seq_len tokens
+    w, cache, xk, xv, ot = small
+    q = pipeline.draw_queries(w, cache.stats, 4, "cuda", scale=4.0)
+    n_max = 700
+    seq = np.array([0, -5, n_max + 50, n_max, 1, 3, 64, 129][: w.n_units], dtype=np.int32)
+    ws, out = cache.decode_buffers(n_max)
+    cache.decode(q, torch.as_tensor(seq, device="cuda"), n_max, out, ws)
+    got = out.cpu().numpy()
+    assert np.all(got[0] == 0.0) and np.all(got[1] == 0.0)
+    eff = np.clip(seq, 0, n_max)
+    ref = _oracle_decode(w, ot, cache, xk, xv, q, np.maximum(eff, 1))
+    for u in range(2, w.n_units):
+        for g in range(w.group):
+            assert normwise(got[u, g], ref[u, g]) <= TOL, (u, g, seq[u])
+
+
 def test_small_decode_is_deterministic(small):
     w, cache, _, _, _ = small
     q = pipeline.draw_queries(w, cache.stats, 3, "cuda")
