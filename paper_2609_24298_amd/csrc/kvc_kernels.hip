@@ -86,7 +86,7 @@ __device__ __forceinline__ bool fast_code(float acc, float err, float step, int 
 // stream layout (K: coordinate group; V: 16 coordinate rows), which are bit-packed from LDS as
 // soon as the group is decided.
 constexpr int kEncMmaThreads = 256;
-constexpr int kEncMmaTilesPerBlock = 16;
+constexpr int kEncMmaTilesPerBlock = 32;
 constexpr int kPRow = kD + 8;  // LDS row stride of the staged basis, in halves
 
 typedef _Float16 h8 __attribute__((ext_vector_type(8)));
