@@ -232,13 +232,17 @@ __global__ __launch_bounds__(kEncMmaThreads) __attribute__((amdgpu_waves_per_eu(
         const bool full = lo == tok0 && hi == tok0 + kTile;
         uint8_t* __restrict__ tbase = stream + (int64_t)tile * 8 * r * b;
 
-        // Token fragments: token 16 nt + col, dims 32 ks + 8 grp + [0, 8). Tokens outside the range
-        // read a valid token and never reach the stream.
+        // Token fragments: operand row 16 nt + col, dims 32 ks + 8 grp + [0, 8). The row holds token
+        // 16 nt + col for K; for V, token 16 nt + kidx_b(col), the token whose slot in the quarter is
+        // position col (pos_b o kidx_b = identity), so that a lane's four results (rows 4 grp + i) are
+        // four consecutive slot bytes. Tokens outside the range read a valid token and never reach the
+        // stream. etok is indexed by operand row.
         h8 xf[4][4];
         float et[4];  // ||x|| of the lane's token (NaN outside the range: such elements are never undecided)
+        const int trow = side == KVC_SIDE_K ? col : kidx_b(b, col);
 #pragma unroll
         for (int nt = 0; nt < 4; ++nt) {
-            const int tk = tok0 + 16 * nt + col;
+            const int tk = tok0 + 16 * nt + trow;
             const bool ok = tk >= lo && tk < hi;
             const h8* row = reinterpret_cast<const h8*>(xu + (int64_t)((ok ? tk : lo) - t0) * kD);
             float s2 = 0.f;
@@ -310,16 +314,9 @@ __global__ __launch_bounds__(kEncMmaThreads) __attribute__((amdgpu_waves_per_eu(
                             if (4 * grp + i < rho) sb[(16 * nt + col) * rho + 4 * grp + i] = (uint8_t)(cw[nt] >> (8 * i));
                 }
             } else if (16 * mc + col < r) {
-                // tokens 16 nt + 4 grp + i of coordinate row col; quarter nt holds them in the order pos_b
-                if (b == 8) {
+                // operand rows 16 nt + 4 grp + i of coordinate row col: slot positions 4 grp + i of quarter nt
 #pragma unroll
-                    for (int nt = 0; nt < 4; ++nt) *reinterpret_cast<uint32_t*>(sb + 64 * col + 16 * nt + 4 * grp) = cw[nt];
-                } else {
-#pragma unroll
-                    for (int nt = 0; nt < 4; ++nt)
-#pragma unroll
-                        for (int i = 0; i < 4; ++i) sb[64 * col + 16 * nt + pos_b(b, 4 * grp + i)] = (uint8_t)(cw[nt] >> (8 * i));
-                }
+                for (int nt = 0; nt < 4; ++nt) *reinterpret_cast<uint32_t*>(sb + 64 * col + 16 * nt + 4 * grp) = cw[nt];
             }
             // undecided elements (rare): flag them again per lane, then the whole wavefront settles
             // them one by one
@@ -344,19 +341,21 @@ __global__ __launch_bounds__(kEncMmaThreads) __attribute__((amdgpu_waves_per_eu(
                         const int bit = __builtin_ctz(m);
                         m &= m - 1;
                         const int nt = bit >> 2, i = bit & 3;
-                        int tkn, c, sl;
+                        int tkn, c, sl, row;  // token, coordinate, slot, operand row of the element
                         if constexpr (side == KVC_SIDE_K) {
                             tkn = 16 * nt + Lcol;
+                            row = tkn;
                             c = 16 * mc + 4 * Lgrp + i;
                             sl = tailg ? tkn * rho + 4 * Lgrp + i : 16 * tkn + 4 * Lgrp + i;
                         } else {
-                            tkn = 16 * nt + 4 * Lgrp + i;
+                            row = 16 * nt + 4 * Lgrp + i;
+                            tkn = 16 * nt + kidx_b(b, 4 * Lgrp + i);
                             c = 16 * mc + Lcol;
-                            sl = 64 * Lcol + 16 * nt + pos_b(b, 4 * Lgrp + i);
+                            sl = 64 * Lcol + row;
                         }
                         const uint16_t* xrow = xu + (int64_t)(tok0 + tkn - t0) * kD;
                         const uint32_t code = resolve_code_wave(Pl + c * kPRow, Pg + (int64_t)c * kD, xrow, step, b,
-                                                                pnrm[c], etok[tkn], lane);
+                                                                pnrm[c], etok[row], lane);
                         if (lane == 0) sb[sl] = (uint8_t)code;
                     }
                 }
