@@ -45,17 +45,22 @@ def softmax(s: np.ndarray) -> np.ndarray:
     return e / np.sum(e, axis=-1, keepdims=True)
 
 
+def decode_logits(codes_k, Pk_bits, step_k, b_k, q_bits, seq_len):
+    """Logits s[g, t] = (P_K q_g) . z_K,t / sqrt(d) of the first seq_len tokens (G x seq_len), in nats."""
+    q = fp16_to_f64(q_bits)
+    d = q.shape[1]
+    zk = dequantize(codes_k[:seq_len], step_k, b_k)
+    qt = q @ fp16_to_f64(Pk_bits).T                 # G x r_K
+    return (qt @ zk.T) / math.sqrt(d)
+
+
 def decode_attention(codes_k, codes_v, Pk_bits, Pv_bits, step_k, step_v, b_k, b_v, q_bits, seq_len):
     """One decode step for one unit: out[g] = P_V^T sum_t p_gt z_V,t with p = softmax((P_K q_g) . z_K,t / sqrt(d)).
 
     codes_*: (T x r) uint8, only the first seq_len tokens are attended; q_bits: (G x d) fp16 bits.
     """
-    q = fp16_to_f64(q_bits)
-    d = q.shape[1]
-    zk = dequantize(codes_k[:seq_len], step_k, b_k)
+    s = decode_logits(codes_k, Pk_bits, step_k, b_k, q_bits, seq_len)
     zv = dequantize(codes_v[:seq_len], step_v, b_v)
-    qt = q @ fp16_to_f64(Pk_bits).T                 # G x r_K
-    s = (qt @ zk.T) / math.sqrt(d)                   # G x T
     p = softmax(s)
     zbar = p @ zv                                    # G x r_V
     return zbar @ fp16_to_f64(Pv_bits)               # G x d

@@ -14,7 +14,7 @@
  *   k_i = clamp(floor(y_i / step) + 2^(b-1), 0, 2^b - 1), exactly.
  * The packed layout is the one documented in oracle/layout.py.
  *
- * Build: gcc -O2 -ffp-contract=off -fPIC -shared (no fast-math).
+ * Build: gcc -O2 -ffp-contract=off -fopenmp -fPIC -shared (no fast-math).
  */
 #include <stdint.h>
 #include <string.h>
@@ -52,6 +52,9 @@ int oracle_encode_codes(const uint16_t *P, int r, int d, float step, int b,
     if (step_units(step, &D)) return -1;
     const int64_t h = (int64_t)1 << (b - 1);
     const int64_t kmax = ((int64_t)1 << b) - 1;
+    int bad = 0;
+    /* tokens are independent: spread over threads (no effect on any value) */
+#pragma omp parallel for schedule(static) reduction(|: bad)
     for (int t = 0; t < n; ++t) {
         const uint16_t *xt = x + (int64_t)t * d;
         for (int i = 0; i < r; ++i) {
@@ -59,7 +62,7 @@ int oracle_encode_codes(const uint16_t *P, int r, int d, float step, int b,
             i128 N = 0;
             for (int j = 0; j < d; ++j) {
                 int64_t mp, mx; int ep, exx;
-                if (half_parts(Pi[j], &mp, &ep) || half_parts(xt[j], &mx, &exx)) return -1;
+                if (half_parts(Pi[j], &mp, &ep) || half_parts(xt[j], &mx, &exx)) { bad = 1; mp = mx = 0; ep = exx = -24; }
                 int s = ep + exx + 48;              /* 0 .. 58 */
                 N += (i128)(mp * mx) * ((i128)1 << s);  /* exact, no overflow */
             }
@@ -71,7 +74,7 @@ int oracle_encode_codes(const uint16_t *P, int r, int d, float step, int b,
             codes[(int64_t)t * r + i] = (uint8_t)k;
         }
     }
-    return 0;
+    return bad ? -1 : 0;
 }
 
 static int n_planes(int b, int *w) {
@@ -150,4 +153,95 @@ void oracle_unpack(const uint8_t *stream, int n, int r, int b, int side, uint8_t
             codes[(int64_t)tok * r + i] = (uint8_t)c;
         }
     }
+}
+
+/*
+ * Calibration, table step 1: eigendecomposition of a symmetric d x d matrix S
+ * (row-major, fp64) by the cyclic-by-row Jacobi method (Golub and Van Loan,
+ * Matrix Computations, Sec. 8.5: the symmetric Schur decomposition of each
+ * 2 x 2 pivot block annihilates a_pq; A <- J^T A J, V <- V J).
+ * A rotation is skipped when |a_pq| <= 2^-60 sqrt(|a_pp a_qq|) (or a_pq = 0);
+ * the iteration ends after a sweep with no rotation, or after 60 sweeps.
+ * Outputs, in the calibration reading of the oracle: eigenvalues in descending
+ * order (ties keep the diagonal index order), negative ones clamped to 0;
+ * U[j*d + k] = component j of eigenvector k; each eigenvector's entry of
+ * largest magnitude (the first such) made positive.
+ * Returns the number of sweeps, or -1 if it did not converge.
+ */
+#include <math.h>
+#include <stdlib.h>
+
+static int jacobi_one(const double *S, int d, double *lam, double *U, double *A, double *V, int *idx) {
+    for (int i = 0; i < d * d; ++i) A[i] = S[i];
+    for (int i = 0; i < d; ++i)
+        for (int j = 0; j < d; ++j) V[i * d + j] = (i == j) ? 1.0 : 0.0;
+    int sweeps = 0, converged = 0;
+    while (sweeps < 60) {
+        int rotated = 0;
+        for (int p = 0; p < d - 1; ++p) {
+            for (int q = p + 1; q < d; ++q) {
+                const double apq = A[p * d + q];
+                if (apq == 0.0 || fabs(apq) <= ldexp(sqrt(fabs(A[p * d + p]) * fabs(A[q * d + q])), -60)) continue;
+                rotated = 1;
+                const double theta = (A[q * d + q] - A[p * d + p]) / (2.0 * apq);
+                const double t = (theta >= 0.0 ? 1.0 : -1.0) / (fabs(theta) + sqrt(1.0 + theta * theta));
+                const double c = 1.0 / sqrt(1.0 + t * t);
+                const double s = t * c;
+                for (int k = 0; k < d; ++k) {  /* columns p, q: A <- A J */
+                    const double akp = A[k * d + p], akq = A[k * d + q];
+                    A[k * d + p] = c * akp - s * akq;
+                    A[k * d + q] = s * akp + c * akq;
+                }
+                for (int k = 0; k < d; ++k) {  /* rows p, q: A <- J^T A */
+                    const double apk = A[p * d + k], aqk = A[q * d + k];
+                    A[p * d + k] = c * apk - s * aqk;
+                    A[q * d + k] = s * apk + c * aqk;
+                }
+                A[p * d + q] = A[q * d + p] = 0.0;
+                for (int k = 0; k < d; ++k) {  /* V <- V J */
+                    const double vkp = V[k * d + p], vkq = V[k * d + q];
+                    V[k * d + p] = c * vkp - s * vkq;
+                    V[k * d + q] = s * vkp + c * vkq;
+                }
+            }
+        }
+        ++sweeps;
+        if (!rotated) { converged = 1; break; }
+    }
+    /* descending order, stable (insertion sort on the diagonal index) */
+    for (int i = 0; i < d; ++i) idx[i] = i;
+    for (int i = 1; i < d; ++i) {
+        const int v = idx[i];
+        int j = i - 1;
+        while (j >= 0 && A[idx[j] * d + idx[j]] < A[v * d + v]) { idx[j + 1] = idx[j]; --j; }
+        idx[j + 1] = v;
+    }
+    for (int k = 0; k < d; ++k) {
+        const int src = idx[k];
+        const double l = A[src * d + src];
+        lam[k] = l > 0.0 ? l : 0.0;
+        int jm = 0;
+        for (int j = 1; j < d; ++j)
+            if (fabs(V[j * d + src]) > fabs(V[jm * d + src])) jm = j;
+        const double sg = V[jm * d + src] < 0.0 ? -1.0 : 1.0;
+        for (int j = 0; j < d; ++j) U[j * d + k] = sg * V[j * d + src];
+    }
+    return converged ? sweeps : -1;
+}
+
+/* n matrices S[n][d][d] -> lam[n][d], U[n][d][d]; sweeps[n] as jacobi_one returns. Matrices are
+ * independent: spread over threads. Returns 0, or -1 if any did not converge. */
+int oracle_jacobi_eigh(const double *S, int n, int d, double *lam, double *U, int *sweeps) {
+    int bad = 0;
+#pragma omp parallel for schedule(dynamic) reduction(|: bad)
+    for (int h = 0; h < n; ++h) {
+        double *A = (double *)malloc(sizeof(double) * d * d);
+        double *V = (double *)malloc(sizeof(double) * d * d);
+        int *idx = (int *)malloc(sizeof(int) * d);
+        const int s = jacobi_one(S + (int64_t)h * d * d, d, lam + (int64_t)h * d, U + (int64_t)h * d * d, A, V, idx);
+        sweeps[h] = s;
+        if (s < 0) bad = 1;
+        free(A); free(V); free(idx);
+    }
+    return bad ? -1 : 0;
 }

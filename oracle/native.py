@@ -17,10 +17,10 @@ _lib = None
 
 
 def build(force: bool = False) -> str:
-    """Compile the C oracle with gcc (plain -O2, no FMA contraction, no fast-math)."""
+    """Compile the C oracle with gcc (plain -O2, no FMA contraction, no fast-math; OpenMP over tokens)."""
     if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
         tmp = _LIB + ".tmp%d" % os.getpid()
-        subprocess.check_call(["gcc", "-O2", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared",
+        subprocess.check_call(["gcc", "-O2", "-ffp-contract=off", "-fno-fast-math", "-fopenmp", "-fPIC", "-shared",
                                "-o", tmp, _SRC])
         os.replace(tmp, _LIB)
     return _LIB
@@ -40,6 +40,9 @@ def _load():
         lib.oracle_pack.restype = None
         lib.oracle_unpack.argtypes = [u8p, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, u8p]
         lib.oracle_unpack.restype = None
+        f64p = ctypes.POINTER(ctypes.c_double)
+        lib.oracle_jacobi_eigh.argtypes = [f64p, ctypes.c_int, ctypes.c_int, f64p, f64p, ctypes.POINTER(ctypes.c_int)]
+        lib.oracle_jacobi_eigh.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -77,3 +80,21 @@ def unpack(stream: np.ndarray, n: int, r: int, b: int, side: int) -> np.ndarray:
     out = np.zeros((n, r), dtype=np.uint8)
     _load().oracle_unpack(_ptr(stream, ctypes.c_uint8), n, r, b, side, _ptr(out, ctypes.c_uint8))
     return out
+
+
+def jacobi_eigh(S: np.ndarray):
+    """Eigendecomposition of symmetric matrices S (n x d x d, or one d x d) by cyclic Jacobi in fp64:
+    (eigenvalues descending, eigenvectors as columns with their largest entry positive, sweeps)."""
+    S = np.ascontiguousarray(S, dtype=np.float64)
+    one = S.ndim == 2
+    if one:
+        S = S[None]
+    n, d, _ = S.shape
+    lam = np.zeros((n, d))
+    U = np.zeros((n, d, d))
+    sw = np.zeros(n, dtype=np.int32)
+    rc = _load().oracle_jacobi_eigh(_ptr(S, ctypes.c_double), n, d, _ptr(lam, ctypes.c_double),
+                                    _ptr(U, ctypes.c_double), _ptr(sw, ctypes.c_int))
+    if rc != 0:
+        raise ValueError("oracle Jacobi: no convergence within 60 sweeps")
+    return (lam[0], U[0], int(sw[0])) if one else (lam, U, sw)

@@ -9,8 +9,12 @@
 //  * codes enter as int8 (raw codes for b <= 7; c - 128 for b = 8);
 //  * the rank-space query q~ = P_K q is split into three balanced base-254
 //    int8 limbs with a per-query scale (relative error ~1e-7 of max|q~|);
-//  * the softmax weights p in [0, 2^6] are quantised to P < 2^23 and split into
-//    three signed byte limbs, P = S0 + 2^8 S1 + 2^16 S2;
+//  * the softmax weights p in [0, 2^6] (relative to the chunk's running max) are
+//    quantised to P < 2^31 - 2^24 and split into four byte limbs,
+//    P = S0 + 2^8 S1 + 2^16 S2 + 2^24 S3 (S0..S2 signed, S3 in [0, 127]). The
+//    quantum is 2^-25 of the running max, so a chunk of n tokens loses at most
+//    n 2^-26 of its mass to rounding (<= 2^-12 at the longest chunk, 2^14
+//    tokens), whatever the shape of the attention;
 //  * centring (c - 2^(b-1)) is exact in integers: the logits subtract
 //    2^(b-1) sum_i Q_i, and the value accumulator carries an all-ones virtual
 //    coordinate whose column gives sum_t P_t (also the softmax denominator).
@@ -46,10 +50,12 @@ constexpr int kTile = KVC_TILE_TOKENS;
 constexpr int kPartStride = 132;  // floats per (item, query head): m, l, pad, pad, acc[128]
 constexpr int kLimbs = 3;
 constexpr float kLazy = 6.f;              // the running max is raised only when a tile beats it by > 2^6
-constexpr float kPScale = 130047.96875f;  // (2^23 - 2^16 - 2) / 2^6: p <= 2^6 maps to P < 2^23 - 2^16
-constexpr float kPBias = 32896.5f;        // 0x8080 (offsets of the two signed low limbs) + 1/2 (rounding)
-// Tiles per chunk at most: |S_l c| <= 2^14 per token keeps the int32 accumulators below 2^31
-// (2^28 per chunk, plus at most 2^29 carried by a rescale).
+constexpr float kPScale = 33292288.f;     // (2^31 - 2^24) / 2^6: p <= 2^6 maps to P <= 2^31 - 2^24
+constexpr float kPBias = 8421504.f;       // 0x808080, the offsets of the three signed low limbs; the fma's
+                                          // result is >= 2^23, so its rounding to nearest is the rounding of P
+// Tiles per chunk at most: |S_l c| <= 2^15 per token keeps the int32 accumulators below 2^31
+// (2^29 per chunk, plus at most 2^24 carried into a limb by a rescale), and bounds the rounding
+// loss of a chunk's softmax mass (see kPScale).
 constexpr int kMaxChunkTiles = 256;
 constexpr int kPRowBytes = 80;            // LDS row of the probability limbs (64 tokens + pad)
 constexpr uint32_t kLaneOOB = 0x10000000u;  // lane offset (in plane-width units) past any stream
@@ -795,9 +801,9 @@ __device__ __attribute__((always_inline)) void run_item(const DevSide& K, const 
 #pragma unroll
             for (int lm = 0; lm < LM; ++lm) mx[lm] = row_max(ml[lm]);
             // Raise the max of each head whose tile beats it by more than 2^kLazy (every head on the
-            // first tile) to the tile's own max, and rescale that head's accumulators exactly (every
-            // limb of a (head, coordinate) sits in this lane): value = C0 + 2^8 C1 + 2^16 C2 ->
-            // rint(value alpha), split again.
+            // first tile) to the tile's own max, and rescale that head's accumulators (every limb of a
+            // (head, coordinate) sits in this lane): value = C0 + 2^8 C1 + 2^16 C2 + 2^24 C3 (exact in
+            // fp64: |value| <= 2^53) -> rint(value alpha), split again into C3 and three bytes.
 #pragma unroll
             for (int lm = 0; lm < LM; ++lm) {
                 if ((first && mx[lm] > -INFINITY) || mx[lm] > kLazy) {
@@ -813,22 +819,26 @@ __device__ __attribute__((always_inline)) void run_item(const DevSide& K, const 
                         const double a = (double)alpha;
 #pragma unroll
                         for (int nt = 0; nt < 9; ++nt) {
-                            const double v = (double)C[lm][nt][0] + 256.0 * (double)C[lm][nt][1] + 65536.0 * (double)C[lm][nt][2];
+                            const double v = ((double)C[lm][nt][0] + 256.0 * (double)C[lm][nt][1]) +
+                                             (65536.0 * (double)C[lm][nt][2] + 16777216.0 * (double)C[lm][nt][3]);
                             const double vs = rint(v * a);
-                            const double c2 = floor(vs * (1.0 / 65536.0));
-                            const double rem = vs - 65536.0 * c2;
-                            const double c1 = floor(rem * (1.0 / 256.0));
+                            const double c3 = floor(vs * (1.0 / 16777216.0));
+                            const double r3 = vs - 16777216.0 * c3;  // [0, 2^24): exact from here on
+                            const double c2 = floor(r3 * (1.0 / 65536.0));
+                            const double r2 = r3 - 65536.0 * c2;
+                            const double c1 = floor(r2 * (1.0 / 256.0));
+                            C[lm][nt][3] = (int)c3;
                             C[lm][nt][2] = (int)c2;
                             C[lm][nt][1] = (int)c1;
-                            C[lm][nt][0] = (int)(rem - 256.0 * c1);
+                            C[lm][nt][0] = (int)(r2 - 256.0 * c1);
                         }
                     }
                 }
             }
         }
 
-        // ---- probability limbs: P'' = round(p kPScale) + 0x8080; bytes 0, 1 (xor 0x80) and 2 are
-        // the signed limbs S0, S1, S2 with P = S0 + 2^8 S1 + 2^16 S2. Row 4 h + limb, bytes 4 col + st.
+        // ---- probability limbs: P'' = round(p kPScale) + 0x808080; bytes 0, 1, 2 (xor 0x80) and 3 are
+        // the limbs S0..S3 with P = S0 + 2^8 S1 + 2^16 S2 + 2^24 S3. Row 4 h + limb, bytes 4 col + st.
 #pragma unroll
         for (int lm = 0; lm < LM; ++lm) {
             uint32_t P[4];
@@ -836,15 +846,17 @@ __device__ __attribute__((always_inline)) void run_item(const DevSide& K, const 
             for (int st = 0; st < 4; ++st)
                 P[st] = (uint32_t)fmaf(__builtin_amdgcn_exp2f(s[lm][st]), kPScale, kPBias);
             const uint32_t q01 = perm(P[1], P[0], 0x05010400u), q23 = perm(P[3], P[2], 0x05010400u);
-            const uint32_t r01 = perm(P[1], P[0], 0x00000602u), r23 = perm(P[3], P[2], 0x00000602u);
+            const uint32_t r01 = perm(P[1], P[0], 0x07030602u), r23 = perm(P[3], P[2], 0x07030602u);
             const uint32_t L0 = perm(q23, q01, 0x05040100u) ^ 0x80808080u;
             const uint32_t L1 = perm(q23, q01, 0x07060302u) ^ 0x80808080u;
-            const uint32_t L2 = perm(r23, r01, 0x05040100u);
+            const uint32_t L2 = perm(r23, r01, 0x05040100u) ^ 0x80808080u;
+            const uint32_t L3 = perm(r23, r01, 0x07060302u);
             // every lane writes (heads past G have -inf logits, so zero limbs): no divergent LDS writes
             uint8_t* row = pmat + (16 * lm + 4 * grp) * kPRowBytes + 4 * col;
             *reinterpret_cast<uint32_t*>(row) = L0;
             *reinterpret_cast<uint32_t*>(row + kPRowBytes) = L1;
             *reinterpret_cast<uint32_t*>(row + 2 * kPRowBytes) = L2;
+            *reinterpret_cast<uint32_t*>(row + 3 * kPRowBytes) = L3;
         }
         wave_lds_sync();
         v4i ap[LM];
@@ -884,19 +896,21 @@ __device__ __attribute__((always_inline)) void run_item(const DevSide& K, const 
     for (int pm = 0; pm < LM; ++pm) {
         const int h = 4 * pm + grp;
         const int o0 = __shfl(C[pm][8][0], lane & 48), o1 = __shfl(C[pm][8][1], lane & 48),
-                  o2 = __shfl(C[pm][8][2], lane & 48);
+                  o2 = __shfl(C[pm][8][2], lane & 48), o3 = __shfl(C[pm][8][3], lane & 48);
         if (G % 4 == 0 || h < G) {
             float* o = out + h * kPartStride;
             if (col == 0) {
                 o[0] = mrun[pm];
-                o[1] = (float)o0 + 256.f * (float)o1 + 65536.f * (float)o2;
+                o[1] = ((float)o0 + 256.f * (float)o1) + (65536.f * (float)o2 + 16777216.f * (float)o3);
             }
 #pragma unroll
             for (int nt = 0; nt < 8; ++nt) {
                 const int cc = 16 * nt + col;
                 if (nt < nv) {
-                    const int a0 = C[pm][nt][0] - hv * o0, a1 = C[pm][nt][1] - hv * o1, a2 = C[pm][nt][2] - hv * o2;
-                    o[4 + cc] = cc < rv ? (float)a0 + 256.f * (float)a1 + 65536.f * (float)a2 : 0.f;
+                    const int a0 = C[pm][nt][0] - hv * o0, a1 = C[pm][nt][1] - hv * o1, a2 = C[pm][nt][2] - hv * o2,
+                              a3 = C[pm][nt][3] - hv * o3;
+                    o[4 + cc] = cc < rv ? ((float)a0 + 256.f * (float)a1) + (65536.f * (float)a2 + 16777216.f * (float)a3)
+                                        : 0.f;
                 }
             }
         }

@@ -1,0 +1,127 @@
+"""GPU parity of decode attention and reconstruction over every pair of code widths.
+
+The allocator's tables at the measured budgets reach only part of the (b_K, b_V) plane, so this test
+builds its own tables: 64 width pairs (b_K, b_V) in {1..8}^2, each on 8 units whose ranks cycle
+through {2, 6, 14, 18, 64, 66, 84, 96, 126, 128} (ranks with and without a tail group of r mod 16
+coordinates, one and two 64-coordinate K-steps, value N-tiles from 1 to 8). Bases are random
+orthonormal rows rounded to fp16, steps scaled to each width. 512 units of 4133 tokens split into
+multi-tile context chunks with a ragged last tile. One cache is decoded with every query-group size
+G in {1, 2, 4, 8, 16} (the streams do not depend on G) and checked unit by unit against the oracle's
+fp64 decode from its own codes; reconstruction of a token range is checked for every unit.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from oracle import attention as oatt
+from oracle import native as onat
+from paper_2609_24298_amd import kvc
+
+from test_gpu_parity import TOL, normwise
+
+pytestmark = pytest.mark.gpu
+
+RANKS = (2, 6, 14, 18, 64, 66, 84, 96, 126, 128)
+REPS = 8
+T = 4133
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def _table():
+    rows = []
+    for i, (bk, bv) in enumerate((bk, bv) for bk in range(1, 9) for bv in range(1, 9)):
+        for j in range(REPS):
+            rows.append((RANKS[(i + j) % 10], bk, RANKS[(i + 3 * j + 5) % 10], bv))
+    return rows
+
+
+def _side(side, rows, rng):
+    Ps, ds = [], []
+    for rk, bk, rv, bv in rows:
+        r, b = (rk, bk) if side == kvc.SIDE_K else (rv, bv)
+        Q, _ = np.linalg.qr(rng.standard_normal((128, 128)))
+        Ps.append(Q[:r].astype(np.float16).view(np.uint16))
+        ds.append(np.float32(rng.uniform(0.6, 1.2) * 1.596 / 2 ** (b - 1) * 0.6))
+    rs = [row[0] if side == kvc.SIDE_K else row[2] for row in rows]
+    bs = [row[1] if side == kvc.SIDE_K else row[3] for row in rows]
+    flat = np.concatenate([p.reshape(-1) for p in Ps])
+    offs = np.concatenate([[0], np.cumsum([p.size for p in Ps])[:-1]]).astype(np.int64)
+    return kvc.Side(side, rs, bs, np.array(ds, np.float32), flat, offs, T), Ps, ds
+
+
+@pytest.fixture(scope="module")
+def width_cache():
+    rows = _table()
+    rng = np.random.default_rng(31)
+    K, Pk, dk = _side(kvc.SIDE_K, rows, rng)
+    V, Pv, dv = _side(kvc.SIDE_V, rows, rng)
+    U = len(rows)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(4133)
+    xk = (torch.randn((U, T, 128), generator=gen, device="cuda") * 0.6).to(torch.float16)
+    xv = (torch.randn((U, T, 128), generator=gen, device="cuda") * 0.6).to(torch.float16)
+    log(f"[widths] encode {U} units x {T} tokens")
+    kvc.kvc_encode_kv(K, V, xk, xv, 0, T)
+    torch.cuda.synchronize()
+    xkb = xk.view(torch.int16).cpu().numpy().view(np.uint16)
+    xvb = xv.view(torch.int16).cpu().numpy().view(np.uint16)
+    codes = []
+    for u, (rk, bk, rv, bv) in enumerate(rows):
+        ck = onat.encode_codes(Pk[u], dk[u], bk, xkb[u])
+        cv = onat.encode_codes(Pv[u], dv[u], bv, xvb[u])
+        assert np.array_equal(K.unit_codes(u, T).cpu().numpy(), onat.pack(ck, rk, bk, kvc.SIDE_K)), (u, rk, bk)
+        assert np.array_equal(V.unit_codes(u, T).cpu().numpy(), onat.pack(cv, rv, bv, kvc.SIDE_V)), (u, rv, bv)
+        codes.append((ck, cv))
+    log("[widths] streams bit-exact for every unit")
+    return rows, K, V, Pk, dk, Pv, dv, codes
+
+
+@pytest.mark.parametrize("G", [1, 2, 4, 8, 16])
+def test_decode_every_width_pair(width_cache, G):
+    rows, K, V, Pk, dk, Pv, dv, codes = width_cache
+    U = len(rows)
+    rng = np.random.default_rng(100 + G)
+    q = (rng.standard_normal((U, G, 128)) * 1.5).astype(np.float16)
+    qt = torch.as_tensor(q.view(np.int16), device="cuda").view(torch.float16)
+    # lengths: most units attend over everything, some over ragged prefixes
+    seq = np.full(U, T, dtype=np.int32)
+    seq[::7] = rng.integers(1, T, size=len(seq[::7]))
+    nbytes = kvc.kvc_decode_attn_workspace(K, V, G, T)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    out = torch.empty((U, G, 128), dtype=torch.float32, device="cuda")
+    log(f"[widths G={G}] decode")
+    kvc.kvc_decode_attn(K, V, qt, G, torch.as_tensor(seq, device="cuda"), T, out, ws)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    worst = {}
+    for u, (rk, bk, rv, bv) in enumerate(rows):
+        ck, cv = codes[u]
+        ref = oatt.decode_attention(ck, cv, Pk[u], Pv[u], dk[u], dv[u], bk, bv, q[u].view(np.uint16), int(seq[u]))
+        for g in range(G):
+            e = normwise(got[u, g], ref[g])
+            worst[(bk, bv)] = max(worst.get((bk, bv), 0.0), e)
+            assert e <= TOL, (G, u, (rk, bk, rv, bv), g, e)
+    log(f"[widths G={G}] 64 width pairs, max normwise error {max(worst.values()):.2e}")
+
+
+def test_reconstruct_every_width(width_cache):
+    rows, K, V, Pk, dk, Pv, dv, codes = width_cache
+    U = len(rows)
+    t0, n = 1000, 1100
+    for side, S, P, dl in ((kvc.SIDE_K, K, Pk, dk), (kvc.SIDE_V, V, Pv, dv)):
+        out = torch.empty((U, n, 128), dtype=torch.float32, device="cuda")
+        kvc.kvc_reconstruct(S, t0, n, out)
+        torch.cuda.synchronize()
+        got = out.cpu().numpy()
+        for u, row in enumerate(rows):
+            b = row[1] if side == kvc.SIDE_K else row[3]
+            c = codes[u][side][t0:t0 + n]
+            ref = oatt.reconstruct(c, P[u], dl[u], b)
+            assert normwise(got[u], ref) <= 1e-5, (side, u, row)
+        log(f"[widths] reconstruct side {'KV'[side]}: every unit within 1e-5")
