@@ -151,3 +151,39 @@ def test_allocate_c1_only_and_infeasible_fallback():
     o = oa.AllocOpts(d=16, bpd=0.05, solver=oa.SOLVER_C1_ONLY)   # B = 0.8 < r_min * b_min
     out = oa.allocate([power_law(16, 1.0)], None, o)
     assert out["r"][0] == 2 and out["b"][0] == 1
+
+
+# ---------------------------------------------------------------- C2 update, worked by hand
+#
+# Three heads, d = 4 (ranks 2 and 4), bpd = 1: B_h = 4 at the start, B_tot = 12, B_bar = 4,
+# eta B_bar = 1.2. Weights: A = (192, 0, 0, 0), B = (6, 6, 6, 6), C = (48, 0, 0, 0).
+# C1 by hand (q(b) = 4^-b / 12, b = floor(B_h / r)):
+#   A, C (one nonzero weight): r = 2 always wins, D = w_1 q(floor(B/2));
+#   B (flat): for B_h in [4, 8) r = 4, b = 1, D = 24/48 = 0.5; for B_h in [2, 4) only r = 2 is
+#   feasible, b = 1, D = 12 + 12/48 = 12.25.
+# Round 1 (B = 4, 4, 4): D = (1, 0.5, 0.25), D_bar = 7/12;
+#   B'_h = 4 + 1.2 (sqrt(D_h / D_bar) - 1) = 4 + 1.2 (sqrt(12/7), sqrt(6/7), sqrt(3/7)) - 1.2,
+#   then B_h = B'_h * 12 / sum B'.
+# Round 2 at those budgets (4.42, 3.95, 3.63): D = (1, 12.25, 1), D_bar = 4.75; each head moves by
+#   1.2 (sqrt(D_h / 4.75) - 1) from its own budget (eta times the mean budget, not its own), C falls
+#   to 2.976, which the floor B_min = 3 (second case) raises to 3 before renormalising.
+# Final C1: A (r, b) = (2, 1), B = (4, 1), C = (2, 1). The literals below are those numbers to 16
+# digits; a dropped square root, eta B_h for eta B_bar, renormalising before the clamp or a missing
+# clamp each change them in the third digit or earlier.
+C2_HAND = {
+    (1, 2.0): [4.419884282818997, 3.9545709611535416, 3.6255447560274607],
+    (2, 2.0): [3.9591044405021916, 4.9158683300781805, 3.1250272294196257],
+    (2, 3.0): [3.950856704883234, 4.905627432690046, 3.1435158624267183],
+}
+
+
+@pytest.mark.parametrize("rounds,B_min", sorted(C2_HAND))
+def test_c2_damped_update_worked_by_hand(rounds, B_min):
+    o = oa.AllocOpts(d=4, bpd=1.0, rounds=rounds, B_min=B_min)
+    W = [[192.0, 0.0, 0.0, 0.0], [6.0] * 4, [48.0, 0.0, 0.0, 0.0]]
+    B, allocs = oa.c2_damped(W, o)
+    assert np.allclose(B, C2_HAND[(rounds, B_min)], rtol=1e-14, atol=0)
+    assert abs(sum(B) - 12.0) < 1e-12
+    if rounds == 2:
+        assert [(a[0], a[1]) for a in allocs] == [(2, 1), (4, 1), (2, 1)]
+        assert [a[2] for a in allocs] == pytest.approx([4.0, 0.5, 1.0], rel=1e-15)
