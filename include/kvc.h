@@ -221,6 +221,28 @@ int kvc_decode_attn(const kvc_stream_desc* k, const kvc_stream_desc* v, const ui
 size_t kvc_decode_attn_workspace(const kvc_stream_desc* k, const kvc_stream_desc* v,
                                  int32_t G, int32_t max_seq_len);
 
+/* Size of the library's own decode workspace (see kvc_decode_attn_noalloc): 64 MiB per GPU. */
+#define KVC_NOALLOC_SCRATCH_BYTES (64ll << 20)
+
+/*
+ * kvc_decode_attn_noalloc - kvc_decode_attn without a caller workspace and without any allocation.
+ * For callers that cannot allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc). Same kernels, arguments, results and errors as kvc_decode_attn,
+ * except that the workspace is a fixed array inside the library: KVC_NOALLOC_SCRATCH_BYTES bytes of
+ * device memory on each GPU the library runs on, held from the library's load until the process ends
+ * (its address is looked up once per device, on the first call with that device current).
+ *  - KVC_ENOSPACE if these descriptors need more workspace than that (kvc_decode_attn_workspace gives
+ *    the need; the measured workloads need at most ~45 MiB).
+ *  - Calls no hipMalloc, hipFree or allocating library routine.
+ *  - Every call on one GPU uses the same array: calls that overlap on one GPU (two streams, or two
+ *    host threads without ordering) race and give undefined results. Calls ordered on one stream are
+ *    safe. The array's contents on entry are ignored (every byte a call reads it wrote first).
+ * Async on `stream`.
+ */
+int kvc_decode_attn_noalloc(const kvc_stream_desc* k, const kvc_stream_desc* v, const uint16_t* q,
+                            int32_t G, const int32_t* seq_len, int32_t max_seq_len, float* out,
+                            void* stream);
+
 /*
  * kvc_encode_kv - kvc_encode of the keys and the values of the same tokens in one call.
  * Paper: table step 7-8 (a decode step caches the new token's key and value). For

@@ -39,6 +39,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdint>
+#include <mutex>
 
 #include "kvc_device.h"
 #include "kvc_internal.h"
@@ -1282,19 +1283,13 @@ extern "C" size_t kvc_decode_attn_workspace(const kvc_stream_desc* k, const kvc_
     return (size_t)ws_layout(k, G, max_seq_len).total;
 }
 
-extern "C" int kvc_decode_attn(const kvc_stream_desc* k, const kvc_stream_desc* v, const uint16_t* q, int32_t G,
-                               const int32_t* seq_len, int32_t max_seq_len, float* out, void* ws, size_t ws_bytes,
-                               void* stream) {
-    clear_error();
-    if (int e = decode_check(k, v, G, max_seq_len)) return e;
-    if (k->n_units == 0) return KVC_OK;
-    if (!q || !seq_len || !out || !ws) return set_error(KVC_EINVAL, "kvc_decode_attn: null pointer");
-    if (reinterpret_cast<uintptr_t>(q) & 15) return set_error(KVC_EINVAL, "kvc_decode_attn: q not 16-byte aligned");
-    if (reinterpret_cast<uintptr_t>(ws) & 255) return set_error(KVC_EINVAL, "kvc_decode_attn: workspace not 256-byte aligned");
+namespace kvc {
+namespace {
+
+// Launches of one decode step into the workspace ws (validated by the caller, of layout L).
+int decode_launch(const kvc_stream_desc* k, const kvc_stream_desc* v, const uint16_t* q, int32_t G,
+                  const int32_t* seq_len, int32_t max_seq_len, float* out, void* ws, const WsLayout& L, void* stream) {
     const int U = k->n_units;
-    const WsLayout L = ws_layout(k, G, max_seq_len);
-    if ((int64_t)ws_bytes < L.total)
-        return set_error(KVC_ENOSPACE, "kvc_decode_attn: workspace %zu < %lld bytes", ws_bytes, (long long)L.total);
     char* w = reinterpret_cast<char*>(ws);
     v4i* qa = reinterpret_cast<v4i*>(w + L.qa);
     float4* qk = reinterpret_cast<float4*>(w + L.qk);
@@ -1330,6 +1325,75 @@ extern "C" int kvc_decode_attn(const kvc_stream_desc* k, const kvc_stream_desc* 
         default: launch_combine<16>(cw, dim3(U), cblk, csm, st, V, L.n_chunks, part, out); break;
     }
     return check_launch("kvc_decode_attn");
+}
+
+// Checks shared by both decode entry points (pointers and alignment; the descriptors are checked by
+// decode_check).
+int decode_args(const char* fn, const uint16_t* q, const int32_t* seq_len, const float* out) {
+    if (!q || !seq_len || !out) return set_error(KVC_EINVAL, "%s: null pointer", fn);
+    if (reinterpret_cast<uintptr_t>(q) & 15) return set_error(KVC_EINVAL, "%s: q not 16-byte aligned", fn);
+    return KVC_OK;
+}
+
+// The no-allocation variant's workspace: one file-scope array per device (each GPU holds its own copy
+// at its own address, from the library's load until the process ends). Host code never passes the
+// array's name to a kernel: its device address comes from hipGetSymbolAddress, taken once per device
+// with that device current.
+__device__ __align__(256) uint8_t scratch[KVC_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+int scratch_of_current_device(void** out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return set_error(KVC_EDEVICE, "hipGetDevice: %s", hipGetErrorString(e));
+    if (dev < 0 || dev >= kMaxDevices) return set_error(KVC_EUNSUPPORTED, "device %d beyond %d", dev, kMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            return set_error(KVC_EDEVICE, "hipGetSymbolAddress(scratch) on device %d: %s", dev, hipGetErrorString(e));
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return KVC_OK;
+}
+
+}  // namespace
+}  // namespace kvc
+
+extern "C" int kvc_decode_attn(const kvc_stream_desc* k, const kvc_stream_desc* v, const uint16_t* q, int32_t G,
+                               const int32_t* seq_len, int32_t max_seq_len, float* out, void* ws, size_t ws_bytes,
+                               void* stream) {
+    clear_error();
+    if (int e = decode_check(k, v, G, max_seq_len)) return e;
+    if (k->n_units == 0) return KVC_OK;
+    if (int e = decode_args("kvc_decode_attn", q, seq_len, out)) return e;
+    if (!ws) return set_error(KVC_EINVAL, "kvc_decode_attn: null workspace");
+    if (reinterpret_cast<uintptr_t>(ws) & 255) return set_error(KVC_EINVAL, "kvc_decode_attn: workspace not 256-byte aligned");
+    const WsLayout L = ws_layout(k, G, max_seq_len);
+    if ((int64_t)ws_bytes < L.total)
+        return set_error(KVC_ENOSPACE, "kvc_decode_attn: workspace %zu < %lld bytes", ws_bytes, (long long)L.total);
+    return decode_launch(k, v, q, G, seq_len, max_seq_len, out, ws, L, stream);
+}
+
+extern "C" int kvc_decode_attn_noalloc(const kvc_stream_desc* k, const kvc_stream_desc* v, const uint16_t* q,
+                                       int32_t G, const int32_t* seq_len, int32_t max_seq_len, float* out,
+                                       void* stream) {
+    clear_error();
+    if (int e = decode_check(k, v, G, max_seq_len)) return e;
+    if (k->n_units == 0) return KVC_OK;
+    if (int e = decode_args("kvc_decode_attn_noalloc", q, seq_len, out)) return e;
+    const WsLayout L = ws_layout(k, G, max_seq_len);
+    if (L.total > (int64_t)KVC_NOALLOC_SCRATCH_BYTES)
+        return set_error(KVC_ENOSPACE, "kvc_decode_attn_noalloc: needs %lld bytes of workspace, the scratch holds %lld",
+                         (long long)L.total, (long long)KVC_NOALLOC_SCRATCH_BYTES);
+    void* ws = nullptr;
+    if (int e = scratch_of_current_device(&ws)) return e;
+    return decode_launch(k, v, q, G, seq_len, max_seq_len, out, ws, L, stream);
 }
 
 extern "C" int kvc_read_probe(const void* buf, size_t bytes, uint32_t* sink, void* stream) {

@@ -19,6 +19,7 @@ SIDE_K, SIDE_V = 0, 1
 SOLVER_DAMPED, SOLVER_DP, SOLVER_C1_ONLY = 0, 1, 2
 TILE = 64
 HEAD_DIM = 128
+NOALLOC_SCRATCH_BYTES = 64 << 20  # KVC_NOALLOC_SCRATCH_BYTES of include/kvc.h
 
 
 class KvcError(RuntimeError):
@@ -68,6 +69,8 @@ def lib():
         L.kvc_decode_attn_workspace.argtypes = [ctypes.POINTER(StreamDesc), ctypes.POINTER(StreamDesc),
                                                 ctypes.c_int32, ctypes.c_int32]
         L.kvc_decode_attn_workspace.restype = ctypes.c_size_t
+        L.kvc_decode_attn_noalloc.argtypes = [ctypes.POINTER(StreamDesc), ctypes.POINTER(StreamDesc), _p,
+                                              ctypes.c_int32, _p, ctypes.c_int32, _p, _p]
         L.kvc_reconstruct.argtypes = [ctypes.POINTER(StreamDesc), ctypes.c_int32, ctypes.c_int32, _p, _p]
         L.kvc_read_probe.argtypes = [_p, ctypes.c_size_t, _p, _p]
         L.kvc_encode_kv.argtypes = [ctypes.POINTER(StreamDesc), ctypes.POINTER(StreamDesc), _p, ctypes.c_int64, _p,
@@ -249,6 +252,20 @@ def kvc_decode_attn(k: Side, v: Side, q, G: int, seq_len, max_seq_len: int, out,
                                  ctypes.c_void_p(seq_len.data_ptr()), int(max_seq_len),
                                  ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(ws.data_ptr()), ws.numel(),
                                  _stream_ptr(stream)))
+
+
+def kvc_decode_attn_noalloc(k: Side, v: Side, q, G: int, seq_len, max_seq_len: int, out, stream=None):
+    """kvc_decode_attn with the library's fixed workspace (no allocation; calls on one GPU must not overlap)."""
+    import torch
+    U = k.n_units
+    assert q.is_contiguous() and out.is_contiguous() and seq_len.is_contiguous()
+    assert q.dtype == torch.float16 and q.numel() == U * G * HEAD_DIM
+    assert out.dtype == torch.float32 and out.numel() == U * G * HEAD_DIM
+    assert seq_len.dtype == torch.int32 and seq_len.numel() == U and v.n_units == U
+    assert q.device == out.device == seq_len.device == k.codes.device
+    _check(lib().kvc_decode_attn_noalloc(ctypes.byref(k.desc), ctypes.byref(v.desc), ctypes.c_void_p(q.data_ptr()),
+                                         int(G), ctypes.c_void_p(seq_len.data_ptr()), int(max_seq_len),
+                                         ctypes.c_void_p(out.data_ptr()), _stream_ptr(stream)))
 
 
 def kvc_reconstruct(side: Side, t0: int, n_tok: int, out, stream=None):

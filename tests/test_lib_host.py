@@ -260,3 +260,9 @@ def test_encode_kv_rejects_swapped_sides_without_gpu():
     assert rc == kvc.KVC_EINVAL and b"16-byte" in L.kvc_last_error()
     rc = L.kvc_encode_kv(ctypes.byref(dk), ctypes.byref(dv), fake, 128, fake, 128, 60, 5, None)
     assert rc == kvc.KVC_ENOSPACE
+
+
+def test_noalloc_scratch_size_matches_header():
+    src = open(os.path.join(ROOT, "include", "kvc.h")).read()
+    m = re.search(r"#define KVC_NOALLOC_SCRATCH_BYTES \((\d+)ll << (\d+)\)", src)
+    assert m and int(m.group(1)) << int(m.group(2)) == kvc.NOALLOC_SCRATCH_BYTES
