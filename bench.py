@@ -76,12 +76,18 @@ def cpu_baseline(w, stats, seed: int, units, n_tok: int):
     from oracle import alloc as oa
     from oracle import attention as oatt
     from oracle import basis as ob
+    from oracle import calib
     from oracle import native as onat
     from paper_2609_24298_amd import kvc, pipeline
 
-    lam_k = np.stack([s.lam_k for s in stats])
-    sq = np.stack([s.sigma2_q for s in stats])
-    lam_v = np.stack([s.lam_v for s in stats])
+    # the oracle's own calibration of every head (the allocation couples all heads)
+    cal = calib.calibrate_heads(np.stack([s.cov.S_k for s in stats]), np.stack([s.cov.S_v for s in stats]),
+                                np.stack([np.stack(s.cov.S_q) for s in stats]))
+    stats = [pipeline.HeadStats(s.cov, cal["lam_k"][h], cal["U_k"][h], cal["sigma2_q"][h], cal["lam_v"][h],
+                                cal["U_v"][h]) for h, s in enumerate(stats)]
+    lam_k = cal["lam_k"]
+    sq = cal["sigma2_q"]
+    lam_v = cal["lam_v"]
     ak = oa.allocate(lam_k, sq, oa.AllocOpts(bpd=w.bpd))
     av = oa.allocate(lam_v, None, oa.AllocOpts(bpd=w.bpd, solver=oa.SOLVER_C1_ONLY))
     prepared = []

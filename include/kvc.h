@@ -275,6 +275,41 @@ int kvc_reconstruct(const kvc_stream_desc* s, int32_t t0, int32_t n_tok, float* 
  */
 int kvc_read_probe(const void* buf, size_t bytes, uint32_t* sink, void* stream);
 
+/*
+ * Calibration on the device (table step 1; Section 2 for the query variance; the paper computes the
+ * eigendecomposition in fp32). Batched over heads; every array is device memory owned by the caller;
+ * async on `stream`. The results feed kvc_allocate (lambda, sigma2_q) and kvc_make_basis (U) on the host.
+ *
+ * kvc_covariance - cov[h] = (1/n) sum_t x_t x_t^T - mu mu^T (centered = 1) or without the mean term
+ * (centered = 0), mu = (1/n) sum_t x_t, for the n_tok calibration activations of each head.
+ *  x      device fp16 [n_heads][...]: head h's tokens start at x + h * x_head_stride elements, n_tok
+ *         rows of d = 128. 16-byte aligned; x_head_stride a multiple of 8, >= n_tok * d.
+ *  cov    device f32 [n_heads][d][d], row-major. fp32 accumulation of exact fp16 products.
+ */
+int kvc_covariance(const uint16_t* x, int64_t x_head_stride, int32_t n_heads, int32_t n_tok,
+                   int32_t centered, float* cov, void* stream);
+
+/*
+ * kvc_eigh - eigendecomposition S = U diag(lambda) U^T of n symmetric d x d matrices (fp32 Jacobi).
+ *  S        device f32 [n][d][d] (read only; only symmetric input is meaningful).
+ *  lambda   device f32 [n][d] out: eigenvalues in descending order (negative ones clamped to 0).
+ *  U        device f32 [n][d][d] out, row-major: column k (U[j*d + k]) is the eigenvector of
+ *           lambda[k], its largest-magnitude entry made positive.
+ *  sweeps   device int32 [n] out, or NULL: Jacobi sweeps used per matrix (-1: not converged in 30).
+ * Ties in lambda keep the order of the converged diagonal.
+ */
+int kvc_eigh(const float* S, int32_t n, float* lambda, float* U, int32_t* sweeps, void* stream);
+
+/*
+ * kvc_query_variance - sigma2_q[h][i] = (1/G) sum_g u_i^T S_q[h][g] u_i: the query variance along each
+ * eigendirection u_i (column i of U[h]), averaged over the G query heads sharing KV head h.
+ *  U        device f32 [n_heads][d][d] as kvc_eigh writes it.
+ *  S_q      device f32 [n_heads][G][d][d]: query covariances.
+ *  sigma2_q device f32 [n_heads][d] out.
+ */
+int kvc_query_variance(const float* U, const float* S_q, int32_t n_heads, int32_t G, float* sigma2_q,
+                       void* stream);
+
 /* Message of the last failing call on this thread ("" if none). */
 const char* kvc_last_error(void);
 

@@ -38,7 +38,7 @@ def build(verbose: bool = True) -> str:
     _run(["g++", "-std=c++17", "-O2", "-fPIC", "-ffp-contract=off", "-fno-fast-math", "-Wall",
           "-I", INCLUDE, "-c", os.path.join(CSRC, "kvc_host.cpp"), "-o", host_o])
     objs = [host_o]
-    for src in ("kvc_kernels.hip", "kvc_decode.hip"):
+    for src in ("kvc_kernels.hip", "kvc_decode.hip", "kvc_calib.hip"):
         o = os.path.join(BUILD, src.replace(".hip", ".o"))
         _run([hipcc, "-std=c++17", "-O3", "-fPIC", f"--offload-arch={ARCH}", "-ffp-contract=fast",
               "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

@@ -75,6 +75,9 @@ def lib():
         L.kvc_read_probe.argtypes = [_p, ctypes.c_size_t, _p, _p]
         L.kvc_encode_kv.argtypes = [ctypes.POINTER(StreamDesc), ctypes.POINTER(StreamDesc), _p, ctypes.c_int64, _p,
                                     ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, _p]
+        L.kvc_covariance.argtypes = [_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _p, _p]
+        L.kvc_eigh.argtypes = [_p, ctypes.c_int32, _p, _p, _p, _p]
+        L.kvc_query_variance.argtypes = [_p, _p, ctypes.c_int32, ctypes.c_int32, _p, _p]
         L.kvc_last_error.restype = ctypes.c_char_p
         L.kvc_version.restype = ctypes.c_int32
         _lib = L
@@ -284,3 +287,39 @@ def kvc_read_probe(buf, sink, stream=None):
     assert sink.dtype in (torch.int32, torch.uint32) and buf.device == sink.device
     _check(lib().kvc_read_probe(ctypes.c_void_p(buf.data_ptr()), buf.numel() * buf.element_size(),
                                 ctypes.c_void_p(sink.data_ptr()), _stream_ptr(stream)))
+
+
+# ------------------------------------------------------------------ calibration (table step 1)
+
+def kvc_covariance(x, n_tok: int, cov, centered: bool = True, stream=None):
+    """x: fp16 (n_heads, >= n_tok, d) on the device; cov: f32 (n_heads, d, d)."""
+    import torch
+    assert x.dtype == torch.float16 and x.is_contiguous() and x.dim() == 3 and x.shape[2] == HEAD_DIM
+    assert cov.dtype == torch.float32 and cov.is_contiguous() and cov.shape == (x.shape[0], HEAD_DIM, HEAD_DIM)
+    assert x.shape[1] >= n_tok and x.device == cov.device
+    _check(lib().kvc_covariance(ctypes.c_void_p(x.data_ptr()), int(x.stride(0)), int(x.shape[0]), int(n_tok),
+                                int(bool(centered)), ctypes.c_void_p(cov.data_ptr()), _stream_ptr(stream)))
+
+
+def kvc_eigh(S, lam, U, sweeps=None, stream=None):
+    """S: f32 (n, d, d); lam: f32 (n, d); U: f32 (n, d, d); sweeps: int32 (n,) or None. All on the device."""
+    import torch
+    n = S.shape[0]
+    for t in (S, U):
+        assert t.dtype == torch.float32 and t.is_contiguous() and t.shape == (n, HEAD_DIM, HEAD_DIM)
+    assert lam.dtype == torch.float32 and lam.is_contiguous() and lam.shape == (n, HEAD_DIM)
+    assert sweeps is None or (sweeps.dtype == torch.int32 and sweeps.numel() == n)
+    _check(lib().kvc_eigh(ctypes.c_void_p(S.data_ptr()), int(n), ctypes.c_void_p(lam.data_ptr()),
+                          ctypes.c_void_p(U.data_ptr()), None if sweeps is None else ctypes.c_void_p(sweeps.data_ptr()),
+                          _stream_ptr(stream)))
+
+
+def kvc_query_variance(U, S_q, sig, stream=None):
+    """U: f32 (n, d, d); S_q: f32 (n, G, d, d); sig: f32 (n, d). All on the device."""
+    import torch
+    n, G = S_q.shape[0], S_q.shape[1]
+    assert U.dtype == S_q.dtype == sig.dtype == torch.float32
+    assert U.is_contiguous() and S_q.is_contiguous() and sig.is_contiguous()
+    assert U.shape == (n, HEAD_DIM, HEAD_DIM) and S_q.shape == (n, G, HEAD_DIM, HEAD_DIM) and sig.shape == (n, HEAD_DIM)
+    _check(lib().kvc_query_variance(ctypes.c_void_p(U.data_ptr()), ctypes.c_void_p(S_q.data_ptr()), int(n), int(G),
+                                    ctypes.c_void_p(sig.data_ptr()), _stream_ptr(stream)))

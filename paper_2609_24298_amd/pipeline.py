@@ -1,6 +1,7 @@
 """Assemble a KV-COBRA compressed cache for a synthetic workload through libkvc.
 
-Calibration statistics come from the synthetic generator (synth); allocation,
+The synthetic generator (synth) supplies exact covariances and draws tokens;
+calibration (table step 1: eigendecomposition, query variance), allocation,
 basis construction, encode, decode attention and reconstruction are library
 calls. Layout of units: u = (layer * batch + sequence) * kv_heads + head; the
 sequences of one (layer, head) share its basis.
@@ -12,6 +13,65 @@ from dataclasses import dataclass
 import numpy as np
 
 from . import kvc, synth
+
+
+@dataclass
+class HeadStats:
+    """Calibration record of one (layer, KV head): its covariances (and token factors) plus the
+    results of table step 1 in fp64 arrays (eigenvalues descending, eigenvectors as columns)."""
+    cov: synth.HeadCov
+    lam_k: np.ndarray
+    U_k: np.ndarray
+    sigma2_q: np.ndarray
+    lam_v: np.ndarray
+    U_v: np.ndarray
+
+    @property
+    def F_k(self):
+        return self.cov.F_k
+
+    @property
+    def F_v(self):
+        return self.cov.F_v
+
+    @property
+    def F_q(self):
+        return self.cov.F_q
+
+    @property
+    def sign_k(self):
+        return self.cov.sign_k
+
+    @property
+    def sign_v(self):
+        return self.cov.sign_v
+
+
+def calibrate(covs, device="cuda", batch: int = 1024):
+    """Table step 1 on the device for every head: kvc_eigh of the key and value covariances and
+    kvc_query_variance of the query heads along the key eigendirections (fp32, as the paper states)."""
+    import torch
+    dev = torch.device(device)
+    H, d = len(covs), covs[0].S_k.shape[0]
+    out = {k: np.zeros((H, d)) for k in ("lam_k", "lam_v", "sigma2_q")}
+    out.update({k: np.zeros((H, d, d)) for k in ("U_k", "U_v")})
+    for h0 in range(0, H, batch):
+        hs = covs[h0:h0 + batch]
+        n = len(hs)
+        for side in ("k", "v"):
+            S = torch.as_tensor(np.stack([getattr(c, "S_" + side) for c in hs]).astype(np.float32), device=dev)
+            lam = torch.empty((n, d), dtype=torch.float32, device=dev)
+            U = torch.empty((n, d, d), dtype=torch.float32, device=dev)
+            kvc.kvc_eigh(S, lam, U)
+            if side == "k":
+                Sq = torch.as_tensor(np.stack([np.stack(c.S_q) for c in hs]).astype(np.float32), device=dev)
+                sig = torch.empty((n, d), dtype=torch.float32, device=dev)
+                kvc.kvc_query_variance(U, Sq, sig)
+                out["sigma2_q"][h0:h0 + n] = sig.cpu().numpy()
+            out["lam_" + side][h0:h0 + n] = lam.cpu().numpy()
+            out["U_" + side][h0:h0 + n] = U.cpu().numpy()
+    return [HeadStats(c, out["lam_k"][h], out["U_k"][h], out["sigma2_q"][h], out["lam_v"][h], out["U_v"][h])
+            for h, c in enumerate(covs)]
 
 
 @dataclass
@@ -96,7 +156,7 @@ class Cache:
         self.w = w
         self.seed = seed
         self.device = torch.device(device)
-        self.stats = synth.workload_stats(w, seed) if stats is None else stats
+        self.stats = calibrate(synth.workload_covs(w, seed), device) if stats is None else stats
         self.k_tab, self.v_tab = allocate_workload(w, self.stats, bpd, solver, uniform)
         self.capacity = w.tokens if capacity is None else capacity
         self.K = build_side(kvc.SIDE_K, self.k_tab, w, self.capacity, device)

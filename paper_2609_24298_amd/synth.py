@@ -8,10 +8,11 @@ N(0, Sigma) with a power-law spectrum lambda_i = i^(-alpha), alpha ~ U[0.5, 2]
 outlier channels whose standard deviation is multiplied by 8. Queries are
 drawn the same way, one covariance per query head.
 
-The calibration statistics the paper measures on real activations (table
-step 1: eigenvalues and eigenbasis of the key covariance, the query variance
-along each eigendirection) are computed here from the exact synthetic
-covariances in fp64.
+What a calibration pass would measure on real activations, the covariances,
+is known exactly here (Sigma = F F^T for the generator's factor F) and is
+handed out as such. Table step 1 (the eigendecomposition and the query
+variance along each eigendirection) is not done here: the library computes it
+on the device (kvc_eigh, kvc_query_variance) and the oracle on its own.
 """
 from __future__ import annotations
 
@@ -79,33 +80,20 @@ def power_law_factor(rng: np.random.Generator, d: int = D_HEAD):
     return F, F @ F.T, alpha
 
 
-def eig_desc(S: np.ndarray):
-    """Eigenvalues (descending) and eigenvectors (columns) of a symmetric matrix, fp64."""
-    lam, U = np.linalg.eigh(S)
-    idx = np.argsort(-lam, kind="stable")
-    lam = lam[idx]
-    U = U[:, idx]
-    # fix the sign so the largest-magnitude entry of each eigenvector is positive
-    j = np.argmax(np.abs(U), axis=0)
-    U = U * np.sign(U[j, np.arange(U.shape[1])])[None, :]
-    return np.maximum(lam, 0.0), U
-
-
 @dataclass
-class HeadStats:
-    lam_k: np.ndarray
-    U_k: np.ndarray
-    sigma2_q: np.ndarray     # query variance along each key eigendirection, mean over the group
-    lam_v: np.ndarray
-    U_v: np.ndarray
-    F_k: np.ndarray
+class HeadCov:
+    """Exact covariances of one (layer, KV head) with the factors that generate its tokens."""
+    S_k: np.ndarray          # key covariance (d x d)
+    S_v: np.ndarray          # value covariance
+    S_q: list                # one covariance per query head of the group
+    F_k: np.ndarray          # S_k = F_k F_k^T
     F_v: np.ndarray
     F_q: list = field(default_factory=list)
-    sign_k: np.ndarray | None = None  # +-1 per importance position (length d)
+    sign_k: np.ndarray | None = None  # +-1 per importance position (length d), the random sign flip
     sign_v: np.ndarray | None = None
 
 
-def head_stats(seed: int, layer: int, head: int, group: int, d: int = D_HEAD) -> HeadStats:
+def head_cov(seed: int, layer: int, head: int, group: int, d: int = D_HEAD) -> HeadCov:
     F_k, S_k, _ = power_law_factor(rng_for(seed, KIND_K, layer, head), d)
     F_v, S_v, _ = power_law_factor(rng_for(seed, KIND_V, layer, head), d)
     F_q, S_q = [], []
@@ -113,19 +101,14 @@ def head_stats(seed: int, layer: int, head: int, group: int, d: int = D_HEAD) ->
         F, S, _ = power_law_factor(rng_for(seed, KIND_Q, layer, head, g), d)
         F_q.append(F)
         S_q.append(S)
-    lam_k, U_k = eig_desc(S_k)
-    lam_v, U_v = eig_desc(S_v)
-    sig2 = np.zeros(d)
-    for S in S_q:
-        sig2 += np.einsum("ji,jk,ki->i", U_k, S, U_k)
-    sig2 /= group
     sk = rng_for(seed, KIND_SIGN_K, layer, head).integers(0, 2, size=d) * 2 - 1
     sv = rng_for(seed, KIND_SIGN_V, layer, head).integers(0, 2, size=d) * 2 - 1
-    return HeadStats(lam_k, U_k, sig2, lam_v, U_v, F_k, F_v, F_q, sk.astype(np.int8), sv.astype(np.int8))
+    return HeadCov(S_k, S_v, S_q, F_k, F_v, F_q, sk.astype(np.int8), sv.astype(np.int8))
 
 
-def workload_stats(w: Workload, seed: int = 0) -> list[HeadStats]:
-    return [head_stats(seed, l, h, w.group, w.d) for l in range(w.layers) for h in range(w.kv_heads)]
+def workload_covs(w: Workload, seed: int = 0) -> list[HeadCov]:
+    """Covariances of every (layer, KV head) of a workload, head index layer * kv_heads + head."""
+    return [head_cov(seed, l, h, w.group, w.d) for l in range(w.layers) for h in range(w.kv_heads)]
 
 
 def draw_tokens_np(F: np.ndarray, n: int, rng: np.random.Generator) -> np.ndarray:

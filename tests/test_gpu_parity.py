@@ -19,6 +19,8 @@ from oracle import basis as ob
 from oracle import native as onat
 from paper_2609_24298_amd import kvc, pipeline, synth
 
+from oracle_stats import oracle_stats
+
 pytestmark = pytest.mark.gpu
 TOL = 2e-3
 
@@ -68,7 +70,7 @@ def x_bits(x_unit):
 def small():
     w = synth.WORKLOADS["small_l1_h8_t4k"]
     log("[small] build cache", w)
-    cache = pipeline.Cache(w, seed=0)
+    cache = pipeline.Cache(w, seed=0, stats=oracle_stats(w, 0))
     xk = pipeline.draw_unit_tokens(w, cache.stats, kvc.SIDE_K, w.tokens, 0, "cuda")
     xv = pipeline.draw_unit_tokens(w, cache.stats, kvc.SIDE_V, w.tokens, 0, "cuda")
     cache.encode(xk, xv, 0, w.tokens)

@@ -28,6 +28,7 @@ from oracle import native as onat
 from oracle import quant as oq
 from paper_2609_24298_amd import kvc, pipeline, synth
 
+from oracle_stats import oracle_stats
 from test_gpu_parity import TOL, OracleTables, normwise, x_bits
 
 pytestmark = pytest.mark.gpu
@@ -38,7 +39,7 @@ def log(*a):
 
 
 def _build(w, T, capacity, seed=0, bpd=None):
-    cache = pipeline.Cache(w, seed=seed, bpd=bpd, capacity=capacity)
+    cache = pipeline.Cache(w, seed=seed, bpd=bpd, capacity=capacity, stats=oracle_stats(w, seed))
     xk = pipeline.draw_unit_tokens(w, cache.stats, kvc.SIDE_K, T, seed, "cuda")
     xv = pipeline.draw_unit_tokens(w, cache.stats, kvc.SIDE_V, T, seed, "cuda")
     return cache, xk, xv

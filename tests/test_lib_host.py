@@ -13,6 +13,8 @@ from oracle import alloc as oa
 from oracle import basis as ob
 from paper_2609_24298_amd import kvc, synth
 
+from oracle_stats import oracle_stats
+
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
@@ -47,7 +49,7 @@ def _oracle_opts(o: kvc.AllocOpts) -> oa.AllocOpts:
 
 def _stats(n_layers, group=4, seed=0):
     w = synth.Workload("t", n_layers, 8, group, 1, 64, 2.0)
-    return synth.workload_stats(w, seed)
+    return oracle_stats(w, seed)
 
 
 @pytest.mark.parametrize("bpd", [0.5, 1.0, 2.0, 3.0, 4.0])

@@ -136,15 +136,18 @@ def test_kl_weights_and_stable_reorder():
 
 def test_kl_query_variance_matches_monte_carlo():
     # sigma_Q,i^2 = E[(u_i . q)^2] along each key eigendirection (Proposition prop:kl-bound (c))
+    # on a synthetic head: the oracle's calibration of its exact covariances against samples
+    from oracle import calib
     from paper_2609_24298_amd import synth
-    st = synth.head_stats(0, 0, 0, 4, d=128)
+    c = synth.head_cov(0, 0, 0, 4, d=128)
+    _, U_k, sig2, _, _ = calib.head_calibration(c.S_k, c.S_v, c.S_q)
     rng = np.random.default_rng(1)
     est = np.zeros(128)
-    for F in st.F_q:
+    for F in c.F_q:
         q = rng.standard_normal((200_000, 128)) @ F.T
-        est += np.mean((q @ st.U_k) ** 2, axis=0)
+        est += np.mean((q @ U_k) ** 2, axis=0)
     est /= 4
-    assert np.allclose(est, st.sigma2_q, rtol=0.03, atol=1e-3 * st.sigma2_q.max())
+    assert np.allclose(est, sig2, rtol=0.03, atol=1e-3 * sig2.max())
 
 
 def test_allocate_c1_only_and_infeasible_fallback():
