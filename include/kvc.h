@@ -217,6 +217,24 @@ int kvc_decode_attn(const kvc_stream_desc* k, const kvc_stream_desc* v, const ui
                     int32_t G, const int32_t* seq_len, int32_t max_seq_len, float* out,
                     void* ws, size_t ws_bytes, void* stream);
 
+/*
+ * kvc_decode_step - one serving decode step in one call: append the new token's key and value to
+ * every unit, then attend. Paper: table steps 7-8 (each new token is compressed and cached; attention
+ * reads the cache). Equivalent to kvc_encode_kv(k, v, xk, .., xv, .., t_new, 1) followed by
+ * kvc_decode_attn(k, v, q, G, seq_len, max_seq_len, out, ws, ..), with identical codes and outputs,
+ * but the append runs in the same launch as the query projection (three launches instead of four).
+ *  xk, xv        device fp16 [n_units][...], the new token of unit u at xk + u * xk_unit_stride (one
+ *                row of d); 16-byte aligned, strides multiples of 8 elements and >= d.
+ *  t_new         host: the new token's position in every unit's stream (t_new + 1 <= capacities).
+ *  seq_len       as kvc_decode_attn; a step that attends to the new token passes t_new + 1.
+ * Other arguments, workspace (kvc_decode_attn_workspace) and errors as kvc_decode_attn and
+ * kvc_encode_kv. Async on `stream`.
+ */
+int kvc_decode_step(const kvc_stream_desc* k, const kvc_stream_desc* v, const uint16_t* xk,
+                    int64_t xk_unit_stride, const uint16_t* xv, int64_t xv_unit_stride, int32_t t_new,
+                    const uint16_t* q, int32_t G, const int32_t* seq_len, int32_t max_seq_len, float* out,
+                    void* ws, size_t ws_bytes, void* stream);
+
 /* Workspace bytes kvc_decode_attn needs for these descriptors (host only). */
 size_t kvc_decode_attn_workspace(const kvc_stream_desc* k, const kvc_stream_desc* v,
                                  int32_t G, int32_t max_seq_len);

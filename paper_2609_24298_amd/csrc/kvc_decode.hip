@@ -40,7 +40,9 @@
 #include <cmath>
 #include <cstdint>
 #include <mutex>
+#include <utility>
 
+#include "kvc_append.h"
 #include "kvc_device.h"
 #include "kvc_internal.h"
 
@@ -480,15 +482,15 @@ typedef float qp_f4 __attribute__((ext_vector_type(4)));
 // rows 16 rb + 4 kq + v of head col; a head's max and limb sums reduce over its four lanes, then over
 // the wavefronts through LDS.
 template <int NW>
-__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2, 2))) void qprep_kernel(DevSide K, const uint16_t* __restrict__ q, int G, int LM,
-                                                   v4i* __restrict__ qa, float4* __restrict__ qk) {
+__device__ __forceinline__ void qprep_unit(const DevSide& K, const uint16_t* __restrict__ q, int G, int LM,
+                                           v4i* __restrict__ qa, float4* __restrict__ qk, const int u) {
     constexpr int RB = 8 / NW;                 // row blocks per wavefront
     constexpr int HALF = RB > 4 ? 2 : 1;       // rounds of at most four row blocks' loads
     constexpr int RQ = RB / HALF;
     extern __shared__ uint8_t img[];  // [2][LM][64][16] operand image
     __shared__ float red_m[NW][16];
     __shared__ int red_l[NW][16][kLimbs];
-    const int u = blockIdx.x, wv = threadIdx.x >> 6, lane = threadIdx.x & 63, col = lane & 15, kq = lane >> 4;
+    const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63, col = lane & 15, kq = lane >> 4;
     const int r = K.r[u], b = K.b[u];
     const uint16_t* __restrict__ P = K.basis + K.basis_off[u];
     const int img_words = 2 * LM * 64 * 4;
@@ -599,6 +601,26 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2, 2)))
     __syncthreads();
     v4i* dst = qa + (int64_t)u * 2 * LM * 64;
     for (int k = threadIdx.x; k < 2 * LM * 64; k += 64 * NW) dst[k] = reinterpret_cast<const v4i*>(img)[k];
+}
+
+template <int NW>
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2, 2))) void qprep_kernel(
+    DevSide K, const uint16_t* __restrict__ q, int G, int LM, v4i* __restrict__ qa, float4* __restrict__ qk) {
+    qprep_unit<NW>(K, q, G, LM, qa, qk, blockIdx.x);
+}
+
+// The first launch of a fused decode step (kvc_decode_step): block (u, 0) projects unit u's queries
+// (two wavefronts, four row blocks each), blocks (u, 1) and (u, 2) append the new token's key and
+// value to unit u's streams (the append of kvc_encode_kv). The decode partials, launched next on the
+// same stream, read the appended codes.
+constexpr int kStepPrepThreads = 128;
+static_assert(kStepPrepThreads == kAppThreads, "the append uses one thread per coordinate");
+__global__ __launch_bounds__(kStepPrepThreads) void step_prep_kernel(
+    DevSide K, DevSide V, const uint16_t* __restrict__ q, int G, int LM, v4i* __restrict__ qa, float4* __restrict__ qk,
+    const uint16_t* __restrict__ xk, int64_t xk_stride, const uint16_t* __restrict__ xv, int64_t xv_stride, int t_new) {
+    if (blockIdx.y == 0) qprep_unit<2>(K, q, G, LM, qa, qk, blockIdx.x);
+    else if (blockIdx.y == 1) append_unit(K, KVC_SIDE_K, xk, xk_stride, t_new, 1, blockIdx.x);
+    else append_unit(V, KVC_SIDE_V, xv, xv_stride, t_new, 1, blockIdx.x);
 }
 
 // ---------------------------------------------------------------- partials
@@ -1286,9 +1308,20 @@ extern "C" size_t kvc_decode_attn_workspace(const kvc_stream_desc* k, const kvc_
 namespace kvc {
 namespace {
 
-// Launches of one decode step into the workspace ws (validated by the caller, of layout L).
+// The new token of a fused decode step (none for a plain decode call).
+struct StepAppend {
+    const uint16_t* xk = nullptr;
+    int64_t xk_stride = 0;
+    const uint16_t* xv = nullptr;
+    int64_t xv_stride = 0;
+    int t_new = -1;
+};
+
+// Launches of one decode step into the workspace ws (validated by the caller, of layout L); with an
+// append, the query projection and the append share the first launch.
 int decode_launch(const kvc_stream_desc* k, const kvc_stream_desc* v, const uint16_t* q, int32_t G,
-                  const int32_t* seq_len, int32_t max_seq_len, float* out, void* ws, const WsLayout& L, void* stream) {
+                  const int32_t* seq_len, int32_t max_seq_len, float* out, void* ws, const WsLayout& L, void* stream,
+                  const StepAppend& app = StepAppend()) {
     const int U = k->n_units;
     char* w = reinterpret_cast<char*>(ws);
     v4i* qa = reinterpret_cast<v4i*>(w + L.qa);
@@ -1298,8 +1331,11 @@ int decode_launch(const kvc_stream_desc* k, const kvc_stream_desc* v, const uint
     const DevSide K = dev_side(k), V = dev_side(v);
     const int LM = (G + 3) / 4;
     const size_t qsm = (size_t)2 * LM * 64 * 16;
+    if (app.t_new >= 0)
+        hipLaunchKernelGGL(step_prep_kernel, dim3(U, 3), dim3(kStepPrepThreads), qsm, st, K, V, q, G, LM, qa, qk, app.xk,
+                           app.xk_stride, app.xv, app.xv_stride, app.t_new);
     // one wavefront per unit while the units fill the device, eight (one per row block) for a few units
-    if ((int64_t)U * 4 >= (int64_t)device_cus() * 8)
+    else if ((int64_t)U * 4 >= (int64_t)device_cus() * 8)
         hipLaunchKernelGGL(qprep_kernel<1>, dim3(U), dim3(64), qsm, st, K, q, G, LM, qa, qk);
     else
         hipLaunchKernelGGL(qprep_kernel<8>, dim3(U), dim3(512), qsm, st, K, q, G, LM, qa, qk);
@@ -1378,6 +1414,34 @@ extern "C" int kvc_decode_attn(const kvc_stream_desc* k, const kvc_stream_desc* 
     if ((int64_t)ws_bytes < L.total)
         return set_error(KVC_ENOSPACE, "kvc_decode_attn: workspace %zu < %lld bytes", ws_bytes, (long long)L.total);
     return decode_launch(k, v, q, G, seq_len, max_seq_len, out, ws, L, stream);
+}
+
+extern "C" int kvc_decode_step(const kvc_stream_desc* k, const kvc_stream_desc* v, const uint16_t* xk,
+                               int64_t xk_unit_stride, const uint16_t* xv, int64_t xv_unit_stride, int32_t t_new,
+                               const uint16_t* q, int32_t G, const int32_t* seq_len, int32_t max_seq_len, float* out,
+                               void* ws, size_t ws_bytes, void* stream) {
+    clear_error();
+    if (int e = decode_check(k, v, G, max_seq_len)) return e;
+    if (t_new < 0) return set_error(KVC_EINVAL, "kvc_decode_step: negative t_new");
+    if ((int64_t)t_new + 1 > k->capacity || (int64_t)t_new + 1 > v->capacity)
+        return set_error(KVC_ENOSPACE, "kvc_decode_step: t_new + 1 > capacity");
+    if (k->n_units == 0) return KVC_OK;
+    for (const auto& xs : {std::make_pair(xk, xk_unit_stride), std::make_pair(xv, xv_unit_stride)})
+        if (!xs.first || (reinterpret_cast<uintptr_t>(xs.first) & 15) || (xs.second & 7) || xs.second < (int64_t)kD)
+            return set_error(KVC_EINVAL, "kvc_decode_step: xk, xv must be 16-byte aligned with stride a multiple of 8 and >= d");
+    if (int e = decode_args("kvc_decode_step", q, seq_len, out)) return e;
+    if (!ws) return set_error(KVC_EINVAL, "kvc_decode_step: null workspace");
+    if (reinterpret_cast<uintptr_t>(ws) & 255) return set_error(KVC_EINVAL, "kvc_decode_step: workspace not 256-byte aligned");
+    const WsLayout L = ws_layout(k, G, max_seq_len);
+    if ((int64_t)ws_bytes < L.total)
+        return set_error(KVC_ENOSPACE, "kvc_decode_step: workspace %zu < %lld bytes", ws_bytes, (long long)L.total);
+    StepAppend app;
+    app.xk = xk;
+    app.xk_stride = xk_unit_stride;
+    app.xv = xv;
+    app.xv_stride = xv_unit_stride;
+    app.t_new = t_new;
+    return decode_launch(k, v, q, G, seq_len, max_seq_len, out, ws, L, stream, app);
 }
 
 extern "C" int kvc_decode_attn_noalloc(const kvc_stream_desc* k, const kvc_stream_desc* v, const uint16_t* q,

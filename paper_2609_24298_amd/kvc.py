@@ -69,6 +69,9 @@ def lib():
         L.kvc_decode_attn_workspace.argtypes = [ctypes.POINTER(StreamDesc), ctypes.POINTER(StreamDesc),
                                                 ctypes.c_int32, ctypes.c_int32]
         L.kvc_decode_attn_workspace.restype = ctypes.c_size_t
+        L.kvc_decode_step.argtypes = [ctypes.POINTER(StreamDesc), ctypes.POINTER(StreamDesc), _p, ctypes.c_int64, _p,
+                                      ctypes.c_int64, ctypes.c_int32, _p, ctypes.c_int32, _p, ctypes.c_int32, _p, _p,
+                                      ctypes.c_size_t, _p]
         L.kvc_decode_attn_noalloc.argtypes = [ctypes.POINTER(StreamDesc), ctypes.POINTER(StreamDesc), _p,
                                               ctypes.c_int32, _p, ctypes.c_int32, _p, _p]
         L.kvc_reconstruct.argtypes = [ctypes.POINTER(StreamDesc), ctypes.c_int32, ctypes.c_int32, _p, _p]
@@ -255,6 +258,26 @@ def kvc_decode_attn(k: Side, v: Side, q, G: int, seq_len, max_seq_len: int, out,
                                  ctypes.c_void_p(seq_len.data_ptr()), int(max_seq_len),
                                  ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(ws.data_ptr()), ws.numel(),
                                  _stream_ptr(stream)))
+
+
+def kvc_decode_step(k: Side, v: Side, xk, xv, t_new: int, q, G: int, seq_len, max_seq_len: int, out, ws,
+                    stream=None):
+    """Append the new token (xk, xv: fp16 (n_units, >= 1, d)) at t_new to every unit, then decode attention."""
+    import torch
+    U = k.n_units
+    for side, x in ((k, xk), (v, xv)):
+        assert x.dtype == torch.float16 and x.is_contiguous() and x.dim() == 3
+        assert x.shape[0] == side.n_units and x.shape[1] >= 1 and x.shape[2] == HEAD_DIM and x.device == side.codes.device
+    assert q.is_contiguous() and out.is_contiguous() and seq_len.is_contiguous()
+    assert q.dtype == torch.float16 and q.numel() == U * G * HEAD_DIM
+    assert out.dtype == torch.float32 and out.numel() == U * G * HEAD_DIM
+    assert seq_len.dtype == torch.int32 and seq_len.numel() == U and v.n_units == U
+    assert q.device == out.device == seq_len.device == ws.device == k.codes.device
+    _check(lib().kvc_decode_step(ctypes.byref(k.desc), ctypes.byref(v.desc), ctypes.c_void_p(xk.data_ptr()),
+                                 int(xk.stride(0)), ctypes.c_void_p(xv.data_ptr()), int(xv.stride(0)), int(t_new),
+                                 ctypes.c_void_p(q.data_ptr()), int(G), ctypes.c_void_p(seq_len.data_ptr()),
+                                 int(max_seq_len), ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(ws.data_ptr()),
+                                 ws.numel(), _stream_ptr(stream)))
 
 
 def kvc_decode_attn_noalloc(k: Side, v: Side, q, G: int, seq_len, max_seq_len: int, out, stream=None):

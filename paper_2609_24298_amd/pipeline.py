@@ -175,6 +175,10 @@ class Cache:
     def decode(self, q, seq_len, max_seq_len: int, out, ws, stream=None):
         kvc.kvc_decode_attn(self.K, self.V, q, self.w.group, seq_len, max_seq_len, out, ws, stream)
 
+    def step(self, xk, xv, t_new: int, q, seq_len, max_seq_len: int, out, ws, stream=None):
+        """Fused decode step: append (xk, xv) at t_new to every unit, then decode attention."""
+        kvc.kvc_decode_step(self.K, self.V, xk, xv, t_new, q, self.w.group, seq_len, max_seq_len, out, ws, stream)
+
     def layer_sides(self, layer: int):
         """Descriptors of one layer's units (u = (layer * batch + sequence) * kv_heads + head is
         layer-major, so they are one contiguous range) for per-layer calls."""
