@@ -17,6 +17,9 @@ Passages followed
   table steps 3-4).
 * Exact DP over integer per-head budgets (Appendix D, "Alternative solver").
 * V side in joint K+V mode: uniform per-head budget, C1 only (Appendix F).
+* Exact DP over measured distortion tables (Appendix D, "Exact DP over
+  measured distortion"): the same knapsack with the per-head optimum taken
+  over a table of measured D(r, b) (measured.py) instead of the model.
 
 Readings (paper silent or inconsistent)
 ---------------------------------------
@@ -182,16 +185,20 @@ def c2_damped(W, o: AllocOpts):
 
 def dp_exact(W, o: AllocOpts):
     """Exact separable knapsack over integer budgets (Appendix D), full enumeration."""
-    N = len(W)
+    W = [HeadSums(w) for w in W]
+    return _dp(len(W), lambda h, beta: c1(W[h], float(beta), o), o)
+
+
+def _dp(N, head_opt, o: AllocOpts):
+    """The knapsack of dp_exact over integer budgets with the per-head optimum head_opt(h, beta)."""
     B_tot = o.bpd * float(N * o.d)
     cap = math.floor(B_tot)
     lo = math.ceil(o.bmin())
     hi = math.floor(o.bmax())
-    W = [HeadSums(w) for w in W]
     dstar = [[None] * (hi + 1) for _ in range(N)]
     for h in range(N):
         for beta in range(lo, hi + 1):
-            dstar[h][beta] = c1(W[h], float(beta), o)
+            dstar[h][beta] = head_opt(h, beta)
     INF = math.inf
     prev = [0.0] * (cap + 1)
     choice = []
@@ -221,6 +228,49 @@ def dp_exact(W, o: AllocOpts):
         tot -= budgets[h]
     allocs = [dstar[h][budgets[h]] for h in range(N)]
     return [float(x) for x in budgets], allocs, prev[cap]
+
+
+def c1_table(Dt, B: float, o: AllocOpts):
+    """Per-head optimum over a distortion table Dt[ri][bi] (r = r_min + ri r_step, b = b_min + bi): the
+    smallest D over every grid pair with r b <= B (ties: smallest r, then smallest b), as (r, b, D).
+    Below the smallest pair the head gets (r_min, b_min)."""
+    best = None
+    for ri in range(len(Dt)):
+        r = o.r_min + ri * o.r_step
+        for bi in range(len(Dt[ri])):
+            b = o.b_min + bi
+            if r * b <= B and (best is None or Dt[ri][bi] < best[2]):
+                best = (r, b, float(Dt[ri][bi]))
+    if best is None:
+        best = (o.r_min, o.b_min, float(Dt[0][0]))
+    return best
+
+
+def dp_tables(tables, o: AllocOpts):
+    """Exact DP (Appendix D) with D*_h(beta) = c1_table(tables[h], beta): the measured-distortion solver."""
+    return _dp(len(tables), lambda h, beta: c1_table(tables[h], float(beta), o), o)
+
+
+def brute_force_tables(tables, o: AllocOpts) -> float:
+    """min sum_h tables[h][r_h][b_h] s.t. sum r_h b_h <= floor(B_tot), every pair enumerated (tiny only)."""
+    N = len(tables)
+    cap = math.floor(o.bpd * float(N * o.d))
+    best = math.inf
+
+    def rec(h, used, acc):
+        nonlocal best
+        if h == N:
+            best = min(best, acc)
+            return
+        for ri in range(len(tables[h])):
+            r = o.r_min + ri * o.r_step
+            for bi in range(len(tables[h][ri])):
+                b = o.b_min + bi
+                if used + r * b <= cap:
+                    rec(h + 1, used + r * b, acc + tables[h][ri][bi])
+
+    rec(0, 0, 0.0)
+    return best
 
 
 def brute_force_global(W, o: AllocOpts) -> float:
