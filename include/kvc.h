@@ -145,6 +145,41 @@ int kvc_allocate(const double* lambda, const double* sigma2_q, int32_t n_heads,
                  const kvc_alloc_opts* o, kvc_head_alloc* out, int32_t* order);
 
 /*
+ * kvc_allocate_measured - the exact DP of Appendix D over measured distortion tables ("exact DP over
+ * measured distortion": the calibration activations quantized once per candidate (r, b) replace the
+ * Bennett model). Per head, D(r, b) = T[r] + quant[r][b] with the measured truncation term
+ * T[r] = sum over importance positions p >= r of trunc_w[order[p]] (summed from the last position
+ * down, fp64); the per-head optimum at budget beta is the smallest D over the grid pairs with
+ * r b <= beta (ties: smallest r, then smallest b), and the budgets beta_h are the exact integer
+ * knapsack of kvc_allocate's DP (same B_min, B_max, B_tot = bpd n_heads d).
+ *  quant     host, [n_heads][n_r][n_b]: measured quantization term (kvc_measured_quant), rank
+ *            r = r_min + ri r_step (n_r = (d - r_min) / r_step + 1), width b = b_min + bi.
+ *  trunc_w   host, [n_heads][d]: weight times the measured variance along each eigendirection, by eigen
+ *            index (sigma2_q * lambda_hat for the attention-KL objective, lambda_hat for MSE).
+ *  order     host, [n_heads][d]: the importance order the candidate bases were built with.
+ *  out       host, [n_heads]: (r, b, integer budget, D). o->solver is ignored.
+ * Synchronous, host only, deterministic.
+ */
+int kvc_allocate_measured(const double* quant, const double* trunc_w, const int32_t* order, int32_t n_heads,
+                          const kvc_alloc_opts* o, kvc_head_alloc* out);
+
+/*
+ * kvc_make_candidates - the records of every candidate rank of one head, for the measured tables:
+ * for r = r_min, r_min + r_step, ..., <= d (even grid) the fused basis P_r exactly as kvc_make_basis
+ * builds it, its step for every b = 1..8, and per row k of P_r the weight
+ * c_k = (sum of wt over the importance positions dealt to row k's Hadamard block) / (block size),
+ * which spreads a rotated coordinate's quantization error evenly over its block's eigendirections.
+ *  wt         host, [d]: weight per eigen index (sigma2_q for the attention-KL objective, 1 for MSE).
+ *  P_all      host out: the bases one after another, sum of r*d fp16 values.
+ *  delta_all  host out, [n_r][8]: steps, b = 1..8.
+ *  row_w_all  host out: sum of r floats, the row weights of each rank in turn.
+ * Other arguments as kvc_make_basis. Host only.
+ */
+int kvc_make_candidates(const double* U, const int32_t* order, const double* lambda, const double* wt,
+                        int32_t d, const int8_t* sign, int32_t r_min, int32_t r_step, uint16_t* P_all,
+                        float* delta_all, float* row_w_all);
+
+/*
  * kvc_make_basis - the stored per-head record: fused basis and quantizer step.
  * Paper: Section 3.4 and table steps 5-6 (P = H_r diag(s) U_r^T), Appendix A.1
  * (after the rotation every channel has the mean retained variance).
@@ -327,6 +362,25 @@ int kvc_eigh(const float* S, int32_t n, float* lambda, float* U, int32_t* sweeps
  */
 int kvc_query_variance(const float* U, const float* S_q, int32_t n_heads, int32_t G, float* sigma2_q,
                        void* stream);
+
+/*
+ * kvc_measured_quant - the quantization term of the measured distortion tables on the device: for every
+ * head h, candidate rank r (grid r_min, r_min + r_step, ..., <= d) and width b = 1..8,
+ *   quant[h][ri][b-1] = (1/n_tok) sum_t sum_k c_k (z_tk - zhat_tk)^2,  z_t = P_r x_t,
+ * zhat the dequantized b-bit code of z with the candidate's step (fp32 projection of the exact fp16
+ * products; a measurement, so codes are decided in fp32).
+ *  x          device fp16 [n_heads][...] calibration activations, head h at x + h * x_head_stride, n_tok
+ *             rows of d; 16-byte aligned, stride a multiple of 8 and >= n_tok * d.
+ *  P_all, delta_all, row_w_all  device copies of kvc_make_candidates' outputs, one head after another
+ *             (P_head_stride elements, a multiple of 8, between heads' bases; delta [n_heads][n_r][8];
+ *             rw_head_stride floats between heads' row weights).
+ *  quant      device f32 [n_heads][n_r][8] out.
+ * Async on `stream`.
+ */
+int kvc_measured_quant(const uint16_t* x, int64_t x_head_stride, int32_t n_heads, int32_t n_tok,
+                       const uint16_t* P_all, int64_t P_head_stride, const float* delta_all,
+                       const float* row_w_all, int64_t rw_head_stride, int32_t r_min, int32_t r_step,
+                       float* quant, void* stream);
 
 /* Message of the last failing call on this thread ("" if none). */
 const char* kvc_last_error(void);

@@ -16,6 +16,8 @@
 //    x - s (y + tau x) form (Rutishauser), which keeps the rounding of the diagonal small.
 //  * query_variance_kernel: sigma^2_Q,i = (1/G) sum_g u_i^T Sigma_Q,g u_i, U and Sigma_Q,g staged
 //    in LDS, one thread per (column i, half of the rows).
+//  * measured_quant_kernel: the quantization term of the measured distortion tables (Appendix D,
+//    exact DP over measured distortion) for every candidate rank and width.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -291,6 +293,86 @@ __global__ __launch_bounds__(256) void query_variance_kernel(const float* __rest
     if (tid < kD) sig[(int64_t)h * kD + tid] = (part[0][tid] + part[1][tid]) / (float)G;
 }
 
+// ---------------------------------------------------------------- measured quantization error
+
+// Quantization term of the measured distortion table, one block per (rank on the grid, head): the
+// candidate basis P_r (fp16, staged in LDS) projects every calibration token (fp32 accumulation of
+// the exact fp16 products, v_dot2_f32_f16), each projected coordinate is quantized at every width
+// b = 1..8 with its step, and c_k (z - zhat)^2 accumulates per width; the block's sums over its
+// tokens give mean_t sum_k c_k (z_tk - zhat_tk)^2.
+constexpr int kMqThreads = 256;
+typedef _Float16 mq_h2 __attribute__((ext_vector_type(2)));
+
+__global__ __launch_bounds__(kMqThreads) void measured_quant_kernel(
+    const uint16_t* __restrict__ x, int64_t x_head_stride, int n_tok, const uint16_t* __restrict__ P_all,
+    int64_t P_head_stride, const float* __restrict__ delta_all, const float* __restrict__ row_w_all,
+    int64_t rw_head_stride, int r_min, int r_step, int n_r, float* __restrict__ quant) {
+    __shared__ __attribute__((aligned(16))) uint16_t Ps[kD * kD];
+    __shared__ float cw[kD];
+    __shared__ float red[8][kMqThreads / 64];
+    const int ri = blockIdx.x, h = blockIdx.y, tid = threadIdx.x;
+    const int r = r_min + ri * r_step;
+    // offset of rank r's records: sum of the ranks before it
+    const int64_t before = (int64_t)ri * r_min + (int64_t)r_step * ri * (ri - 1) / 2;
+    const uint16_t* __restrict__ P = P_all + (int64_t)h * P_head_stride + before * kD;
+    const float* __restrict__ c = row_w_all + (int64_t)h * rw_head_stride + before;
+    for (int e = tid; e < r * kD / 8; e += kMqThreads)
+        reinterpret_cast<uint4*>(Ps)[e] = reinterpret_cast<const uint4*>(P)[e];
+    for (int k = tid; k < r; k += kMqThreads) cw[k] = c[k];
+    float st[8], inv[8];
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+        st[b] = delta_all[((int64_t)h * n_r + ri) * 8 + b];
+        inv[b] = 1.f / st[b];
+    }
+    __syncthreads();
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    const uint16_t* __restrict__ xh = x + (int64_t)h * x_head_stride;
+    for (int t = tid; t < n_tok; t += kMqThreads) {
+        mq_h2 xv[kD / 2];
+#pragma unroll
+        for (int q = 0; q < kD / 8; ++q) {
+            const uint4 w = reinterpret_cast<const uint4*>(xh + (int64_t)t * kD)[q];
+            xv[4 * q] = __builtin_bit_cast(mq_h2, w.x);
+            xv[4 * q + 1] = __builtin_bit_cast(mq_h2, w.y);
+            xv[4 * q + 2] = __builtin_bit_cast(mq_h2, w.z);
+            xv[4 * q + 3] = __builtin_bit_cast(mq_h2, w.w);
+        }
+        for (int k = 0; k < r; ++k) {
+            float z = 0.f;
+            const uint4* Pk = reinterpret_cast<const uint4*>(Ps + k * kD);
+#pragma unroll
+            for (int q = 0; q < kD / 8; ++q) {
+                const uint4 w = Pk[q];
+                z = __builtin_amdgcn_fdot2(__builtin_bit_cast(mq_h2, w.x), xv[4 * q], z, false);
+                z = __builtin_amdgcn_fdot2(__builtin_bit_cast(mq_h2, w.y), xv[4 * q + 1], z, false);
+                z = __builtin_amdgcn_fdot2(__builtin_bit_cast(mq_h2, w.z), xv[4 * q + 2], z, false);
+                z = __builtin_amdgcn_fdot2(__builtin_bit_cast(mq_h2, w.w), xv[4 * q + 3], z, false);
+            }
+            const float ck = cw[k];
+#pragma unroll
+            for (int b = 0; b < 8; ++b) {
+                const float hb = (float)(1 << b);  // 2^(b+1-1) for width b + 1
+                const float code = fminf(fmaxf(floorf(z * inv[b]) + hb, 0.f), 2.f * hb - 1.f);
+                const float e = z - (code - hb + 0.5f) * st[b];
+                acc[b] = fmaf(ck * e, e, acc[b]);
+            }
+        }
+    }
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+        float v = acc[b];
+        for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+        if ((tid & 63) == 0) red[b][tid >> 6] = v;
+    }
+    __syncthreads();
+    if (tid < 8) {
+        float v = 0.f;
+        for (int w = 0; w < kMqThreads / 64; ++w) v += red[tid][w];
+        quant[((int64_t)h * n_r + ri) * 8 + tid] = v / (float)n_tok;
+    }
+}
+
 int check_launch_calib(const char* what) {
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return set_error(KVC_EDEVICE, "%s: %s", what, hipGetErrorString(e));
@@ -332,6 +414,30 @@ extern "C" int kvc_eigh(const float* S, int32_t n, float* lambda, float* U, int3
     if (int e = set_big_lds((const void*)eigh_kernel, smem, "kvc_eigh")) return e;
     hipLaunchKernelGGL(eigh_kernel, dim3(n), dim3(kEighThreads), smem, (hipStream_t)stream, S, lambda, U, sweeps);
     return check_launch_calib("kvc_eigh");
+}
+
+extern "C" int kvc_measured_quant(const uint16_t* x, int64_t x_head_stride, int32_t n_heads, int32_t n_tok,
+                                  const uint16_t* P_all, int64_t P_head_stride, const float* delta_all,
+                                  const float* row_w_all, int64_t rw_head_stride, int32_t r_min, int32_t r_step,
+                                  float* quant, void* stream) {
+    clear_error();
+    if (n_heads < 0 || n_tok < 1) return set_error(KVC_EINVAL, "kvc_measured_quant: n_heads < 0 or n_tok < 1");
+    if (n_heads == 0) return KVC_OK;
+    if (!x || !P_all || !delta_all || !row_w_all || !quant) return set_error(KVC_EINVAL, "kvc_measured_quant: null pointer");
+    if (r_min < 2 || r_step < 2 || (r_min & 1) || (r_step & 1) || r_min > kD)
+        return set_error(KVC_EUNSUPPORTED, "kvc_measured_quant: rank grid (%d, %d) must be even, r_min <= d", r_min, r_step);
+    const int n_r = (kD - r_min) / r_step + 1;
+    const int64_t sum_r = (int64_t)n_r * r_min + (int64_t)r_step * n_r * (n_r - 1) / 2;
+    if ((reinterpret_cast<uintptr_t>(x) & 15) || (x_head_stride & 7) || x_head_stride < (int64_t)n_tok * kD)
+        return set_error(KVC_EINVAL, "kvc_measured_quant: x must be 16-byte aligned, head stride a multiple of 8 and >= n_tok * d");
+    if ((reinterpret_cast<uintptr_t>(P_all) & 15) || (P_head_stride & 7) || P_head_stride < sum_r * kD)
+        return set_error(KVC_EINVAL, "kvc_measured_quant: P_all must be 16-byte aligned, its head stride a multiple of 8 "
+                                     "and >= the candidate bases of one head");
+    if (rw_head_stride < sum_r) return set_error(KVC_EINVAL, "kvc_measured_quant: row-weight head stride too small");
+    hipLaunchKernelGGL(measured_quant_kernel, dim3(n_r, n_heads), dim3(kMqThreads), 0, (hipStream_t)stream, x,
+                       x_head_stride, n_tok, P_all, P_head_stride, delta_all, row_w_all, rw_head_stride, r_min, r_step,
+                       n_r, quant);
+    return check_launch_calib("kvc_measured_quant");
 }
 
 extern "C" int kvc_query_variance(const float* U, const float* S_q, int32_t n_heads, int32_t G, float* sigma2_q,

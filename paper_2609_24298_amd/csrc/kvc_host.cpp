@@ -97,6 +97,80 @@ C1Result c1(const Head& h, double B, const kvc_alloc_opts& o) {
     return best;
 }
 
+// Exact DP (Appendix D) over integer budgets beta_h in [ceil(B_min), floor(B_max)], sum <= floor(B_tot),
+// for a per-head optimum opt(h, beta) that is non-increasing in beta. The running table is
+// non-increasing in the total, so only the budgets where D*_h drops (plus the lowest one) can be the
+// smallest minimiser: scanning those in ascending order with a strict comparison picks the same beta_h
+// as scanning all.
+template <class Opt>
+int dp_solve(int N, const kvc_alloc_opts& o, double B_tot, Opt opt, kvc_head_alloc* out, const char* fn) {
+    const int64_t lo = (int64_t)std::ceil(o.B_min), hi = (int64_t)std::floor(o.B_max);
+    const int64_t cap = (int64_t)std::floor(B_tot);
+    if (lo < 0 || hi < lo) return set_error(KVC_EINVAL, "%s: empty DP budget range", fn);
+    if (cap > (int64_t)1 << 26) return set_error(KVC_EINVAL, "%s: DP budget too large", fn);
+    if ((int64_t)N * lo > cap) return set_error(KVC_EINVAL, "%s: B_tot below n_heads * B_min", fn);
+    const double INF = std::numeric_limits<double>::infinity();
+    std::vector<std::vector<int32_t>> bp_beta(N);
+    std::vector<std::vector<double>> bp_D(N);
+    for (int h = 0; h < N; ++h) {
+        double prevD = 0.0;
+        for (int64_t beta = lo; beta <= hi; ++beta) {
+            const double D = opt(h, (double)beta).D;
+            if (beta == lo || D < prevD) {
+                bp_beta[h].push_back((int32_t)beta);
+                bp_D[h].push_back(D);
+            }
+            prevD = D;
+        }
+    }
+    std::vector<double> prev(cap + 1, 0.0), cur(cap + 1);
+    std::vector<int32_t> choice((size_t)N * (cap + 1));
+    for (int h = 0; h < N; ++h) {
+        const int32_t* bb = bp_beta[h].data();
+        const double* bd = bp_D[h].data();
+        const int nb = (int)bp_beta[h].size();
+        int32_t* ch = choice.data() + (size_t)h * (cap + 1);
+        for (int64_t tot = 0; tot <= cap; ++tot) {
+            double best = INF;
+            int32_t arg = -1;
+            for (int k = 0; k < nb && bb[k] <= tot; ++k) {
+                const double base = prev[tot - bb[k]];
+                if (base == INF) continue;
+                const double v = base + bd[k];
+                if (v < best) { best = v; arg = bb[k]; }
+            }
+            cur[tot] = best;
+            ch[tot] = arg;
+        }
+        std::swap(prev, cur);
+    }
+    if (prev[cap] == INF) return set_error(KVC_EINVAL, "%s: DP found no feasible allocation", fn);
+    int64_t tot = cap;
+    for (int h = N - 1; h >= 0; --h) {
+        const int32_t beta = choice[(size_t)h * (cap + 1) + tot];
+        C1Result a = opt(h, (double)beta);
+        out[h] = {a.r, a.b, (double)beta, a.D};
+        tot -= beta;
+    }
+    return KVC_OK;
+}
+
+// Per-head optimum over a table D[ri][bi] (r = r_min + ri r_step, b = b_min + bi): the smallest D
+// over every grid pair with r b <= B, ties at the smallest r, then the smallest b; below the smallest
+// pair, (r_min, b_min).
+C1Result c1_table(const double* D, int n_r, int n_b, double B, const kvc_alloc_opts& o) {
+    C1Result best{-1, -1, 0.0};
+    for (int ri = 0; ri < n_r; ++ri) {
+        const int r = o.r_min + ri * o.r_step;
+        for (int bi = 0; bi < n_b; ++bi) {
+            const int b = o.b_min + bi;
+            if ((double)r * b <= B && (best.r < 0 || D[ri * n_b + bi] < best.D)) best = {r, b, D[ri * n_b + bi]};
+        }
+    }
+    if (best.r < 0) best = {o.r_min, o.b_min, D[0]};
+    return best;
+}
+
 int check_opts(const kvc_alloc_opts* o) {
     if (!o) return set_error(KVC_EINVAL, "kvc_allocate: null options");
     if (o->d < 2 || o->d > 4096) return set_error(KVC_EINVAL, "kvc_allocate: d = %d", o->d);
@@ -203,60 +277,42 @@ extern "C" int kvc_allocate(const double* lambda, const double* sigma2_q, int32_
         return KVC_OK;
     }
 
-    // Exact DP (Appendix D) over integer budgets beta_h in [ceil(B_min), floor(B_max)],
-    // sum <= floor(B_tot). D*_h(beta) = C1(beta) is a step function of beta, and the
-    // running table is non-increasing in the total, so only the budgets where D*_h
-    // drops (plus the lowest one) can be the smallest minimiser: scanning those in
-    // ascending order with a strict comparison picks the same beta_h as scanning all.
-    const int64_t lo = (int64_t)std::ceil(bmin), hi = (int64_t)std::floor(o.B_max);
-    const int64_t cap = (int64_t)std::floor(B_tot);
-    if (lo < 0 || hi < lo) return set_error(KVC_EINVAL, "kvc_allocate: empty DP budget range");
-    if (cap > (int64_t)1 << 26) return set_error(KVC_EINVAL, "kvc_allocate: DP budget too large");
-    if ((int64_t)N * lo > cap) return set_error(KVC_EINVAL, "kvc_allocate: B_tot below n_heads * B_min");
-    const double INF = std::numeric_limits<double>::infinity();
-    std::vector<std::vector<int32_t>> bp_beta(N);
-    std::vector<std::vector<double>> bp_D(N);
+    // Exact DP (Appendix D).
+    return dp_solve(N, o, B_tot, [&](int h, double beta) { return c1(heads[h], beta, o); }, out, "kvc_allocate");
+}
+
+extern "C" int kvc_allocate_measured(const double* quant, const double* trunc_w, const int32_t* order,
+                                     int32_t n_heads, const kvc_alloc_opts* opts, kvc_head_alloc* out) {
+    clear_error();
+    if (int e = check_opts(opts)) return e;
+    const kvc_alloc_opts& o = *opts;
+    if (n_heads <= 0 || !quant || !trunc_w || !order || !out)
+        return set_error(KVC_EINVAL, "kvc_allocate_measured: null input or n_heads <= 0");
+    const int N = n_heads, d = o.d;
+    const int n_r = (d - o.r_min) / o.r_step + 1, n_b = o.b_max - o.b_min + 1;
+    // D[h][ri][bi] = T[r] + quant[h][ri][bi], T[r] the measured truncation term summed from the last
+    // importance position down
+    std::vector<double> D((size_t)N * n_r * n_b);
+    std::vector<double> T(d + 1);
     for (int h = 0; h < N; ++h) {
-        double prevD = 0.0;
-        for (int64_t beta = lo; beta <= hi; ++beta) {
-            const double D = c1(heads[h], (double)beta, o).D;
-            if (beta == lo || D < prevD) {
-                bp_beta[h].push_back((int32_t)beta);
-                bp_D[h].push_back(D);
-            }
-            prevD = D;
+        T[d] = 0.0;
+        for (int p = d - 1; p >= 0; --p) {
+            const int i = order[(int64_t)h * d + p];
+            if (i < 0 || i >= d) return set_error(KVC_EINVAL, "kvc_allocate_measured: order out of range (head %d)", h);
+            T[p] = T[p + 1] + trunc_w[(int64_t)h * d + i];
         }
-    }
-    std::vector<double> prev(cap + 1, 0.0), cur(cap + 1);
-    std::vector<int32_t> choice((size_t)N * (cap + 1));
-    for (int h = 0; h < N; ++h) {
-        const int32_t* bb = bp_beta[h].data();
-        const double* bd = bp_D[h].data();
-        const int nb = (int)bp_beta[h].size();
-        int32_t* ch = choice.data() + (size_t)h * (cap + 1);
-        for (int64_t tot = 0; tot <= cap; ++tot) {
-            double best = INF;
-            int32_t arg = -1;
-            for (int k = 0; k < nb && bb[k] <= tot; ++k) {
-                const double base = prev[tot - bb[k]];
-                if (base == INF) continue;
-                const double v = base + bd[k];
-                if (v < best) { best = v; arg = bb[k]; }
+        for (int ri = 0; ri < n_r; ++ri)
+            for (int bi = 0; bi < n_b; ++bi) {
+                const double q = quant[((int64_t)h * n_r + ri) * n_b + bi];
+                const double v = T[o.r_min + ri * o.r_step] + q;
+                if (!std::isfinite(v)) return set_error(KVC_EINVAL, "kvc_allocate_measured: non-finite table (head %d)", h);
+                D[((size_t)h * n_r + ri) * n_b + bi] = v;
             }
-            cur[tot] = best;
-            ch[tot] = arg;
-        }
-        std::swap(prev, cur);
     }
-    if (prev[cap] == INF) return set_error(KVC_EINVAL, "kvc_allocate: DP found no feasible allocation");
-    int64_t tot = cap;
-    for (int h = N - 1; h >= 0; --h) {
-        const int32_t beta = choice[(size_t)h * (cap + 1) + tot];
-        C1Result a = c1(heads[h], (double)beta, o);
-        out[h] = {a.r, a.b, (double)beta, a.D};
-        tot -= beta;
-    }
-    return KVC_OK;
+    const double B_tot = o.bpd * (double)((int64_t)N * d);
+    return dp_solve(N, o, B_tot,
+                    [&](int h, double beta) { return c1_table(D.data() + (size_t)h * n_r * n_b, n_r, n_b, beta, o); },
+                    out, "kvc_allocate_measured");
 }
 
 // ------------------------------------------------------------------ basis
@@ -296,18 +352,12 @@ std::vector<int> block_sizes(int r) {
 
 }  // namespace
 
-extern "C" int kvc_make_basis(const double* U, const int32_t* order, const double* lambda, int32_t d,
-                              int32_t r, int32_t b, const int8_t* sign, uint16_t* P, float* delta) {
-    clear_error();
-    if (!U || !order || !lambda || !sign || !P || !delta) return set_error(KVC_EINVAL, "kvc_make_basis: null pointer");
-    if (d < 2 || r < 2 || r > d || (r & 1)) return set_error(KVC_EUNSUPPORTED, "kvc_make_basis: r = %d, d = %d", r, d);
-    if (b < 1 || b > 8) return set_error(KVC_EUNSUPPORTED, "kvc_make_basis: b = %d", b);
-    for (int i = 0; i < r; ++i) {
-        if (order[i] < 0 || order[i] >= d) return set_error(KVC_EINVAL, "kvc_make_basis: order[%d] = %d", i, order[i]);
-        if (sign[i] != 1 && sign[i] != -1) return set_error(KVC_EINVAL, "kvc_make_basis: sign[%d] not +-1", i);
-    }
-    // Deal importance positions to the Hadamard blocks by largest remaining quota.
-    const std::vector<int> sizes = block_sizes(r);
+namespace kvc {
+namespace {
+
+// Importance positions 0..r-1 dealt to the Hadamard blocks (binary expansion of r, largest first): position
+// i goes to the block with the largest remaining quota (i + 1) n_j - r count_j, ties to the larger block.
+std::vector<std::vector<int>> deal_blocks(int r, const std::vector<int>& sizes) {
     const int nblk = (int)sizes.size();
     std::vector<std::vector<int>> members(nblk);
     std::vector<int> count(nblk, 0);
@@ -322,9 +372,25 @@ extern "C" int kvc_make_basis(const double* U, const int32_t* order, const doubl
         members[best].push_back(i);
         ++count[best];
     }
-    // P rows of block j: (1/sqrt(n)) sum_c H_n[a][c] sign[i_c] u_{order[i_c]}, c ascending.
+    return members;
+}
+
+int check_basis_args(const char* fn, const double* U, const int32_t* order, const double* lambda, int32_t d, int32_t r,
+                     const int8_t* sign) {
+    if (!U || !order || !lambda || !sign) return set_error(KVC_EINVAL, "%s: null pointer", fn);
+    if (d < 2 || r < 2 || r > d || (r & 1)) return set_error(KVC_EUNSUPPORTED, "%s: r = %d, d = %d", fn, r, d);
+    for (int i = 0; i < r; ++i) {
+        if (order[i] < 0 || order[i] >= d) return set_error(KVC_EINVAL, "%s: order[%d] = %d", fn, i, order[i]);
+        if (sign[i] != 1 && sign[i] != -1) return set_error(KVC_EINVAL, "%s: sign[%d] not +-1", fn, i);
+    }
+    return KVC_OK;
+}
+
+// P rows of block j: (1/sqrt(n)) sum_c H_n[a][c] sign[i_c] u_{order[i_c]}, c ascending, rounded to fp16.
+void build_basis(const double* U, const int32_t* order, int32_t d, int32_t r, const int8_t* sign,
+                 const std::vector<int>& sizes, const std::vector<std::vector<int>>& members, uint16_t* P) {
     int row0 = 0;
-    for (int j = 0; j < nblk; ++j) {
+    for (size_t j = 0; j < sizes.size(); ++j) {
         const int n = sizes[j];
         const double inv = 1.0 / std::sqrt((double)n);
         for (int a = 0; a < n; ++a) {
@@ -340,14 +406,60 @@ extern "C" int kvc_make_basis(const double* U, const int32_t* order, const doubl
         }
         row0 += n;
     }
-    // Step: sqrt of the mean retained variance times delta_b (Appendix A.1).
+}
+
+// Step: sqrt of the mean retained variance times delta_b (Appendix A.1).
+int step_of(const double* lambda, const int32_t* order, int32_t r, int32_t b, float* delta, const char* fn) {
     double s = 0.0;
     for (int i = 0; i < r; ++i) s = s + lambda[order[i]];
     const double sigma2 = s / r;
     const float st = (float)(std::sqrt(sigma2) * kStep[b]);
     if (!(st >= std::ldexp(1.0f, -24) && st <= std::ldexp(1.0f, 24)))
-        return set_error(KVC_EUNSUPPORTED, "kvc_make_basis: step %g outside [2^-24, 2^24]", (double)st);
+        return set_error(KVC_EUNSUPPORTED, "%s: step %g outside [2^-24, 2^24]", fn, (double)st);
     *delta = st;
+    return KVC_OK;
+}
+
+}  // namespace
+}  // namespace kvc
+
+extern "C" int kvc_make_basis(const double* U, const int32_t* order, const double* lambda, int32_t d,
+                              int32_t r, int32_t b, const int8_t* sign, uint16_t* P, float* delta) {
+    clear_error();
+    if (!P || !delta) return set_error(KVC_EINVAL, "kvc_make_basis: null pointer");
+    if (int e = check_basis_args("kvc_make_basis", U, order, lambda, d, r, sign)) return e;
+    if (b < 1 || b > 8) return set_error(KVC_EUNSUPPORTED, "kvc_make_basis: b = %d", b);
+    const std::vector<int> sizes = block_sizes(r);
+    build_basis(U, order, d, r, sign, sizes, deal_blocks(r, sizes), P);
+    return step_of(lambda, order, r, b, delta, "kvc_make_basis");
+}
+
+extern "C" int kvc_make_candidates(const double* U, const int32_t* order, const double* lambda, const double* wt,
+                                   int32_t d, const int8_t* sign, int32_t r_min, int32_t r_step, uint16_t* P_all,
+                                   float* delta_all, float* row_w_all) {
+    clear_error();
+    if (!wt || !P_all || !delta_all || !row_w_all) return set_error(KVC_EINVAL, "kvc_make_candidates: null pointer");
+    if (r_min < 2 || r_step < 2 || (r_min & 1) || (r_step & 1) || r_min > d)
+        return set_error(KVC_EUNSUPPORTED, "kvc_make_candidates: rank grid (%d, %d) must be even", r_min, r_step);
+    if (int e = check_basis_args("kvc_make_candidates", U, order, lambda, d, d - (d - r_min) % r_step, sign)) return e;
+    int64_t po = 0, wo = 0;
+    for (int r = r_min, ri = 0; r <= d; r += r_step, ++ri) {
+        const std::vector<int> sizes = block_sizes(r);
+        const std::vector<std::vector<int>> members = deal_blocks(r, sizes);
+        build_basis(U, order, d, r, sign, sizes, members, P_all + po);
+        for (int b = 1; b <= 8; ++b)
+            if (int e = step_of(lambda, order, r, b, delta_all + (int64_t)ri * 8 + (b - 1), "kvc_make_candidates")) return e;
+        int row = 0;
+        for (size_t j = 0; j < sizes.size(); ++j) {
+            double s = 0.0;
+            for (int i : members[j]) s = s + wt[order[i]];
+            const float c = (float)(s / sizes[j]);
+            for (int a = 0; a < sizes[j]; ++a) row_w_all[wo + row + a] = c;
+            row += sizes[j];
+        }
+        po += (int64_t)r * d;
+        wo += r;
+    }
     return KVC_OK;
 }
 

@@ -78,6 +78,10 @@ def lib():
         L.kvc_read_probe.argtypes = [_p, ctypes.c_size_t, _p, _p]
         L.kvc_encode_kv.argtypes = [ctypes.POINTER(StreamDesc), ctypes.POINTER(StreamDesc), _p, ctypes.c_int64, _p,
                                     ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, _p]
+        L.kvc_allocate_measured.argtypes = [_p, _p, _p, ctypes.c_int32, ctypes.POINTER(AllocOpts), _p]
+        L.kvc_make_candidates.argtypes = [_p, _p, _p, _p, ctypes.c_int32, _p, ctypes.c_int32, ctypes.c_int32, _p, _p, _p]
+        L.kvc_measured_quant.argtypes = [_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, _p, ctypes.c_int64, _p, _p,
+                                         ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, _p, _p]
         L.kvc_covariance.argtypes = [_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _p, _p]
         L.kvc_eigh.argtypes = [_p, ctypes.c_int32, _p, _p, _p, _p]
         L.kvc_query_variance.argtypes = [_p, _p, ctypes.c_int32, ctypes.c_int32, _p, _p]
@@ -118,6 +122,40 @@ def kvc_allocate(lam: np.ndarray, sigma2_q: np.ndarray | None, opts: AllocOpts):
                               ctypes.cast(out, ctypes.c_void_p), _np_ptr(order)))
     return {"r": np.array([h.r for h in out], dtype=np.int32), "b": np.array([h.b for h in out], dtype=np.int32),
             "B": np.array([h.B for h in out]), "D": np.array([h.D for h in out]), "order": order}
+
+
+def kvc_allocate_measured(quant: np.ndarray, trunc_w: np.ndarray, order: np.ndarray, opts: AllocOpts):
+    """quant (n_heads, n_r, n_b), trunc_w (n_heads, d), order (n_heads, d) -> dict of r, b, B, D arrays."""
+    quant = np.ascontiguousarray(quant, dtype=np.float64)
+    trunc_w = np.ascontiguousarray(trunc_w, dtype=np.float64)
+    order = np.ascontiguousarray(order, dtype=np.int32)
+    n = quant.shape[0]
+    out = (HeadAlloc * n)()
+    _check(lib().kvc_allocate_measured(_np_ptr(quant), _np_ptr(trunc_w), _np_ptr(order), n, ctypes.byref(opts),
+                                       ctypes.cast(out, ctypes.c_void_p)))
+    return {"r": np.array([h.r for h in out], dtype=np.int32), "b": np.array([h.b for h in out], dtype=np.int32),
+            "B": np.array([h.B for h in out]), "D": np.array([h.D for h in out])}
+
+
+def rank_grid(r_min: int = 2, r_step: int = 2, d: int = HEAD_DIM):
+    return list(range(r_min, d + 1, r_step))
+
+
+def kvc_make_candidates(U: np.ndarray, order: np.ndarray, lam: np.ndarray, wt: np.ndarray, sign: np.ndarray,
+                        r_min: int = 2, r_step: int = 2):
+    """Candidate records of one head: (P_all fp16 bits, delta_all (n_r, 8), row_w_all)."""
+    U = np.ascontiguousarray(U, dtype=np.float64)
+    d = U.shape[0]
+    ranks = rank_grid(r_min, r_step, d)
+    P = np.zeros(sum(ranks) * d, dtype=np.uint16)
+    dl = np.zeros((len(ranks), 8), dtype=np.float32)
+    rw = np.zeros(sum(ranks), dtype=np.float32)
+    _check(lib().kvc_make_candidates(_np_ptr(U), _np_ptr(np.ascontiguousarray(order, dtype=np.int32)),
+                                     _np_ptr(np.ascontiguousarray(lam, dtype=np.float64)),
+                                     _np_ptr(np.ascontiguousarray(wt, dtype=np.float64)), d,
+                                     _np_ptr(np.ascontiguousarray(sign, dtype=np.int8)), r_min, r_step, _np_ptr(P),
+                                     _np_ptr(dl), _np_ptr(rw)))
+    return P, dl, rw
 
 
 def kvc_make_basis(U: np.ndarray, order: np.ndarray, lam: np.ndarray, r: int, b: int, sign: np.ndarray):
@@ -346,3 +384,20 @@ def kvc_query_variance(U, S_q, sig, stream=None):
     assert U.shape == (n, HEAD_DIM, HEAD_DIM) and S_q.shape == (n, G, HEAD_DIM, HEAD_DIM) and sig.shape == (n, HEAD_DIM)
     _check(lib().kvc_query_variance(ctypes.c_void_p(U.data_ptr()), ctypes.c_void_p(S_q.data_ptr()), int(n), int(G),
                                     ctypes.c_void_p(sig.data_ptr()), _stream_ptr(stream)))
+
+
+def kvc_measured_quant(x, n_tok: int, P_all, delta_all, row_w_all, quant, r_min: int = 2, r_step: int = 2,
+                       stream=None):
+    """x fp16 (n_heads, >= n_tok, d); P_all int16/uint16 (n_heads, sum r * d); delta_all f32 (n_heads, n_r, 8);
+    row_w_all f32 (n_heads, sum r); quant f32 (n_heads, n_r, 8). All on the device."""
+    import torch
+    n = x.shape[0]
+    assert x.dtype == torch.float16 and x.is_contiguous() and x.dim() == 3 and x.shape[2] == HEAD_DIM
+    for t in (P_all, delta_all, row_w_all, quant):
+        assert t.is_contiguous() and t.shape[0] == n and t.device == x.device
+    assert delta_all.dtype == row_w_all.dtype == quant.dtype == torch.float32
+    _check(lib().kvc_measured_quant(ctypes.c_void_p(x.data_ptr()), int(x.stride(0)), int(n), int(n_tok),
+                                    ctypes.c_void_p(P_all.data_ptr()), int(P_all.stride(0)),
+                                    ctypes.c_void_p(delta_all.data_ptr()), ctypes.c_void_p(row_w_all.data_ptr()),
+                                    int(row_w_all.stride(0)), int(r_min), int(r_step),
+                                    ctypes.c_void_p(quant.data_ptr()), _stream_ptr(stream)))

@@ -83,9 +83,49 @@ class SideTables:
     delta: np.ndarray      # per head, float32
 
 
+def measured_tables(stats, x_cal, n_tok: int, side: int = kvc.SIDE_K, r_min: int = 2, r_step: int = 2,
+                    threads: int = 16):
+    """Measured distortion tables of every head (Appendix D, exact DP over measured distortion), for
+    kvc_allocate_measured: the candidate records on the host (kvc_make_candidates, heads in parallel
+    threads), the quantization term on the device (kvc_measured_quant over the calibration activations
+    x_cal, fp16 (H, >= n_tok, d) on the device), and the truncation term from the measured variance along
+    each eigendirection (kvc_covariance without centring, then kvc_query_variance with G = 1). The K side
+    weighs with sigma2_q (the attention-KL objective), the V side with 1 (MSE).
+    Returns (quant (H, n_r, 8), trunc_w (H, d), order (H, d))."""
+    import concurrent.futures as cf
+
+    import torch
+    dev = x_cal.device
+    H, d = len(stats), stats[0].lam_k.shape[0]
+    lam = np.stack([s.lam_k if side == kvc.SIDE_K else s.lam_v for s in stats])
+    U = np.stack([s.U_k if side == kvc.SIDE_K else s.U_v for s in stats])
+    wt = np.stack([s.sigma2_q for s in stats]) if side == kvc.SIDE_K else np.ones((H, d))
+    sq = wt if side == kvc.SIDE_K else None
+    order = kvc.kvc_allocate(lam, sq, kvc.alloc_opts(1.0, kvc.SOLVER_C1_ONLY))["order"]
+    sign = [s.sign_k if side == kvc.SIDE_K else s.sign_v for s in stats]
+    with cf.ThreadPoolExecutor(max_workers=threads) as ex:  # the host calls release the GIL
+        cands = list(ex.map(lambda h: kvc.kvc_make_candidates(U[h], order[h], lam[h], wt[h], sign[h], r_min, r_step),
+                            range(H)))
+    P_all = torch.as_tensor(np.stack([c[0] for c in cands]).view(np.int16), device=dev)
+    delta_all = torch.as_tensor(np.stack([c[1] for c in cands]), device=dev)
+    rw_all = torch.as_tensor(np.stack([c[2] for c in cands]), device=dev)
+    n_r = delta_all.shape[1]
+    quant = torch.empty((H, n_r, 8), dtype=torch.float32, device=dev)
+    kvc.kvc_measured_quant(x_cal, n_tok, P_all, delta_all, rw_all, quant, r_min, r_step)
+    C = torch.empty((H, d, d), dtype=torch.float32, device=dev)
+    kvc.kvc_covariance(x_cal, n_tok, C, centered=False)
+    lam_hat = torch.empty((H, d), dtype=torch.float32, device=dev)
+    kvc.kvc_query_variance(torch.as_tensor(U.astype(np.float32), device=dev), C.view(H, 1, d, d), lam_hat)
+    trunc_w = wt * lam_hat.cpu().numpy().astype(np.float64)
+    return quant.cpu().numpy().astype(np.float64), trunc_w, order
+
+
 def allocate_workload(w: synth.Workload, stats, bpd: float | None = None, solver: int = kvc.SOLVER_DAMPED,
-                      uniform=None):
+                      uniform=None, measured=None):
     """Joint K+V tables: K with attention-KL weights and C1+C2, V with MSE weights and C1 only.
+
+    measured = (quant, trunc_w, order) from measured_tables takes the K side from the exact DP over
+    measured distortion tables instead of C1 + C2 on the model.
 
     uniform = (r_K, b_K, r_V, b_V) replaces the allocator's (r, b) by one pair per side for every head
     (the coordinate order and the bases are still built per head): a measurement case that isolates
@@ -96,6 +136,10 @@ def allocate_workload(w: synth.Workload, stats, bpd: float | None = None, solver
     lam_v = np.stack([s.lam_v for s in stats])
     ak = kvc.kvc_allocate(lam_k, sq, kvc.alloc_opts(bpd, solver))
     av = kvc.kvc_allocate(lam_v, None, kvc.alloc_opts(bpd, kvc.SOLVER_C1_ONLY))
+    if measured is not None:  # K side from the exact DP over measured tables (quant, trunc_w, order)
+        quant, trunc_w, order = measured
+        am = kvc.kvc_allocate_measured(quant, trunc_w, order, kvc.alloc_opts(bpd))
+        ak = {"r": am["r"], "b": am["b"], "B": am["B"], "D": am["D"], "order": order}
     if uniform is not None:
         rk, bk, rv, bv = (int(x) for x in uniform)
         for a, r, b in ((ak, rk, bk), (av, rv, bv)):
@@ -151,13 +195,14 @@ class Cache:
     """A compressed K/V cache for a workload plus its decode buffers."""
 
     def __init__(self, w: synth.Workload, seed: int = 0, device="cuda", bpd: float | None = None,
-                 capacity: int | None = None, solver: int = kvc.SOLVER_DAMPED, stats=None, uniform=None):
+                 capacity: int | None = None, solver: int = kvc.SOLVER_DAMPED, stats=None, uniform=None,
+                 measured=None):
         import torch
         self.w = w
         self.seed = seed
         self.device = torch.device(device)
         self.stats = calibrate(synth.workload_covs(w, seed), device) if stats is None else stats
-        self.k_tab, self.v_tab = allocate_workload(w, self.stats, bpd, solver, uniform)
+        self.k_tab, self.v_tab = allocate_workload(w, self.stats, bpd, solver, uniform, measured)
         self.capacity = w.tokens if capacity is None else capacity
         self.K = build_side(kvc.SIDE_K, self.k_tab, w, self.capacity, device)
         self.V = build_side(kvc.SIDE_V, self.v_tab, w, self.capacity, device)

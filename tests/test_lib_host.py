@@ -268,3 +268,51 @@ def test_noalloc_scratch_size_matches_header():
     src = open(os.path.join(ROOT, "include", "kvc.h")).read()
     m = re.search(r"#define KVC_NOALLOC_SCRATCH_BYTES \((\d+)ll << (\d+)\)", src)
     assert m and int(m.group(1)) << int(m.group(2)) == kvc.NOALLOC_SCRATCH_BYTES
+
+
+def test_make_candidates_bit_exact():
+    from oracle import measured as om
+    st = _stats(1)[3]
+    order = kvc.kvc_allocate(st.lam_k[None], st.sigma2_q[None], kvc.alloc_opts(2.0))["order"][0]
+    P_all, dl, rw = kvc.kvc_make_candidates(st.U_k, order, st.lam_k, st.sigma2_q, st.sign_k)
+    po = wo = 0
+    for ri, r in enumerate(kvc.rank_grid()):
+        if r in (2, 6, 16, 18, 48, 66, 100, 128):
+            for b in (1, 3, 8):
+                Pe, de = ob.make_basis(st.U_k, order, st.lam_k, r, b, st.sign_k)
+                assert np.array_equal(P_all[po:po + r * 128].reshape(r, 128), Pe), (r, b)
+                assert np.float32(dl[ri, b - 1]).tobytes() == np.float32(de).tobytes(), (r, b)
+            assert np.array_equal(rw[wo:wo + r], om.row_weights(r, order, st.sigma2_q).astype(np.float32)), r
+        po += r * 128
+        wo += r
+
+
+@pytest.mark.parametrize("bpd", [0.5, 1.0, 3.0])
+def test_allocate_measured_bit_exact(bpd):
+    # tables shaped like measured ones (noisy, not the model) on 12 heads; the oracle's exact DP over them
+    from oracle import measured as om
+    rng = np.random.default_rng(int(bpd * 7))
+    st = _stats(2)[:12]
+    ranks = kvc.rank_grid()
+    quant = np.zeros((12, len(ranks), 8))
+    tw = np.zeros((12, 128))
+    orders = []
+    for h, s in enumerate(st):
+        lam_hat = s.lam_k * rng.uniform(0.9, 1.1, 128)
+        tw[h] = s.sigma2_q * lam_hat
+        order = oa.importance_order(oa.kl_weights(s.lam_k, s.sigma2_q))
+        orders.append(order)
+        S = np.cumsum(tw[h][order])
+        for ri, r in enumerate(ranks):
+            for b in range(1, 9):
+                quant[h, ri, b - 1] = S[r - 1] * 2.0 ** (-2 * b) / 12 * rng.uniform(0.8, 2.0)
+    o = kvc.alloc_opts(bpd)
+    got = kvc.kvc_allocate_measured(quant, tw, np.array(orders, dtype=np.int32), o)
+    oo = _oracle_opts(o)
+    tables = []
+    for h in range(12):
+        T = om.truncation_terms(orders[h], tw[h], np.ones(128))
+        tables.append([[T[r] + quant[h, ri, b] for b in range(8)] for ri, r in enumerate(ranks)])
+    budgets, allocs, _ = oa.dp_tables(tables, oo)
+    assert np.array_equal(got["r"], [a[0] for a in allocs]) and np.array_equal(got["b"], [a[1] for a in allocs])
+    assert np.array_equal(got["B"], budgets) and np.array_equal(got["D"], [a[2] for a in allocs])
