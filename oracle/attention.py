@@ -15,6 +15,18 @@ Passages followed
   <q, P^T z> = <P q, z>, the logits are taken in the rank-r space here, and
   the value output is P_V^T (sum_t p_t z_V,t); both equal the dense
   computation on the reconstructed K and V (checked by a test).
+* Section 5 ("Scope"): keys are compressed before the rotary position
+  embedding. The attention of a model with RoPE then scores the query, rotated
+  at its position, against each reconstructed key rotated at the key's
+  position (decode_attention_rope); rank-space scoring no longer applies,
+  because the rotation depends on the position.
+
+Readings for RoPE (the paper does not restate it)
+--------------------------------------------------
+* The rotary embedding of the Llama family: coordinate pairs (j, j + d/2),
+  j < d/2, rotated by the angle p theta_j with theta_j = base^(-2 j / d);
+  the caller passes the query already rotated at its own position.
+* The key of stream index t sits at position t.
 """
 from __future__ import annotations
 
@@ -73,3 +85,27 @@ def brute_force_attention(q: np.ndarray, K: np.ndarray, V: np.ndarray) -> np.nda
     V = np.asarray(V, dtype=np.float64)
     s = (q @ K.T) / math.sqrt(q.shape[1])
     return softmax(s) @ V
+
+
+def rope_rotate(X: np.ndarray, positions, base: float) -> np.ndarray:
+    """Rows of X (n x d) rotated at their positions: pairs (j, j + d/2) by the angle p base^(-2j/d)."""
+    X = np.asarray(X, dtype=np.float64)
+    d = X.shape[1]
+    h = d // 2
+    theta = base ** (-2.0 * np.arange(h) / d)
+    ang = np.asarray(positions, dtype=np.float64)[:, None] * theta[None, :]
+    c, s = np.cos(ang), np.sin(ang)
+    a, b = X[:, :h], X[:, h:]
+    return np.concatenate([a * c - b * s, a * s + b * c], axis=1)
+
+
+def decode_attention_rope(codes_k, codes_v, Pk_bits, Pv_bits, step_k, step_v, b_k, b_v, q_rot_bits, seq_len, base):
+    """One decode step with RoPE: out[g] = P_V^T sum_t p_gt z_V,t, p = softmax_t(q'_g . rope(k_hat_t, t) / sqrt(d)),
+    k_hat_t = P_K^T z_K,t the reconstructed pre-RoPE key of stream index t and q'_g the rotated query (fp16 bits)."""
+    q = fp16_to_f64(q_rot_bits)
+    d = q.shape[1]
+    K = reconstruct(codes_k[:seq_len], Pk_bits, step_k, b_k)
+    s = (q @ rope_rotate(K, np.arange(seq_len), base).T) / math.sqrt(d)
+    p = softmax(s)
+    zv = dequantize(codes_v[:seq_len], step_v, b_v)
+    return (p @ zv) @ fp16_to_f64(Pv_bits)

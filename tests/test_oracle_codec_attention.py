@@ -266,3 +266,48 @@ def test_rank_space_attention_equals_dense_on_reconstruction():
     Vh = oatt.reconstruct(cv, Pv, stv, 2)[:321]
     ref = oatt.brute_force_attention(q.astype(np.float64), Kh, Vh)
     assert np.allclose(out, ref, rtol=1e-10, atol=1e-12)
+
+
+# ---------------------------------------------------------------- RoPE-aware decode (oracle)
+
+def test_rope_rotation_equals_complex_multiplication():
+    # pair (j, j + d/2) as the complex number x_j + i x_{j+d/2}, multiplied by exp(i p theta_j)
+    from oracle import attention as oatt
+    rng = np.random.default_rng(0)
+    X = rng.standard_normal((7, 128))
+    pos = np.array([0, 1, 5, 64, 1000, 32767, 131071])
+    base = 500000.0
+    Y = oatt.rope_rotate(X, pos, base)
+    z = (X[:, :64] + 1j * X[:, 64:]) * np.exp(1j * pos[:, None] * base ** (-np.arange(64) / 64.0)[None, :])
+    assert np.allclose(Y[:, :64], z.real, atol=1e-12) and np.allclose(Y[:, 64:], z.imag, atol=1e-12)
+    assert np.array_equal(oatt.rope_rotate(X, np.zeros(7), base), X)
+
+
+def test_rope_logits_depend_on_relative_position_only():
+    from oracle import attention as oatt
+    rng = np.random.default_rng(1)
+    q, K = rng.standard_normal((1, 128)), rng.standard_normal((50, 128))
+    t = np.arange(50)
+    for shift in (0, 7, 12345):
+        s = oatt.rope_rotate(q, [60 + shift], 10000.0) @ oatt.rope_rotate(K, t + shift, 10000.0).T
+        if shift == 0:
+            s0 = s
+        assert np.allclose(s, s0, atol=1e-9)
+
+
+def test_rope_decode_on_identity_basis_equals_brute_force():
+    # P = I, unquantized values: decode_attention_rope equals softmax(q' . rope(K)) V on dense inputs
+    from oracle import attention as oatt
+    rng = np.random.default_rng(2)
+    T, G, b = 300, 4, 8
+    step = 1.0
+    codes = rng.integers(0, 256, (T, 128)).astype(np.uint8)
+    I = np.eye(128).astype(np.float16).view(np.uint16)
+    q = (rng.standard_normal((G, 128)) * 0.05).astype(np.float16)
+    got = oatt.decode_attention_rope(codes, codes, I, I, step, step, b, b, q.view(np.uint16), T, 10000.0)
+    K = (codes.astype(np.float64) - 128 + 0.5) * step
+    Kr = oatt.rope_rotate(K, np.arange(T), 10000.0)
+    ref = oatt.brute_force_attention(q.astype(np.float64), Kr, K)
+    assert np.allclose(got, ref, rtol=1e-12, atol=1e-12)
+    # positions matter: without the rotation the output differs
+    assert not np.allclose(got, oatt.brute_force_attention(q.astype(np.float64), K, K), atol=1e-6)
