@@ -279,6 +279,14 @@ def per_layer_loop(cache, w, q, seq, n_att: int, steps: int):
             "graph_GBs": round(dec_bytes / (ms_graph / 1e3) / 1e9, 2), "graph_equals_eager": same}
 
 
+def rope_flop(cache, n_tok: int) -> int:
+    """Matrix-core flops of one RoPE-aware decode call: per 64-token tile of a unit, the key reconstruction
+    (2 x 128 x (r_K rounded up to 32) x 64) and the logits on hi + lo halves (2 x 2 x 16 x 128 x 64)."""
+    tiles = (n_tok + 63) // 64
+    r32 = (cache.K.r_h.astype(np.int64) + 31) // 32 * 32
+    return int(tiles * np.sum(2 * 128 * r32 * 64 + 2 * 2 * 16 * 128 * 64))
+
+
 def model_mse(cache, side: int, units) -> float:
     """Mean of the distortion model D(r, b) / d (MSE weights, Lemma lem:head-dist) over `units`, from the
     product's own calibration and table: the figure the measured MSE is compared with."""
@@ -435,6 +443,16 @@ def main():
         b.record()
     torch.cuda.synchronize()
     t_dec = float(np.mean([a.elapsed_time(b) for a, b in evs])) / 1e3
+    # the same decode with rotary position embeddings (keys cached pre-RoPE, rotated after reconstruction):
+    # same bytes, plus the reconstruction of every key on the matrix cores
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    for i, (a, b) in enumerate(evs):
+        flush.fill_(i & 0xFF)
+        a.record()
+        kvc.kvc_decode_attn_rope(cache.K, cache.V, q, w.group, seq, n_att, 500000.0, out, ws)
+        b.record()
+    torch.cuda.synchronize()
+    t_rope = float(np.mean([a.elapsed_time(b) for a, b in evs])) / 1e3
     del flush
     assert torch.isfinite(out).all().item()
 
@@ -482,6 +500,11 @@ def main():
         "step": {"fused_ms": round(ms_step, 4), "two_calls_ms": round(ms_two, 4),
                  "bytes": step_bytes, "note": "append of the new token + decode attention over T + 1 tokens"},
         "per_layer_decode": per_layer,
+        "rope_decode": {"ms": round(t_rope * 1e3, 4), "GBs": round(dec_bytes / t_rope / 1e9, 2),
+                        "frac": round(dec_bytes / t_rope / 1e9 / HBM_PEAK_GBS, 4),
+                        "mfma_TFLOPs": round(rope_flop(cache, n_att) / t_rope / 1e12, 2),
+                        "note": "kvc_decode_attn_rope, rotary base 500000: K reconstructed per tile on fp16 matrix "
+                                "cores, rotated, scored; MALL flushed before each call"},
         "encode": {"vectors_per_s": round(enc_vectors / t_enc, 1), "model_tokens_per_s": round(w.batch * T / t_enc, 1),
                    "ms_median": round(t_enc * 1e3, 3), "ms_min": round(min(enc_times) * 1e3, 3),
                    "ms_max": round(max(enc_times) * 1e3, 3), "runs": len(enc_times),

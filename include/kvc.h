@@ -270,6 +270,22 @@ int kvc_decode_step(const kvc_stream_desc* k, const kvc_stream_desc* v, const ui
                     const uint16_t* q, int32_t G, const int32_t* seq_len, int32_t max_seq_len, float* out,
                     void* ws, size_t ws_bytes, void* stream);
 
+/*
+ * kvc_decode_attn_rope - decode attention for a model with rotary position embeddings. Paper: Sec. 5
+ * (keys are compressed before RoPE) with the rotary embedding of the Llama family.
+ *  q          device fp16 [n_units][G][d], 16-byte aligned: the queries already rotated at their
+ *             own positions.
+ *  rope_base  host: the rotary base (e.g. 10000 or 500000), finite and > 1.
+ *  out[u][g] = P_V^T sum_t p_t z_V,t,  p = softmax_t(q_g . rope(P_K^T z_K,t, t) / sqrt(d)),
+ *  where rope(x, t) rotates each coordinate pair (j, j + d/2), j < d/2, by the angle
+ *  t * rope_base^(-2j/d): the key of stream index t sits at position t and is rotated after its
+ *  reconstruction (its codes hold the pre-RoPE key).
+ * Other arguments, workspace (kvc_decode_attn_workspace) and errors as kvc_decode_attn. Async.
+ */
+int kvc_decode_attn_rope(const kvc_stream_desc* k, const kvc_stream_desc* v, const uint16_t* q, int32_t G,
+                         const int32_t* seq_len, int32_t max_seq_len, float rope_base, float* out,
+                         void* ws, size_t ws_bytes, void* stream);
+
 /* Workspace bytes kvc_decode_attn needs for these descriptors (host only). */
 size_t kvc_decode_attn_workspace(const kvc_stream_desc* k, const kvc_stream_desc* v,
                                  int32_t G, int32_t max_seq_len);

@@ -991,6 +991,361 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(Shape<G>::W,
     run_item<G, 0, 0, -1, 8>(K, V, qa_ws, qk_ws, k_cap_tiles, v_cap_tiles, u, start, end, out, lane);
 }
 
+// ---------------------------------------------------------------- RoPE-aware partials
+
+// Keys are cached before the rotary position embedding (Sec. 5, scope), so a model with RoPE scores the
+// rotated query q' against each reconstructed key rotated at its own position; that depends on the
+// position and cannot be folded into a rank-space query. Per 64-token tile, in four blocks of 16 tokens:
+//  1. the block's centred K codes (c - 2^(b-1) + 1/2, exact in fp16) go to LDS, token-major;
+//  2. K^T (128 features x 16 tokens) = P_K^T Z^T on v_mfma_f32_16x16x32_f16, with P_K^T staged in LDS once
+//     per block of four wavefronts (the four context chunks of one unit share it); lane (col, kq) then
+//     holds features 16 rb + 4 kq + v of token col, so both members of every rotation pair (j, j + 64)
+//     sit in the same lane;
+//  3. each pair is rotated by the angle p theta_j, the position's turns computed as the tile's start
+//     (fp64, one frequency per lane) plus the offset inside the tile (fp32);
+//  4. the logits q' . K_rot on the same matrix instruction, K_rot split into fp16 hi + lo and q' permuted
+//     to the lane's feature order (the order of the k index of a dot product is free);
+// then the online softmax and the rank-space PV products exactly as in the partials kernel (int8 value
+// codes, probability limbs through LDS, int32 accumulators), writing the same partials, which the
+// combine kernel merges.
+constexpr int kRopeWaves = 4;
+constexpr int kPtPitch = 136;   // halves per feature row of the staged P_K^T (coordinates 0..127 + pad)
+constexpr int kZPitch = 136;    // halves per token row of a staged 16-token block of centred K codes
+__host__ __device__ constexpr int rope_wave_lds(int LM) { return 16 * kZPitch * 2 + 16 * LM * kPRowBytes + 64 * 4; }
+
+typedef _Float16 rp_h8 __attribute__((ext_vector_type(8)));
+typedef float rp_f4 __attribute__((ext_vector_type(4)));
+
+// Codes of group g (16 coordinates) of token t of a K tile, centred and converted: z[m] for coordinate
+// 16 g + m. The group's field of a plane of width p is 16 p bits at bit p (1024 g + 16 t).
+__device__ __forceinline__ void k_group_codes(const uint8_t* __restrict__ tile, int r, int b, int g, int t, float hk,
+                                              float (&z)[16]) {
+    uint32_t c[16];
+#pragma unroll
+    for (int m = 0; m < 16; ++m) c[m] = 0u;
+    if (b == 8) {
+        const uint4 w = *reinterpret_cast<const uint4*>(tile + 16 * (64 * g + t));
+        const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+        for (int m = 0; m < 16; ++m) c[m] = (ww[m >> 2] >> (8 * (m & 3))) & 255u;
+    } else {
+        int rem = b, off = 0;
+#pragma unroll
+        for (int p = 4; p >= 1; p >>= 1) {
+            if (b & p) {
+                rem -= p;
+                const uint8_t* base = tile + 8 * r * off + p * (128 * g + 2 * t);
+                uint32_t f[2] = {0u, 0u};
+                if (p == 1) f[0] = *reinterpret_cast<const uint16_t*>(base);
+                else if (p == 2) f[0] = *reinterpret_cast<const uint32_t*>(base);
+                else { const uint2 v2 = *reinterpret_cast<const uint2*>(base); f[0] = v2.x; f[1] = v2.y; }
+#pragma unroll
+                for (int m = 0; m < 16; ++m) {
+                    const int bit = p * m;
+                    c[m] |= ((f[bit >> 5] >> (bit & 31)) & ((1u << p) - 1u)) << rem;
+                }
+                off += p;
+            }
+        }
+    }
+#pragma unroll
+    for (int m = 0; m < 16; ++m) z[m] = (float)c[m] - hk;
+}
+
+template <int G>
+__global__ __launch_bounds__(64 * kRopeWaves) void decode_rope_kernel(
+    DevSide K, DevSide V, const uint16_t* __restrict__ q, const int32_t* __restrict__ seq_len, int max_seq, int chunk,
+    int n_chunks, int v_cap_tiles, float log2_base, float* __restrict__ part) {
+    constexpr int LM = Shape<G>::LM;
+    extern __shared__ __attribute__((aligned(16))) uint8_t rope_sm[];
+    const int u = blockIdx.y, wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int col = lane & 15, kq = lane >> 4, grp = kq;
+    const int rk = K.r[u], bk = K.b[u];
+    uint16_t* PT = reinterpret_cast<uint16_t*>(rope_sm);  // [128 features][kPtPitch]
+    {
+        // stage P_K^T: zero it (coordinates past the rank take part in the last 32-wide k-step), then
+        // transpose the basis rows in
+        for (int e = threadIdx.x; e < kD * kPtPitch / 8; e += 64 * kRopeWaves)
+            reinterpret_cast<uint4*>(PT)[e] = uint4{0u, 0u, 0u, 0u};
+        __syncthreads();
+        const uint16_t* __restrict__ P = K.basis + K.basis_off[u];
+        for (int e = threadIdx.x; e < rk * (kD / 8); e += 64 * kRopeWaves) {
+            const int i = e / (kD / 8), f0 = 8 * (e % (kD / 8));
+            const uint4 w = reinterpret_cast<const uint4*>(P + (int64_t)i * kD)[f0 / 8];
+            const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+            for (int k = 0; k < 8; ++k) PT[(f0 + k) * kPtPitch + i] = (uint16_t)(ww[k >> 1] >> (16 * (k & 1)));
+        }
+        __syncthreads();
+    }
+    const int c = blockIdx.x * kRopeWaves + wv;
+    if (c >= n_chunks) return;  // no block-wide barrier follows
+    uint8_t* wbase = rope_sm + kD * kPtPitch * 2 + wv * rope_wave_lds(LM);
+    uint16_t* ZT = reinterpret_cast<uint16_t*>(wbase);                 // [16 tokens][kZPitch]
+    uint8_t* pmat = wbase + 16 * kZPitch * 2;                          // [16 LM][kPRowBytes]
+    float* rho0 = reinterpret_cast<float*>(pmat + 16 * LM * kPRowBytes);  // [64] tile start, turns
+
+    int T = seq_len[u];
+    T = T < 0 ? 0 : (T > max_seq ? max_seq : T);
+    const int start = c * chunk;
+    const int end = min(T, start + chunk);
+    float* __restrict__ out = part + ((int64_t)u * n_chunks + c) * G * kPartStride;
+    if (start >= end) {
+        if (lane < G) { out[lane * kPartStride] = -INFINITY; out[lane * kPartStride + 1] = 0.f; }
+        return;
+    }
+    const int rv = V.r[u], bv = V.b[u];
+    const int hv = bv == 8 ? 0 : (1 << (bv - 1));
+    const float hk = (float)(1 << (bk - 1)) - 0.5f;
+    const int nks = (rk + 31) >> 5, nv = (rv + 15) >> 4, g16 = rk >> 4, rho = rk & 15;
+    const int ktb = 8 * rk * bk, vtb = 8 * rv * bv;
+    const int tile0 = start / kTile, tile_last = (end - 1) / kTile;
+    const uint8_t* kstream = K.codes + K.code_off[u];
+    const uint8_t* vstream = V.codes + V.code_off[u];
+    auto v_rs = [&](int t) {
+        const bool ok = t <= tile_last;
+        return __builtin_amdgcn_make_buffer_rsrc((void*)(vstream + (int64_t)t * vtb), (short)0,
+                                                 ok ? (v_cap_tiles - t) * vtb : 0, kRsrcWord3);
+    };
+    // q' as the logits' A operand: row = head (col), k-step ks, element e <-> feature 16 (2 ks + e / 4) + 4 kq + e % 4
+    rp_h8 qa[4];
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const int f = 16 * (2 * ks + (e >> 2)) + 4 * kq + (e & 3);
+            qa[ks][e] = col < G ? __builtin_bit_cast(_Float16, q[((int64_t)u * G + col) * kD + f]) : (_Float16)0.f;
+        }
+    // rotation frequencies of the lane's pairs j = 16 rb + 4 kq + v (rb < 4), in turns per position
+    float om[4][4];
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int j = 16 * rb + 4 * kq + v;
+            om[rb][v] = (float)(exp2(-(double)j / 64.0 * (double)log2_base) * 0.15915494309189535);
+        }
+    const double om_lane = exp2(-(double)lane / 64.0 * (double)log2_base) * 0.15915494309189535;  // frequency j = lane
+    const float scale = K.delta[u] * 1.4426950408889634f * 0.08838834764831845f;  // step_K log2(e) / sqrt(128)
+
+    float mrun[4];  // running max of heads 4 kq + v (log2 domain), replicated over the group's 16 lanes
+#pragma unroll
+    for (int v = 0; v < 4; ++v) mrun[v] = -INFINITY;
+    for (int k = lane; k < 16 * LM * kPRowBytes / 4; k += 64) reinterpret_cast<uint32_t*>(pmat)[k] = 0u;
+    v4i C[LM][9];
+#pragma unroll
+    for (int pm = 0; pm < LM; ++pm)
+#pragma unroll
+        for (int nt = 0; nt < 9; ++nt) C[pm][nt] = v4i{0, 0, 0, 0};
+    const uint32_t one = col == 0 ? 0x01010101u : 0u;
+    const v4i ones = v4i{(int)one, (int)one, (int)one, (int)one};
+    uint32_t vb[kVBufWords];
+#pragma unroll
+    for (int k = 0; k < kVBufWords; ++k) vb[k] = 0u;
+    const uint32_t LV = (uint32_t)(8 * col + 2 * grp);
+    {
+        const auto vrs = v_rs(tile0);
+        KVC_SWITCH_B(bv, (v_prefetch<B_, 8>(vb, vrs, rv, LV, nv)));
+    }
+
+    for (int tile = tile0; tile <= tile_last; ++tile) {
+        const int tok0 = tile * kTile;
+        // Opaque per-tile copies of the widths, ranks and lane offsets: the addresses every width's branch
+        // derives from them are recomputed inside the loop, not hoisted and kept live for all widths.
+        int rkt = rk, bkt = bk, rvt = rv, bvt = bv, nvt = nv, g16t = g16, rhot = rho, nkst = nks;
+        uint32_t LVt = LV;
+        int colt = col, kqt = kq;
+        asm volatile("" : "+v"(LVt), "+v"(colt), "+v"(kqt));
+        asm volatile("" : "+s"(rkt), "+s"(bkt), "+s"(rvt), "+s"(bvt), "+s"(nvt), "+s"(g16t), "+s"(rhot), "+s"(nkst));
+        const uint8_t* ktile = kstream + (int64_t)tile * ktb;
+        {
+            // turns of the tile's first position for frequency j = lane (fp64, then reduced)
+            const double t0 = (double)tok0 * om_lane;
+            rho0[lane] = (float)(t0 - floor(t0));
+        }
+        float s[4][4];  // [token block][head v], log2 domain
+#pragma unroll
+        for (int tb = 0; tb < 4; ++tb) {
+            {
+                // stage the centred codes of tokens 16 tb .. 16 tb + 15: lane (token col, part kq) takes
+                // coordinates 32 kq .. 32 kq + 31 (zero past the rank, within the 32-wide k-steps)
+                const int t = 16 * tb + colt;
+#pragma unroll
+                for (int gg = 0; gg < 2; ++gg) {
+                    const int g = 2 * kqt + gg;
+                    float z[16];
+                    if (g < g16t) {
+                        k_group_codes(ktile, rkt, bkt, g, t, hk, z);
+                    } else {
+#pragma unroll
+                        for (int m = 0; m < 16; ++m) {
+                            const int i = 16 * g + m;
+                            z[m] = (g == g16t && m < rhot) ? (float)load_code(ktile, rkt, bkt, slot_k(t, i, rkt)) - hk : 0.f;
+                        }
+                    }
+                    rp_h8 h0, h1;
+#pragma unroll
+                    for (int m = 0; m < 8; ++m) { h0[m] = (_Float16)z[m]; h1[m] = (_Float16)z[8 + m]; }
+                    *reinterpret_cast<rp_h8*>(ZT + colt * kZPitch + 16 * g) = h0;
+                    *reinterpret_cast<rp_h8*>(ZT + colt * kZPitch + 16 * g + 8) = h1;
+                }
+            }
+            wave_lds_sync();
+            // K^T block: rows 16 rb + 4 kq + v, column token col
+            rp_f4 Cr[8];
+#pragma unroll
+            for (int rb = 0; rb < 8; ++rb) Cr[rb] = rp_f4{0.f, 0.f, 0.f, 0.f};
+            for (int ks = 0; ks < nkst; ++ks) {
+                const rp_h8 bz = *reinterpret_cast<const rp_h8*>(ZT + col * kZPitch + 32 * ks + 8 * kq);
+#pragma unroll
+                for (int rb = 0; rb < 8; ++rb) {
+                    const rp_h8 ap = *reinterpret_cast<const rp_h8*>(PT + (16 * rb + col) * kPtPitch + 32 * ks + 8 * kq);
+                    Cr[rb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ap, bz, Cr[rb], 0, 0, 0);
+                }
+            }
+            wave_lds_sync();  // ZT is rewritten by the next block
+            // rotate each pair (j, j + 64) of token 16 tb + col at its position
+            const float dpos = (float)(16 * tb + col);
+#pragma unroll
+            for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const int j = 16 * rb + 4 * kq + v;
+                    float tr = fmaf(dpos, om[rb][v], rho0[j]);
+                    tr -= floorf(tr);
+                    const float cs = __cosf(6.283185307179586f * tr), sn = __sinf(6.283185307179586f * tr);
+                    const float a = Cr[rb][v], b = Cr[rb + 4][v];
+                    Cr[rb][v] = a * cs - b * sn;
+                    Cr[rb + 4][v] = a * sn + b * cs;
+                }
+            // logits: sum over features of q' times (hi + lo) of the rotated key
+            rp_f4 S = rp_f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks) {
+                rp_h8 bh, bl;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const float x = Cr[2 * ks + (e >> 2)][e & 3];
+                    const _Float16 hx = (_Float16)x;
+                    bh[e] = hx;
+                    bl[e] = (_Float16)(x - (float)hx);
+                }
+                S = __builtin_amdgcn_mfma_f32_16x16x32_f16(qa[ks], bh, S, 0, 0, 0);
+                S = __builtin_amdgcn_mfma_f32_16x16x32_f16(qa[ks], bl, S, 0, 0, 0);
+            }
+            const bool valid_tok = tok0 + 16 * tb + col < end;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) s[tb][v] = (valid_tok && 4 * kq + v < G) ? S[v] * scale : -INFINITY;
+        }
+
+        // ---- online softmax of the tile: heads 4 kq + v live in the 16 lanes of group kq
+        float mx[4];
+        bool raise = false;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            mx[v] = row_max(fmaxf(fmaxf(s[0][v], s[1][v]), fmaxf(s[2][v], s[3][v])));
+            raise = raise || (mx[v] > -INFINITY && (mrun[v] == -INFINITY || mx[v] - mrun[v] > kLazy));
+        }
+        if (__any(raise)) {
+            float alpha[4];
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                alpha[v] = 1.f;
+                if (mx[v] > -INFINITY && (mrun[v] == -INFINITY || mx[v] - mrun[v] > kLazy)) {
+                    alpha[v] = mrun[v] == -INFINITY ? 0.f : exp2f(mrun[v] - mx[v]);
+                    mrun[v] = mx[v];
+                }
+            }
+            // accumulators of head 4 pm + grp: its factor lives in lane 16 pm, element grp
+#pragma unroll
+            for (int pm = 0; pm < LM; ++pm) {
+                float al = 1.f;
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const float t = __shfl(alpha[v], 16 * pm);
+                    if (grp == v) al = t;
+                }
+                if (al != 1.f) {
+                    const double a = (double)al;
+#pragma unroll
+                    for (int nt = 0; nt < 9; ++nt) {
+                        const double vv = ((double)C[pm][nt][0] + 256.0 * (double)C[pm][nt][1]) +
+                                          (65536.0 * (double)C[pm][nt][2] + 16777216.0 * (double)C[pm][nt][3]);
+                        const double vs = rint(vv * a);
+                        const double c3 = floor(vs * (1.0 / 16777216.0));
+                        const double r3 = vs - 16777216.0 * c3;
+                        const double c2 = floor(r3 * (1.0 / 65536.0));
+                        const double r2 = r3 - 65536.0 * c2;
+                        const double c1 = floor(r2 * (1.0 / 256.0));
+                        C[pm][nt][3] = (int)c3;
+                        C[pm][nt][2] = (int)c2;
+                        C[pm][nt][1] = (int)c1;
+                        C[pm][nt][0] = (int)(r2 - 256.0 * c1);
+                    }
+                }
+            }
+        }
+        // ---- probability limbs of heads 4 kq + v, token 16 tb + col: row 16 kq + 4 v + limb, byte = token
+        if (kq < LM) {
+#pragma unroll
+            for (int tb = 0; tb < 4; ++tb)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const float pr = s[tb][v] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(s[tb][v] - mrun[v]);
+                    const uint32_t P = (uint32_t)fmaf(pr, kPScale, kPBias);
+                    uint8_t* row = pmat + (16 * kq + 4 * v) * kPRowBytes + 16 * tb + col;
+                    row[0] = (uint8_t)((P & 255u) ^ 0x80u);
+                    row[kPRowBytes] = (uint8_t)(((P >> 8) & 255u) ^ 0x80u);
+                    row[2 * kPRowBytes] = (uint8_t)(((P >> 16) & 255u) ^ 0x80u);
+                    row[3 * kPRowBytes] = (uint8_t)(P >> 24);
+                }
+        }
+        wave_lds_sync();
+        v4i ap[LM];
+#pragma unroll
+        for (int pm = 0; pm < LM; ++pm)
+            ap[pm] = *reinterpret_cast<const v4i*>(pmat + (16 * pm + col) * kPRowBytes + 16 * grp);
+        {
+            const auto vrs = v_rs(tile), vrs_n = v_rs(tile + 1);
+            KVC_SWITCH_B(bvt, (v_tile<B_, LM, 8>(vb, vrs, vrs_n, rvt, LVt, nvt, ap, C)));
+        }
+#pragma unroll
+        for (int pm = 0; pm < LM; ++pm) C[pm][8] = mfma_i8(ap[pm], ones, C[pm][8]);
+        wave_lds_sync();  // pmat and rho0 are rewritten by the next tile
+    }
+
+    // partials: m of head 4 pm + grp (lane 16 pm, element grp), l and the centred accumulator
+#pragma unroll
+    for (int pm = 0; pm < LM; ++pm) {
+        const int h = 4 * pm + grp;
+        float mh = -INFINITY;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const float t = __shfl(mrun[v], 16 * pm);
+            if (grp == v) mh = t;
+        }
+        const int o0 = __shfl(C[pm][8][0], lane & 48), o1 = __shfl(C[pm][8][1], lane & 48),
+                  o2 = __shfl(C[pm][8][2], lane & 48), o3 = __shfl(C[pm][8][3], lane & 48);
+        if (G % 4 == 0 || h < G) {
+            float* o = out + h * kPartStride;
+            if (col == 0) {
+                o[0] = mh;
+                o[1] = ((float)o0 + 256.f * (float)o1) + (65536.f * (float)o2 + 16777216.f * (float)o3);
+            }
+#pragma unroll
+            for (int nt = 0; nt < 8; ++nt) {
+                const int cc = 16 * nt + col;
+                if (nt < nv) {
+                    const int a0 = C[pm][nt][0] - hv * o0, a1 = C[pm][nt][1] - hv * o1, a2 = C[pm][nt][2] - hv * o2,
+                              a3 = C[pm][nt][3] - hv * o3;
+                    o[4 + cc] = cc < rv ? ((float)a0 + 256.f * (float)a1) + (65536.f * (float)a2 + 16777216.f * (float)a3)
+                                        : 0.f;
+                }
+            }
+        }
+    }
+}
+
 // ---------------------------------------------------------------- combine
 
 // One block of WC wavefronts per unit (one for a few chunks, more when the context is split into
@@ -1442,6 +1797,59 @@ extern "C" int kvc_decode_step(const kvc_stream_desc* k, const kvc_stream_desc* 
     app.xv_stride = xv_unit_stride;
     app.t_new = t_new;
     return decode_launch(k, v, q, G, seq_len, max_seq_len, out, ws, L, stream, app);
+}
+
+namespace kvc {
+namespace {
+
+template <int G>
+int launch_rope(const kvc_stream_desc* k, const kvc_stream_desc* v, const uint16_t* q, const int32_t* seq_len,
+                int32_t max_seq_len, float log2_base, float* out, const WsLayout& L, float* part, hipStream_t st) {
+    constexpr int LM = (G + 3) / 4;
+    const size_t smem = (size_t)kD * kPtPitch * 2 + (size_t)kRopeWaves * rope_wave_lds(LM);
+    if (smem > 64 * 1024) {
+        const hipError_t e = hipFuncSetAttribute((const void*)decode_rope_kernel<G>,
+                                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+        if (e != hipSuccess) return set_error(KVC_EDEVICE, "hipFuncSetAttribute: %s", hipGetErrorString(e));
+    }
+    const int U = k->n_units;
+    const int vct = (v->capacity + kTile - 1) / kTile;
+    const DevSide K = dev_side(k), V = dev_side(v);
+    hipLaunchKernelGGL(decode_rope_kernel<G>, dim3((L.n_chunks + kRopeWaves - 1) / kRopeWaves, U),
+                       dim3(64 * kRopeWaves), smem, st, K, V, q, seq_len, max_seq_len, L.chunk, L.n_chunks, vct,
+                       log2_base, part);
+    const int cw = combine_waves(G, L.n_chunks, U, device_cus());
+    launch_combine<G>(cw, dim3(U), dim3(64 * cw), (size_t)cw * G * kPartStride * 4, st, V, L.n_chunks, part, out);
+    return check_launch("kvc_decode_attn_rope");
+}
+
+}  // namespace
+}  // namespace kvc
+
+extern "C" int kvc_decode_attn_rope(const kvc_stream_desc* k, const kvc_stream_desc* v, const uint16_t* q, int32_t G,
+                                    const int32_t* seq_len, int32_t max_seq_len, float rope_base, float* out,
+                                    void* ws, size_t ws_bytes, void* stream) {
+    clear_error();
+    if (int e = decode_check(k, v, G, max_seq_len)) return e;
+    if (!(rope_base > 1.f) || !std::isfinite(rope_base))
+        return set_error(KVC_EINVAL, "kvc_decode_attn_rope: rope_base must be finite and > 1");
+    if (k->n_units == 0) return KVC_OK;
+    if (int e = decode_args("kvc_decode_attn_rope", q, seq_len, out)) return e;
+    if (!ws) return set_error(KVC_EINVAL, "kvc_decode_attn_rope: null workspace");
+    if (reinterpret_cast<uintptr_t>(ws) & 255) return set_error(KVC_EINVAL, "kvc_decode_attn_rope: workspace not 256-byte aligned");
+    const WsLayout L = ws_layout(k, G, max_seq_len);
+    if ((int64_t)ws_bytes < L.total)
+        return set_error(KVC_ENOSPACE, "kvc_decode_attn_rope: workspace %zu < %lld bytes", ws_bytes, (long long)L.total);
+    float* part = reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + L.part);
+    const float lb = (float)std::log2((double)rope_base);
+    hipStream_t st = (hipStream_t)stream;
+    switch (G) {
+        case 1: return launch_rope<1>(k, v, q, seq_len, max_seq_len, lb, out, L, part, st);
+        case 2: return launch_rope<2>(k, v, q, seq_len, max_seq_len, lb, out, L, part, st);
+        case 4: return launch_rope<4>(k, v, q, seq_len, max_seq_len, lb, out, L, part, st);
+        case 8: return launch_rope<8>(k, v, q, seq_len, max_seq_len, lb, out, L, part, st);
+        default: return launch_rope<16>(k, v, q, seq_len, max_seq_len, lb, out, L, part, st);
+    }
 }
 
 extern "C" int kvc_decode_attn_noalloc(const kvc_stream_desc* k, const kvc_stream_desc* v, const uint16_t* q,

@@ -72,6 +72,8 @@ def lib():
         L.kvc_decode_step.argtypes = [ctypes.POINTER(StreamDesc), ctypes.POINTER(StreamDesc), _p, ctypes.c_int64, _p,
                                       ctypes.c_int64, ctypes.c_int32, _p, ctypes.c_int32, _p, ctypes.c_int32, _p, _p,
                                       ctypes.c_size_t, _p]
+        L.kvc_decode_attn_rope.argtypes = [ctypes.POINTER(StreamDesc), ctypes.POINTER(StreamDesc), _p, ctypes.c_int32, _p,
+                                           ctypes.c_int32, ctypes.c_float, _p, _p, ctypes.c_size_t, _p]
         L.kvc_decode_attn_noalloc.argtypes = [ctypes.POINTER(StreamDesc), ctypes.POINTER(StreamDesc), _p,
                                               ctypes.c_int32, _p, ctypes.c_int32, _p, _p]
         L.kvc_reconstruct.argtypes = [ctypes.POINTER(StreamDesc), ctypes.c_int32, ctypes.c_int32, _p, _p]
@@ -316,6 +318,22 @@ def kvc_decode_step(k: Side, v: Side, xk, xv, t_new: int, q, G: int, seq_len, ma
                                  ctypes.c_void_p(q.data_ptr()), int(G), ctypes.c_void_p(seq_len.data_ptr()),
                                  int(max_seq_len), ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(ws.data_ptr()),
                                  ws.numel(), _stream_ptr(stream)))
+
+
+def kvc_decode_attn_rope(k: Side, v: Side, q, G: int, seq_len, max_seq_len: int, rope_base: float, out, ws,
+                         stream=None):
+    """Decode attention with RoPE: q fp16 (n_units, G, d) already rotated; keys rotated at their stream index."""
+    import torch
+    U = k.n_units
+    assert q.is_contiguous() and out.is_contiguous() and seq_len.is_contiguous()
+    assert q.dtype == torch.float16 and q.numel() == U * G * HEAD_DIM
+    assert out.dtype == torch.float32 and out.numel() == U * G * HEAD_DIM
+    assert seq_len.dtype == torch.int32 and seq_len.numel() == U and v.n_units == U
+    assert q.device == out.device == seq_len.device == ws.device == k.codes.device
+    _check(lib().kvc_decode_attn_rope(ctypes.byref(k.desc), ctypes.byref(v.desc), ctypes.c_void_p(q.data_ptr()), int(G),
+                                      ctypes.c_void_p(seq_len.data_ptr()), int(max_seq_len), float(rope_base),
+                                      ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(ws.data_ptr()), ws.numel(),
+                                      _stream_ptr(stream)))
 
 
 def kvc_decode_attn_noalloc(k: Side, v: Side, q, G: int, seq_len, max_seq_len: int, out, stream=None):

@@ -125,3 +125,29 @@ def test_reconstruct_every_width(width_cache):
             ref = oatt.reconstruct(c, P[u], dl[u], b)
             assert normwise(got[u], ref) <= 1e-5, (side, u, row)
         log(f"[widths] reconstruct side {'KV'[side]}: every unit within 1e-5")
+
+
+def test_rope_decode_every_width_pair(width_cache):
+    # the RoPE-aware path unpacks K codes itself (whole 16-coordinate groups and the tail group)
+    rows, K, V, Pk, dk, Pv, dv, codes = width_cache
+    U, G, base = len(rows), 4, 10000.0
+    rng = np.random.default_rng(77)
+    q = (rng.standard_normal((U, G, 128)) * 1.5).astype(np.float16)
+    qt = torch.as_tensor(q.view(np.int16), device="cuda").view(torch.float16)
+    seq = np.full(U, T, dtype=np.int32)
+    seq[::5] = rng.integers(1, T, size=len(seq[::5]))
+    ws = torch.empty(kvc.kvc_decode_attn_workspace(K, V, G, T), dtype=torch.uint8, device="cuda")
+    out = torch.empty((U, G, 128), dtype=torch.float32, device="cuda")
+    kvc.kvc_decode_attn_rope(K, V, qt, G, torch.as_tensor(seq, device="cuda"), T, base, out, ws)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    worst = 0.0
+    for u, (rk, bk, rv, bv) in enumerate(rows):
+        ck, cv = codes[u]
+        ref = oatt.decode_attention_rope(ck, cv, Pk[u], Pv[u], dk[u], dv[u], bk, bv, q[u].view(np.uint16), int(seq[u]),
+                                         base)
+        for g in range(G):
+            e = normwise(got[u, g], ref[g])
+            worst = max(worst, e)
+            assert e <= TOL, (u, (rk, bk, rv, bv), g, e)
+    log(f"[widths rope] 64 width pairs, max normwise error {worst:.2e}")
