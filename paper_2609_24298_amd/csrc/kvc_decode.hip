@@ -1011,45 +1011,90 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(Shape<G>::W,
 constexpr int kRopeWaves = 4;
 constexpr int kPtPitch = 136;   // halves per feature row of the staged P_K^T (coordinates 0..127 + pad)
 constexpr int kZPitch = 136;    // halves per token row of a staged 16-token block of centred K codes
-__host__ __device__ constexpr int rope_wave_lds(int LM) { return 16 * kZPitch * 2 + 16 * LM * kPRowBytes + 64 * 4; }
+constexpr int kRopeKTile = 8 * kD * 8;  // bytes of the widest K tile (r = 128, b = 8)
+constexpr int kRopeKChunks = kRopeKTile / 16 / 64;  // 16-byte loads per lane for one K tile
+__host__ __device__ constexpr int rope_wave_lds(int LM) {
+    return kRopeKTile + 16 * kZPitch * 2 + 16 * LM * kPRowBytes + 64 * 4;
+}
 
 typedef _Float16 rp_h8 __attribute__((ext_vector_type(8)));
 typedef float rp_f4 __attribute__((ext_vector_type(4)));
 
-// Codes of group g (16 coordinates) of token t of a K tile, centred and converted: z[m] for coordinate
-// 16 g + m. The group's field of a plane of width p is 16 p bits at bit p (1024 g + 16 t).
-__device__ __forceinline__ void k_group_codes(const uint8_t* __restrict__ tile, int r, int b, int g, int t, float hk,
-                                              float (&z)[16]) {
-    uint32_t c[16];
-#pragma unroll
-    for (int m = 0; m < 16; ++m) c[m] = 0u;
-    if (b == 8) {
+// Codes of group g (16 coordinates) of token t of a K tile: c[m] for coordinate 16 g + m. The group's
+// field of a plane of width p is 16 p bits at bit p (1024 g + 16 t) of the plane.
+template <int B>
+__device__ __forceinline__ void k_group_codes(const uint8_t* __restrict__ tile, int r, int g, int t, uint32_t (&c)[16]) {
+    if constexpr (B == 8) {
         const uint4 w = *reinterpret_cast<const uint4*>(tile + 16 * (64 * g + t));
         const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
-        for (int m = 0; m < 16; ++m) c[m] = (ww[m >> 2] >> (8 * (m & 3))) & 255u;
+        for (int m = 0; m < 16; ++m) c[m] = __builtin_amdgcn_ubfe(ww[m >> 2], 8 * (m & 3), 8);
     } else {
-        int rem = b, off = 0;
 #pragma unroll
-        for (int p = 4; p >= 1; p >>= 1) {
-            if (b & p) {
-                rem -= p;
-                const uint8_t* base = tile + 8 * r * off + p * (128 * g + 2 * t);
-                uint32_t f[2] = {0u, 0u};
-                if (p == 1) f[0] = *reinterpret_cast<const uint16_t*>(base);
-                else if (p == 2) f[0] = *reinterpret_cast<const uint32_t*>(base);
-                else { const uint2 v2 = *reinterpret_cast<const uint2*>(base); f[0] = v2.x; f[1] = v2.y; }
+        for (int m = 0; m < 16; ++m) c[m] = 0u;
 #pragma unroll
-                for (int m = 0; m < 16; ++m) {
-                    const int bit = p * m;
-                    c[m] |= ((f[bit >> 5] >> (bit & 31)) & ((1u << p) - 1u)) << rem;
-                }
-                off += p;
+        for (int k = 0; k < n_planes(B); ++k) {
+            const int P = plane_w(B, k), SH = plane_sh(B, k), OFF = plane_off(B, k);
+            const uint8_t* base = tile + 8 * r * OFF + P * (128 * g + 2 * t);
+            uint32_t f[2] = {0u, 0u};
+            if (P == 1) f[0] = *reinterpret_cast<const uint16_t*>(base);
+            else if (P == 2) f[0] = *reinterpret_cast<const uint32_t*>(base);
+            else { const uint2 v2 = *reinterpret_cast<const uint2*>(base); f[0] = v2.x; f[1] = v2.y; }
+#pragma unroll
+            for (int m = 0; m < 16; ++m) {
+                const uint32_t v = __builtin_amdgcn_ubfe(f[(P * m) >> 5], (P * m) & 31, P);
+                c[m] = k == 0 ? (v << SH) : (c[m] | (v << SH));
             }
         }
     }
+}
+
+// Codes of the tail group (rho = r % 16 coordinates after the 16 g16 of the whole groups) of token t: the
+// rho p bits of a plane start at bit p (1024 g16 + t rho); five words around them are aligned with
+// funnel shifts, so that every code sits at a fixed bit of the aligned value.
+template <int B>
+__device__ __forceinline__ void k_tail_codes(const uint8_t* __restrict__ tile, int r, int g16, int rho, int t,
+                                             uint32_t (&c)[16]) {
 #pragma unroll
-    for (int m = 0; m < 16; ++m) z[m] = (float)c[m] - hk;
+    for (int m = 0; m < 16; ++m) c[m] = 0u;
+#pragma unroll
+    for (int k = 0; k < n_planes(B); ++k) {
+        const int P = plane_w(B, k), SH = plane_sh(B, k), OFF = plane_off(B, k);
+        const uint32_t bit0 = (uint32_t)(P * (1024 * g16 + t * rho));
+        const uint32_t* w = reinterpret_cast<const uint32_t*>(tile + 8 * r * OFF) + (bit0 >> 5);
+        const uint32_t d0 = w[0], d1 = w[1], d2 = w[2], d3 = w[3], d4 = w[4];
+        const uint32_t x[4] = {funnel(d1, d0, bit0), funnel(d2, d1, bit0), funnel(d3, d2, bit0), funnel(d4, d3, bit0)};
+#pragma unroll
+        for (int m = 0; m < 16; ++m) {
+            if (P * m >= 128) break;
+            const uint32_t v = __builtin_amdgcn_ubfe(x[(P * m) >> 5], (P * m) & 31, P);
+            c[m] |= v << SH;
+        }
+    }
+}
+
+// Stage the centred K codes (c - 2^(b-1) + 1/2, exact in fp16) of token t for the lane's two groups
+// 2 kq, 2 kq + 1 into its row of ZT (zero past the rank).
+template <int B>
+__device__ __forceinline__ void rope_stage_codes(const uint8_t* __restrict__ ktile, int rk, int g16, int rho, int kq,
+                                                 int t, uint16_t* __restrict__ zrow) {
+    const _Float16 hk = (_Float16)((float)(1 << (B - 1)) - 0.5f);
+#pragma unroll
+    for (int gg = 0; gg < 2; ++gg) {
+        const int g = 2 * kq + gg;
+        uint32_t c[16];
+        if (g < g16) k_group_codes<B>(ktile, rk, g, t, c);
+        else k_tail_codes<B>(ktile, rk, g16, rho, t, c);
+        rp_h8 h0, h1;
+#pragma unroll
+        for (int m = 0; m < 8; ++m) {
+            const bool in0 = g < g16 || (g == g16 && m < rho), in1 = g < g16 || (g == g16 && m + 8 < rho);
+            h0[m] = in0 ? (_Float16)(uint16_t)c[m] - hk : (_Float16)0.f;
+            h1[m] = in1 ? (_Float16)(uint16_t)c[8 + m] - hk : (_Float16)0.f;
+        }
+        *reinterpret_cast<rp_h8*>(zrow + 16 * g) = h0;
+        *reinterpret_cast<rp_h8*>(zrow + 16 * g + 8) = h1;
+    }
 }
 
 template <int G>
@@ -1058,9 +1103,9 @@ __global__ __launch_bounds__(64 * kRopeWaves) void decode_rope_kernel(
     int n_chunks, int v_cap_tiles, float log2_base, float* __restrict__ part) {
     constexpr int LM = Shape<G>::LM;
     extern __shared__ __attribute__((aligned(16))) uint8_t rope_sm[];
-    const int u = blockIdx.y, wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int u = blockIdx.y, wv = uni((int)(threadIdx.x >> 6)), lane = threadIdx.x & 63;
     const int col = lane & 15, kq = lane >> 4, grp = kq;
-    const int rk = K.r[u], bk = K.b[u];
+    const int rk = uni(K.r[u]), bk = uni(K.b[u]);
     uint16_t* PT = reinterpret_cast<uint16_t*>(rope_sm);  // [128 features][kPtPitch]
     {
         // stage P_K^T: zero it (coordinates past the rank take part in the last 32-wide k-step), then
@@ -1081,31 +1126,44 @@ __global__ __launch_bounds__(64 * kRopeWaves) void decode_rope_kernel(
     const int c = blockIdx.x * kRopeWaves + wv;
     if (c >= n_chunks) return;  // no block-wide barrier follows
     uint8_t* wbase = rope_sm + kD * kPtPitch * 2 + wv * rope_wave_lds(LM);
-    uint16_t* ZT = reinterpret_cast<uint16_t*>(wbase);                 // [16 tokens][kZPitch]
-    uint8_t* pmat = wbase + 16 * kZPitch * 2;                          // [16 LM][kPRowBytes]
+    uint8_t* KS = wbase;                                               // the K tile being processed
+    uint16_t* ZT = reinterpret_cast<uint16_t*>(wbase + kRopeKTile);     // [16 tokens][kZPitch]
+    uint8_t* pmat = wbase + kRopeKTile + 16 * kZPitch * 2;             // [16 LM][kPRowBytes]
     float* rho0 = reinterpret_cast<float*>(pmat + 16 * LM * kPRowBytes);  // [64] tile start, turns
 
-    int T = seq_len[u];
+    int T = uni(seq_len[u]);
     T = T < 0 ? 0 : (T > max_seq ? max_seq : T);
-    const int start = c * chunk;
-    const int end = min(T, start + chunk);
+    const int start = uni(c * chunk);
+    const int end = uni(min(T, start + chunk));
     float* __restrict__ out = part + ((int64_t)u * n_chunks + c) * G * kPartStride;
     if (start >= end) {
         if (lane < G) { out[lane * kPartStride] = -INFINITY; out[lane * kPartStride + 1] = 0.f; }
         return;
     }
-    const int rv = V.r[u], bv = V.b[u];
+    const int rv = uni(V.r[u]), bv = uni(V.b[u]);
     const int hv = bv == 8 ? 0 : (1 << (bv - 1));
-    const float hk = (float)(1 << (bk - 1)) - 0.5f;
     const int nks = (rk + 31) >> 5, nv = (rv + 15) >> 4, g16 = rk >> 4, rho = rk & 15;
     const int ktb = 8 * rk * bk, vtb = 8 * rv * bv;
-    const int tile0 = start / kTile, tile_last = (end - 1) / kTile;
-    const uint8_t* kstream = K.codes + K.code_off[u];
-    const uint8_t* vstream = V.codes + V.code_off[u];
+    const int tile0 = uni(start / kTile), tile_last = uni((end - 1) / kTile);
+    const uint8_t* kstream = uni(K.codes + K.code_off[u]);
+    const uint8_t* vstream = uni(V.codes + V.code_off[u]);
+    v_cap_tiles = uni(v_cap_tiles);
     auto v_rs = [&](int t) {
         const bool ok = t <= tile_last;
         return __builtin_amdgcn_make_buffer_rsrc((void*)(vstream + (int64_t)t * vtb), (short)0,
                                                  ok ? (v_cap_tiles - t) * vtb : 0, kRsrcWord3);
+    };
+    // K tile t as one range-checked descriptor (reads past the tile return zero; none past the chunk)
+    auto k_rs = [&](int t) {
+        return __builtin_amdgcn_make_buffer_rsrc((void*)(kstream + (int64_t)t * ktb), (short)0, t <= tile_last ? ktb : 0,
+                                                 kRsrcWord3);
+    };
+    // the K tile's bytes, 16 per lane and load, in flight one tile ahead
+    v4u kpf[kRopeKChunks];
+    auto k_fetch = [&](int t) {
+        const auto rs = k_rs(t);
+#pragma unroll
+        for (int m = 0; m < kRopeKChunks; ++m) kpf[m] = __builtin_amdgcn_raw_buffer_load_b128(rs, 16 * (lane + 64 * m), 0, 0);
     };
     // q' as the logits' A operand: row = head (col), k-step ks, element e <-> feature 16 (2 ks + e / 4) + 4 kq + e % 4
     rp_h8 qa[4];
@@ -1147,8 +1205,14 @@ __global__ __launch_bounds__(64 * kRopeWaves) void decode_rope_kernel(
         const auto vrs = v_rs(tile0);
         KVC_SWITCH_B(bv, (v_prefetch<B_, 8>(vb, vrs, rv, LV, nv)));
     }
+    k_fetch(tile0);
 
     for (int tile = tile0; tile <= tile_last; ++tile) {
+        // the K tile to LDS, then the next tile's loads go out
+#pragma unroll
+        for (int m = 0; m < kRopeKChunks; ++m)
+            if (16 * (lane + 64 * m) < ktb) *reinterpret_cast<v4u*>(KS + 16 * (lane + 64 * m)) = kpf[m];
+        k_fetch(tile + 1);
         const int tok0 = tile * kTile;
         // Opaque per-tile copies of the widths, ranks and lane offsets: the addresses every width's branch
         // derives from them are recomputed inside the loop, not hoisted and kept live for all widths.
@@ -1157,7 +1221,7 @@ __global__ __launch_bounds__(64 * kRopeWaves) void decode_rope_kernel(
         int colt = col, kqt = kq;
         asm volatile("" : "+v"(LVt), "+v"(colt), "+v"(kqt));
         asm volatile("" : "+s"(rkt), "+s"(bkt), "+s"(rvt), "+s"(bvt), "+s"(nvt), "+s"(g16t), "+s"(rhot), "+s"(nkst));
-        const uint8_t* ktile = kstream + (int64_t)tile * ktb;
+        const uint8_t* ktile = KS;
         {
             // turns of the tile's first position for frequency j = lane (fp64, then reduced)
             const double t0 = (double)tok0 * om_lane;
@@ -1165,30 +1229,16 @@ __global__ __launch_bounds__(64 * kRopeWaves) void decode_rope_kernel(
         }
         float s[4][4];  // [token block][head v], log2 domain
 #pragma unroll
+        for (int a = 0; a < 4; ++a)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) s[a][v] = -INFINITY;
+#pragma unroll 1
         for (int tb = 0; tb < 4; ++tb) {
             {
                 // stage the centred codes of tokens 16 tb .. 16 tb + 15: lane (token col, part kq) takes
                 // coordinates 32 kq .. 32 kq + 31 (zero past the rank, within the 32-wide k-steps)
                 const int t = 16 * tb + colt;
-#pragma unroll
-                for (int gg = 0; gg < 2; ++gg) {
-                    const int g = 2 * kqt + gg;
-                    float z[16];
-                    if (g < g16t) {
-                        k_group_codes(ktile, rkt, bkt, g, t, hk, z);
-                    } else {
-#pragma unroll
-                        for (int m = 0; m < 16; ++m) {
-                            const int i = 16 * g + m;
-                            z[m] = (g == g16t && m < rhot) ? (float)load_code(ktile, rkt, bkt, slot_k(t, i, rkt)) - hk : 0.f;
-                        }
-                    }
-                    rp_h8 h0, h1;
-#pragma unroll
-                    for (int m = 0; m < 8; ++m) { h0[m] = (_Float16)z[m]; h1[m] = (_Float16)z[8 + m]; }
-                    *reinterpret_cast<rp_h8*>(ZT + colt * kZPitch + 16 * g) = h0;
-                    *reinterpret_cast<rp_h8*>(ZT + colt * kZPitch + 16 * g + 8) = h1;
-                }
+                KVC_SWITCH_B(bkt, (rope_stage_codes<B_>(ktile, rkt, g16t, rhot, kqt, t, ZT + colt * kZPitch)));
             }
             wave_lds_sync();
             // K^T block: rows 16 rb + 4 kq + v, column token col
@@ -1235,7 +1285,10 @@ __global__ __launch_bounds__(64 * kRopeWaves) void decode_rope_kernel(
             }
             const bool valid_tok = tok0 + 16 * tb + col < end;
 #pragma unroll
-            for (int v = 0; v < 4; ++v) s[tb][v] = (valid_tok && 4 * kq + v < G) ? S[v] * scale : -INFINITY;
+            for (int a = 0; a < 4; ++a)  // s[tb] without a run-time register index
+#pragma unroll
+                for (int v = 0; v < 4; ++v)
+                    if (a == tb) s[a][v] = (valid_tok && 4 * kq + v < G) ? S[v] * scale : -INFINITY;
         }
 
         // ---- online softmax of the tile: heads 4 kq + v live in the 16 lanes of group kq
