@@ -279,6 +279,25 @@ def per_layer_loop(cache, w, q, seq, n_att: int, steps: int):
             "graph_GBs": round(dec_bytes / (ms_graph / 1e3) / 1e9, 2), "graph_equals_eager": same}
 
 
+def allocator_timing(w, stats):
+    """Host allocator (kvc_allocate, one CPU thread) on the workload's K heads: the damped C1 + C2 solve
+    (the paper's default, best of three runs) and the exact DP (one run)."""
+    from paper_2609_24298_amd import kvc
+    lam = np.stack([s.lam_k for s in stats])
+    sq = np.stack([s.sigma2_q for s in stats])
+    out = {"heads": len(stats), "bpd": w.bpd}
+    for name, solver, reps in (("damped_ms", kvc.SOLVER_DAMPED, 3), ("dp_ms", kvc.SOLVER_DP, 1)):
+        best = None
+        for _ in range(reps):
+            t = time.perf_counter()
+            kvc.kvc_allocate(lam, sq, kvc.alloc_opts(w.bpd, solver))
+            el = (time.perf_counter() - t) * 1e3
+            best = el if best is None else min(best, el)
+        out[name] = round(best, 2)
+    log(f"allocator on {len(stats)} heads at {w.bpd} bpd: damped {out['damped_ms']} ms, DP {out['dp_ms']} ms")
+    return out
+
+
 def rope_flop(cache, n_tok: int) -> int:
     """Matrix-core flops of one RoPE-aware decode call: per 64-token tile of a unit, the key reconstruction
     (2 x 128 x (r_K rounded up to 32) x 64) and the logits on hi + lo halves (2 x 2 x 16 x 128 x 64)."""
@@ -349,6 +368,7 @@ def main():
         calib = calibration_timing(w, covs, dev, args.cal_tokens, args.seed)
         torch.cuda.empty_cache()
     stats = pipeline.calibrate(covs, dev)
+    alloc_t = allocator_timing(w, stats)
     cache = pipeline.Cache(w, seed=args.seed, device=dev, capacity=T + kvc.TILE, uniform=args.uniform, stats=stats)
     log(f"calibration + tables + bases in {time.perf_counter() - t_setup:.1f} s; "
         f"K (r,b) spread {len(set(zip(cache.k_tab.r.tolist(), cache.k_tab.b.tolist())))} pairs")
@@ -513,6 +533,7 @@ def main():
                    "mfma_TFLOPs": round(enc_flop / t_enc / 1e12, 2),
                    "mfma_frac": round(enc_flop / t_enc / 1e12 / MFMA_F16_PEAK_TFLOPS, 4)},
         "calibration": calib,
+        "allocator": alloc_t,
         "mse": mse,
     }
     if args.copy_calib:
