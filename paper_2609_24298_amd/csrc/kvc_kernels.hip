@@ -69,10 +69,39 @@ __device__ __forceinline__ uint32_t compact4(uint32_t v) {
     }
 }
 
-// Packs slots [sl0, sl0 + n_sl) of a tile (their codes are bytes sb[0 .. n_sl) in slot order)
-// into every bit plane of a B-bit code: slot phi of a plane of width p takes bits
-// [p phi, p phi + p), so word w of the plane holds slots [w 32/p, (w + 1) 32/p) in order.
-template <int B, int K>
+// The codes of one slot group (1024 slots) wait in LDS in slot order, except that on the V side each
+// 64-slot coordinate row starts kVRow bytes after the previous one: the 16 extra bytes spread the
+// rows' dword writes (lane (col, grp) writes row col at 4 grp + 16 nt) over the banks.
+constexpr int kVRow = 80;
+constexpr int kSlotBufBytes = 16 * kVRow;
+template <int side>
+__device__ __forceinline__ int sb_off(int slot) {
+    return side == KVC_SIDE_K ? slot : (slot >> 6) * kVRow + (slot & 63);
+}
+
+// Codes of the PPW slots [PPW w, PPW w + PPW) of the group, four per dword, read with one LDS access
+// (two for 1-bit planes).
+template <int side, int PPW>
+__device__ __forceinline__ void slot_words(const uint8_t* __restrict__ sb, int w, uint32_t (&v)[PPW / 4]) {
+    const uint8_t* src = sb + sb_off<side>(w * PPW);
+    if constexpr (PPW == 4) {
+        v[0] = *reinterpret_cast<const uint32_t*>(src);
+    } else if constexpr (PPW == 8) {
+        const uint2 a = *reinterpret_cast<const uint2*>(src);
+        v[0] = a.x; v[1] = a.y;
+    } else if constexpr (PPW == 16) {
+        const uint4 a = *reinterpret_cast<const uint4*>(src);
+        v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+    } else {
+        const uint4 a = *reinterpret_cast<const uint4*>(src), c = *reinterpret_cast<const uint4*>(src + 16);
+        v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = c.x; v[5] = c.y; v[6] = c.z; v[7] = c.w;
+    }
+}
+
+// Packs slots [sl0, sl0 + n_sl) of a tile (the group's codes in sb, see sb_off) into every bit plane
+// of a B-bit code: slot phi of a plane of width p takes bits [p phi, p phi + p), so word w of the
+// plane holds slots [w 32/p, (w + 1) 32/p) in order.
+template <int side, int B, int K>
 __device__ __forceinline__ void pack_plane(const uint8_t* __restrict__ sb, uint8_t* __restrict__ tbase, int r, int sl0,
                                            int n_sl, int lane) {
     if constexpr (K < n_planes(B)) {
@@ -81,7 +110,8 @@ __device__ __forceinline__ void pack_plane(const uint8_t* __restrict__ sb, uint8
         uint32_t* __restrict__ pw = reinterpret_cast<uint32_t*>(tbase + 8 * r * plane_off(B, K)) + sl0 / PPW;
         const int nw = n_sl / PPW;
         for (int wi = lane; wi < nw; wi += 64) {
-            const uint32_t* src = reinterpret_cast<const uint32_t*>(sb + wi * PPW);
+            uint32_t src[PPW / 4];
+            slot_words<side, PPW>(sb, wi, src);
             uint32_t word = 0;
 #pragma unroll
             for (int m = 0; m < PPW / 4; ++m) word |= compact4<P>((src[m] >> SH) & PM) << (4 * P * m);
@@ -90,12 +120,12 @@ __device__ __forceinline__ void pack_plane(const uint8_t* __restrict__ sb, uint8
     }
 }
 
-template <int B>
+template <int side, int B>
 __device__ __forceinline__ void pack_group(const uint8_t* __restrict__ sb, uint8_t* __restrict__ tbase, int r, int sl0,
                                            int n_sl, int lane) {
-    pack_plane<B, 0>(sb, tbase, r, sl0, n_sl, lane);
-    pack_plane<B, 1>(sb, tbase, r, sl0, n_sl, lane);
-    pack_plane<B, 2>(sb, tbase, r, sl0, n_sl, lane);
+    pack_plane<side, B, 0>(sb, tbase, r, sl0, n_sl, lane);
+    pack_plane<side, B, 1>(sb, tbase, r, sl0, n_sl, lane);
+    pack_plane<side, B, 2>(sb, tbase, r, sl0, n_sl, lane);
 }
 
 template <int side>
@@ -107,7 +137,7 @@ __global__ __launch_bounds__(kEncMmaThreads) __attribute__((amdgpu_waves_per_eu(
     float* tolc = reinterpret_cast<float*>(Pl + kD * kPRow);           // [128] 2^-16 1.01 ||P_i|| / step (NaN for i >= r)
     float* pnrm = tolc + kD;                                           // [128] ||P_i||
     float* etoks = pnrm + kD;                                          // [4 waves][64] token norms
-    uint8_t* slots = reinterpret_cast<uint8_t*>(etoks + 4 * kTile);    // [4 waves][1024] codes of one slot group
+    uint8_t* slots = reinterpret_cast<uint8_t*>(etoks + 4 * kTile);    // [4 waves][kSlotBufBytes] codes of one slot group
     const int u = blockIdx.y, tid = threadIdx.x;
     const int r = s.r[u], b = s.b[u];
     const float step = s.delta[u];
@@ -131,7 +161,7 @@ __global__ __launch_bounds__(kEncMmaThreads) __attribute__((amdgpu_waves_per_eu(
     __syncthreads();
 
     const int wv = tid >> 6, lane = tid & 63, col = lane & 15, grp = lane >> 4;
-    uint8_t* __restrict__ sb = slots + wv * 1024;
+    uint8_t* __restrict__ sb = slots + wv * kSlotBufBytes;
     float* __restrict__ etok = etoks + wv * kTile;
     const int h = 1 << (b - 1);
     const float fh = (float)h, fmax_code = (float)(2 * h - 1), inv = 1.f / step;
@@ -141,6 +171,27 @@ __global__ __launch_bounds__(kEncMmaThreads) __attribute__((amdgpu_waves_per_eu(
     uint8_t* __restrict__ stream = s.codes + s.code_off[u];
     const uint16_t* __restrict__ xu = x + (int64_t)u * x_stride;
 
+    // Token fragments: operand row 16 nt + col, dims 32 ks + 8 grp + [0, 8). The row holds token
+    // 16 nt + col for K; for V, token 16 nt + kidx_b(col), the token whose slot in the quarter is
+    // position col (pos_b o kidx_b = identity), so that a lane's four results (rows 4 grp + i) are
+    // four consecutive slot bytes. Tokens outside the range read a valid token and never reach the
+    // stream. The fragments of a wavefront's next tile are loaded as soon as the last products of the
+    // current one have read them, so that the loads overlap the tile's last decisions and packing.
+    const int trow = side == KVC_SIDE_K ? col : kidx_b(b, col);
+    h8 xf[4][4];
+    auto load_x = [&](int tl) {
+        const int tok0n = (tile_first + tl) * kTile;
+        const int lon = max(t0, tok0n), hin = min(t0 + n_tok, tok0n + kTile);
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) {
+            const int tk = tok0n + 16 * nt + trow;
+            const h8* row = reinterpret_cast<const h8*>(xu + (int64_t)((tk >= lon && tk < hin ? tk : lon) - t0) * kD);
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks) xf[nt][ks] = row[4 * ks + grp];
+        }
+    };
+    if (blockIdx.x * kEncMmaTilesPerBlock + wv < n_tiles) load_x(blockIdx.x * kEncMmaTilesPerBlock + wv);
+
 #pragma unroll 1
     for (int tt = wv; tt < kEncMmaTilesPerBlock; tt += kEncMmaThreads / 64) {
         const int tl_idx = blockIdx.x * kEncMmaTilesPerBlock + tt;
@@ -149,24 +200,18 @@ __global__ __launch_bounds__(kEncMmaThreads) __attribute__((amdgpu_waves_per_eu(
         const int lo = max(t0, tok0), hi = min(t0 + n_tok, tok0 + kTile);
         const bool full = lo == tok0 && hi == tok0 + kTile;
         uint8_t* __restrict__ tbase = stream + (int64_t)tile * 8 * r * b;
+        const int tl_next = tl_idx + kEncMmaThreads / 64;
+        const bool has_next = tt + kEncMmaThreads / 64 < kEncMmaTilesPerBlock && tl_next < n_tiles;
 
-        // Token fragments: operand row 16 nt + col, dims 32 ks + 8 grp + [0, 8). The row holds token
-        // 16 nt + col for K; for V, token 16 nt + kidx_b(col), the token whose slot in the quarter is
-        // position col (pos_b o kidx_b = identity), so that a lane's four results (rows 4 grp + i) are
-        // four consecutive slot bytes. Tokens outside the range read a valid token and never reach the
-        // stream. etok is indexed by operand row.
-        h8 xf[4][4];
+        // etok is indexed by operand row.
         float et[4];  // ||x|| of the lane's token (NaN outside the range: such elements are never undecided)
-        const int trow = side == KVC_SIDE_K ? col : kidx_b(b, col);
 #pragma unroll
         for (int nt = 0; nt < 4; ++nt) {
             const int tk = tok0 + 16 * nt + trow;
             const bool ok = tk >= lo && tk < hi;
-            const h8* row = reinterpret_cast<const h8*>(xu + (int64_t)((ok ? tk : lo) - t0) * kD);
             float s2 = 0.f;
 #pragma unroll
             for (int ks = 0; ks < 4; ++ks) {
-                xf[nt][ks] = row[4 * ks + grp];
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     const h2 v = {xf[nt][ks][2 * e], xf[nt][ks][2 * e + 1]};
@@ -193,6 +238,7 @@ __global__ __launch_bounds__(kEncMmaThreads) __attribute__((amdgpu_waves_per_eu(
                 for (int ks = 0; ks < 4; ++ks)
                     acc[nt] = side == KVC_SIDE_K ? mfma_f16(pf[ks], xf[nt][ks], acc[nt]) : mfma_f16(xf[nt][ks], pf[ks], acc[nt]);
             }
+            if (mc == n_mc - 1 && has_next) load_x(tl_next);
             // K: lane holds coordinates 16 mc + 4 grp + i of token 16 nt + col.
             // V: lane holds tokens 16 nt + 4 grp + i of coordinate 16 mc + col.
             // t = y / step + 2^(b-1): its floor, clamped, is the code. With t' = t - 1/2 (one fused
@@ -234,7 +280,7 @@ __global__ __launch_bounds__(kEncMmaThreads) __attribute__((amdgpu_waves_per_eu(
             } else if (16 * mc + col < r) {
                 // operand rows 16 nt + 4 grp + i of coordinate row col: slot positions 4 grp + i of quarter nt
 #pragma unroll
-                for (int nt = 0; nt < 4; ++nt) *reinterpret_cast<uint32_t*>(sb + 64 * col + 16 * nt + 4 * grp) = cw[nt];
+                for (int nt = 0; nt < 4; ++nt) *reinterpret_cast<uint32_t*>(sb + kVRow * col + 16 * nt + 4 * grp) = cw[nt];
             }
             // undecided elements (rare): flag them again per lane, then the whole wavefront settles
             // them one by one
@@ -253,7 +299,7 @@ __global__ __launch_bounds__(kEncMmaThreads) __attribute__((amdgpu_waves_per_eu(
                 while (pend) {
                     const int L = __builtin_ctzll(pend);
                     pend &= pend - 1;
-                    uint32_t m = __shfl(ambm, L);
+                    uint32_t m = (uint32_t)__builtin_amdgcn_readlane((int)ambm, L);
                     const int Lcol = L & 15, Lgrp = L >> 4;
                     while (m) {
                         const int bit = __builtin_ctz(m);
@@ -274,7 +320,7 @@ __global__ __launch_bounds__(kEncMmaThreads) __attribute__((amdgpu_waves_per_eu(
                         const uint16_t* xrow = xu + (int64_t)(tok0 + tkn - t0) * kD;
                         const uint32_t code = resolve_code_wave(Pl + c * kPRow, Pg + (int64_t)c * kD, xrow, step, b,
                                                                 pnrm[c], etok[row], lane);
-                        if (lane == 0) sb[sl] = (uint8_t)code;
+                        if (lane == 0) sb[sb_off<side>(sl)] = (uint8_t)code;
                     }
                 }
             }
@@ -283,7 +329,7 @@ __global__ __launch_bounds__(kEncMmaThreads) __attribute__((amdgpu_waves_per_eu(
             const int n_sl = (rho && mc == n_mc - 1) ? 64 * rho : 1024;  // K tail group / V last coordinate rows
             const int sl0 = 1024 * mc;
             if (full) {
-                KVC_SWITCH_B(b, pack_group<B_>(sb, tbase, r, sl0, n_sl, lane));
+                KVC_SWITCH_B(b, (pack_group<side, B_>(sb, tbase, r, sl0, n_sl, lane)));
             } else {
                 // partial tile: rewrite only the slots of tokens in [lo, hi)
                 for (int p = 8, off = 0; p >= 1; p >>= 1) {
@@ -302,7 +348,7 @@ __global__ __launch_bounds__(kEncMmaThreads) __attribute__((amdgpu_waves_per_eu(
                             const int tk = tok0 + t2;
                             if (tk >= lo && tk < hi) {
                                 const int bit = p * io;
-                                word |= (((uint32_t)sb[wi * ppw + io] >> sh) & vm) << bit;
+                                word |= (((uint32_t)sb[sb_off<side>(wi * ppw + io)] >> sh) & vm) << bit;
                                 msk |= vm << bit;
                             }
                         }
@@ -409,7 +455,7 @@ extern "C" int kvc_encode(const kvc_stream_desc* s, const uint16_t* x, int64_t x
     }
     const int tile_first = t0 / kTile;
     const int n_tiles = (t0 + n_tok - 1) / kTile - tile_first + 1;
-    const size_t smem = (size_t)kD * kPRow * 2 + 2 * kD * 4 + (kEncMmaThreads / 64) * (kTile * 4 + 1024);
+    const size_t smem = (size_t)kD * kPRow * 2 + 2 * kD * 4 + (kEncMmaThreads / 64) * (kTile * 4 + kSlotBufBytes);
     dim3 grid((n_tiles + kEncMmaTilesPerBlock - 1) / kEncMmaTilesPerBlock, s->n_units);
     if (s->side == KVC_SIDE_K)
         hipLaunchKernelGGL(encode_mfma_kernel<KVC_SIDE_K>, grid, dim3(kEncMmaThreads), smem, (hipStream_t)stream,
