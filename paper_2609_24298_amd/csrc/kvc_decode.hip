@@ -1626,11 +1626,13 @@ int64_t resident_slots(int G, size_t smem) {
 // Split of each unit's context into n_chunks equal chunks of whole tiles (at most kMaxChunkTiles
 // each). The count minimises
 //   rounds x (tiles per item + per-item overhead) + (straggler share) x tiles per item,
-// rounds = ceil(items / resident slots): whole rounds with no short remainder, items short enough
-// that units of different cost even out, and no more items than that (one round of longer items
-// can beat two rounds of items half as long that would fill every slot).
+// rounds = ceil(items / resident slots): whole rounds with no short remainder, and no more items
+// than that (one round of longer items can beat two rounds of items half as long that would fill
+// every slot). The two constants are fitted to the partials kernel's times on the 8B-shaped 32k
+// workload at 3, 6 and 9 chunks per unit (2, 4 and 6 rounds): about four tiles of work per item,
+// and a small straggler share, as the hardware hands each freed slot the next item.
 constexpr int kItemOverheadTiles = 4;
-constexpr double kStragglerShare = 0.5;
+constexpr double kStragglerShare = 0.1;
 
 struct WsLayout {
     int chunk, n_chunks, stage_bytes;
