@@ -1012,9 +1012,13 @@ constexpr int kRopeWaves = 4;
 constexpr int kPtPitch = 136;   // halves per feature row of the staged P_K^T (coordinates 0..127 + pad)
 constexpr int kZPitch = 136;    // halves per token row of a staged 16-token block of centred K codes
 constexpr int kRopeKTile = 8 * kD * 8;  // bytes of the widest K tile (r = 128, b = 8)
+constexpr int kRopeShared = kD * kPtPitch * 2 + 64 * 8;  // LDS shared by a block's wavefronts: P_K^T, E16
 constexpr int kRopeKChunks = kRopeKTile / 16 / 64;  // 16-byte loads per lane for one K tile
-__host__ __device__ constexpr int rope_wave_lds(int LM) {
-    return kRopeKTile + 16 * kZPitch * 2 + 16 * LM * kPRowBytes + 64 * 4;
+// Blocks of 16 tokens processed together (their chains are independent and share each P_K^T operand
+// read): as many as the register file allows for the group size.
+__host__ __device__ constexpr int rope_blocks(int G) { return G <= 8 ? 2 : 1; }
+__host__ __device__ constexpr int rope_wave_lds(int G) {
+    return kRopeKTile + rope_blocks(G) * 16 * kZPitch * 2 + 16 * ((G + 3) / 4) * kPRowBytes + 64 * 4;
 }
 
 typedef _Float16 rp_h8 __attribute__((ext_vector_type(8)));
@@ -1107,6 +1111,14 @@ __global__ __launch_bounds__(64 * kRopeWaves) void decode_rope_kernel(
     const int col = lane & 15, kq = lane >> 4, grp = kq;
     const int rk = uni(K.r[u]), bk = uni(K.b[u]);
     uint16_t* PT = reinterpret_cast<uint16_t*>(rope_sm);  // [128 features][kPtPitch]
+    float2* E16 = reinterpret_cast<float2*>(rope_sm + kRopeShared - 64 * 8);  // [64 pairs] rotation by 16 positions
+    if (threadIdx.x < 64) {
+        // cos, sin of the rotation of pair j by 16 positions (turns reduced in fp64)
+        const int j = threadIdx.x;
+        const double w = exp2(-(double)j / 64.0 * (double)log2_base) * 0.15915494309189535;
+        const float t16 = (float)(6.283185307179586 * (16.0 * w - floor(16.0 * w)));
+        E16[j] = float2{cosf(t16), sinf(t16)};
+    }
     {
         // stage P_K^T: zero it (coordinates past the rank take part in the last 32-wide k-step), then
         // transpose the basis rows in
@@ -1125,10 +1137,11 @@ __global__ __launch_bounds__(64 * kRopeWaves) void decode_rope_kernel(
     }
     const int c = blockIdx.x * kRopeWaves + wv;
     if (c >= n_chunks) return;  // no block-wide barrier follows
-    uint8_t* wbase = rope_sm + kD * kPtPitch * 2 + wv * rope_wave_lds(LM);
+    constexpr int NB = rope_blocks(G);
+    uint8_t* wbase = rope_sm + kRopeShared + wv * rope_wave_lds(G);
     uint8_t* KS = wbase;                                               // the K tile being processed
-    uint16_t* ZT = reinterpret_cast<uint16_t*>(wbase + kRopeKTile);     // [16 tokens][kZPitch]
-    uint8_t* pmat = wbase + kRopeKTile + 16 * kZPitch * 2;             // [16 LM][kPRowBytes]
+    uint16_t* ZT = reinterpret_cast<uint16_t*>(wbase + kRopeKTile);     // [NB blocks][16 tokens][kZPitch]
+    uint8_t* pmat = wbase + kRopeKTile + NB * 16 * kZPitch * 2;        // [16 LM][kPRowBytes]
     float* rho0 = reinterpret_cast<float*>(pmat + 16 * LM * kPRowBytes);  // [64] tile start, turns
 
     int T = uni(seq_len[u]);
@@ -1227,68 +1240,94 @@ __global__ __launch_bounds__(64 * kRopeWaves) void decode_rope_kernel(
             const double t0 = (double)tok0 * om_lane;
             rho0[lane] = (float)(t0 - floor(t0));
         }
+        // rotation of the lane's token in block 0 (position tok0 + col) for each of its pairs, as cos, sin;
+        // block tb's follows by tb rotations of 16 positions
+        float wc[4][4], ws[4][4];
+        wave_lds_sync();  // rho0 written above
+#pragma unroll
+        for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                float tr = fmaf((float)col, om[rb][v], rho0[16 * rb + 4 * kq + v]);
+                tr -= floorf(tr);
+                wc[rb][v] = __cosf(6.283185307179586f * tr);
+                ws[rb][v] = __sinf(6.283185307179586f * tr);
+            }
         float s[4][4];  // [token block][head v], log2 domain
 #pragma unroll
         for (int a = 0; a < 4; ++a)
 #pragma unroll
             for (int v = 0; v < 4; ++v) s[a][v] = -INFINITY;
+        // The tile's four blocks of 16 tokens in groups of NB (tb = NB tp + h): the blocks' chains are
+        // independent and share each P_K^T operand read.
 #pragma unroll 1
-        for (int tb = 0; tb < 4; ++tb) {
-            {
+        for (int tp = 0; tp < 4 / NB; ++tp) {
+#pragma unroll
+            for (int h = 0; h < NB; ++h) {
                 // stage the centred codes of tokens 16 tb .. 16 tb + 15: lane (token col, part kq) takes
                 // coordinates 32 kq .. 32 kq + 31 (zero past the rank, within the 32-wide k-steps)
-                const int t = 16 * tb + colt;
-                KVC_SWITCH_B(bkt, (rope_stage_codes<B_>(ktile, rkt, g16t, rhot, kqt, t, ZT + colt * kZPitch)));
+                const int t = 16 * (NB * tp + h) + colt;
+                KVC_SWITCH_B(bkt, (rope_stage_codes<B_>(ktile, rkt, g16t, rhot, kqt, t, ZT + (16 * h + colt) * kZPitch)));
             }
             wave_lds_sync();
-            // K^T block: rows 16 rb + 4 kq + v, column token col
-            rp_f4 Cr[8];
+            // K^T blocks: rows 16 rb + 4 kq + v, column token col
+            rp_f4 Cr[NB][8];
 #pragma unroll
-            for (int rb = 0; rb < 8; ++rb) Cr[rb] = rp_f4{0.f, 0.f, 0.f, 0.f};
+            for (int h = 0; h < NB; ++h)
+#pragma unroll
+                for (int rb = 0; rb < 8; ++rb) Cr[h][rb] = rp_f4{0.f, 0.f, 0.f, 0.f};
             for (int ks = 0; ks < nkst; ++ks) {
-                const rp_h8 bz = *reinterpret_cast<const rp_h8*>(ZT + col * kZPitch + 32 * ks + 8 * kq);
+                rp_h8 bz[NB];
+#pragma unroll
+                for (int h = 0; h < NB; ++h)
+                    bz[h] = *reinterpret_cast<const rp_h8*>(ZT + (16 * h + col) * kZPitch + 32 * ks + 8 * kq);
 #pragma unroll
                 for (int rb = 0; rb < 8; ++rb) {
                     const rp_h8 ap = *reinterpret_cast<const rp_h8*>(PT + (16 * rb + col) * kPtPitch + 32 * ks + 8 * kq);
-                    Cr[rb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ap, bz, Cr[rb], 0, 0, 0);
+#pragma unroll
+                    for (int h = 0; h < NB; ++h) Cr[h][rb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ap, bz[h], Cr[h][rb], 0, 0, 0);
                 }
             }
-            wave_lds_sync();  // ZT is rewritten by the next block
-            // rotate each pair (j, j + 64) of token 16 tb + col at its position
-            const float dpos = (float)(16 * tb + col);
+            wave_lds_sync();  // ZT is rewritten by the next group of blocks
 #pragma unroll
-            for (int rb = 0; rb < 4; ++rb)
+            for (int h = 0; h < NB; ++h) {
+                const int tb = NB * tp + h;
+                // rotate each pair (j, j + 64) of token 16 tb + col at its position, then advance the
+                // rotation by 16 positions for the next block
 #pragma unroll
-                for (int v = 0; v < 4; ++v) {
-                    const int j = 16 * rb + 4 * kq + v;
-                    float tr = fmaf(dpos, om[rb][v], rho0[j]);
-                    tr -= floorf(tr);
-                    const float cs = __cosf(6.283185307179586f * tr), sn = __sinf(6.283185307179586f * tr);
-                    const float a = Cr[rb][v], b = Cr[rb + 4][v];
-                    Cr[rb][v] = a * cs - b * sn;
-                    Cr[rb + 4][v] = a * sn + b * cs;
+                for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) {
+                        const float cs = wc[rb][v], sn = ws[rb][v];
+                        const float a = Cr[h][rb][v], b = Cr[h][rb + 4][v];
+                        Cr[h][rb][v] = fmaf(a, cs, -b * sn);
+                        Cr[h][rb + 4][v] = fmaf(a, sn, b * cs);
+                        const float2 e = E16[16 * rb + 4 * kq + v];
+                        wc[rb][v] = fmaf(cs, e.x, -sn * e.y);
+                        ws[rb][v] = fmaf(cs, e.y, sn * e.x);
+                    }
+                // logits: sum over features of q' times (hi + lo) of the rotated key
+                rp_f4 S = rp_f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int ks = 0; ks < 4; ++ks) {
+                    rp_h8 bh, bl;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const float x = Cr[h][2 * ks + (e >> 2)][e & 3];
+                        const _Float16 hx = (_Float16)x;
+                        bh[e] = hx;
+                        bl[e] = (_Float16)(x - (float)hx);
+                    }
+                    S = __builtin_amdgcn_mfma_f32_16x16x32_f16(qa[ks], bh, S, 0, 0, 0);
+                    S = __builtin_amdgcn_mfma_f32_16x16x32_f16(qa[ks], bl, S, 0, 0, 0);
                 }
-            // logits: sum over features of q' times (hi + lo) of the rotated key
-            rp_f4 S = rp_f4{0.f, 0.f, 0.f, 0.f};
+                const bool valid_tok = tok0 + 16 * tb + col < end;
 #pragma unroll
-            for (int ks = 0; ks < 4; ++ks) {
-                rp_h8 bh, bl;
+                for (int a = 0; a < 4; ++a)  // s[tb] without a run-time register index
 #pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const float x = Cr[2 * ks + (e >> 2)][e & 3];
-                    const _Float16 hx = (_Float16)x;
-                    bh[e] = hx;
-                    bl[e] = (_Float16)(x - (float)hx);
-                }
-                S = __builtin_amdgcn_mfma_f32_16x16x32_f16(qa[ks], bh, S, 0, 0, 0);
-                S = __builtin_amdgcn_mfma_f32_16x16x32_f16(qa[ks], bl, S, 0, 0, 0);
+                    for (int v = 0; v < 4; ++v)
+                        if (a == tb) s[a][v] = (valid_tok && 4 * kq + v < G) ? S[v] * scale : -INFINITY;
             }
-            const bool valid_tok = tok0 + 16 * tb + col < end;
-#pragma unroll
-            for (int a = 0; a < 4; ++a)  // s[tb] without a run-time register index
-#pragma unroll
-                for (int v = 0; v < 4; ++v)
-                    if (a == tb) s[a][v] = (valid_tok && 4 * kq + v < G) ? S[v] * scale : -INFINITY;
         }
 
         // ---- online softmax of the tile: heads 4 kq + v live in the 16 lanes of group kq
@@ -1860,8 +1899,7 @@ namespace {
 template <int G>
 int launch_rope(const kvc_stream_desc* k, const kvc_stream_desc* v, const uint16_t* q, const int32_t* seq_len,
                 int32_t max_seq_len, float log2_base, float* out, const WsLayout& L, float* part, hipStream_t st) {
-    constexpr int LM = (G + 3) / 4;
-    const size_t smem = (size_t)kD * kPtPitch * 2 + (size_t)kRopeWaves * rope_wave_lds(LM);
+    const size_t smem = (size_t)kRopeShared + (size_t)kRopeWaves * rope_wave_lds(G);
     if (smem > 64 * 1024) {
         const hipError_t e = hipFuncSetAttribute((const void*)decode_rope_kernel<G>,
                                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
