@@ -1024,80 +1024,109 @@ __host__ __device__ constexpr int rope_wave_lds(int G) {
 typedef _Float16 rp_h8 __attribute__((ext_vector_type(8)));
 typedef float rp_f4 __attribute__((ext_vector_type(4)));
 
-// Codes of group g (16 coordinates) of token t of a K tile: c[m] for coordinate 16 g + m. The group's
-// field of a plane of width p is 16 p bits at bit p (1024 g + 16 t) of the plane.
-template <int B>
-__device__ __forceinline__ void k_group_codes(const uint8_t* __restrict__ tile, int r, int g, int t, uint32_t (&c)[16]) {
-    if constexpr (B == 8) {
-        const uint4 w = *reinterpret_cast<const uint4*>(tile + 16 * (64 * g + t));
-        const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
+// Position of coordinate i in a staged row of centred K codes (and in the staged P_K^T): inside each
+// group of 16, coordinates m and m + 8 (m < 8) are neighbours, at 2 m and 2 m + 1, so that a pair of
+// codes converts to fp16 as one packed dword. The k order of the reconstruction's products is free.
+__host__ __device__ constexpr int zpos(int i) { return (i & ~15) | ((i & 7) << 1) | ((i >> 3) & 1); }
+
+// A 16-code field of one plane of width p (codes 16 g + m at bits p m), aligned at bit 0 in f[0 .. p / 2)
+// (f[0] low 16 bits for p = 1), as the pairs (m, m + 8): bits [0, p) and [16, 16 + p) of pr[m], the rest
+// of each half zero.
+template <int P>
+__device__ __forceinline__ void plane_pairs(const uint32_t (&f)[4], uint32_t (&pr)[8]) {
+    if constexpr (P == 1) {
+        const uint32_t y = (f[0] & 0xffu) | ((f[0] & 0xff00u) << 8);  // code m + 8 at bit 16 + m
 #pragma unroll
-        for (int m = 0; m < 16; ++m) c[m] = __builtin_amdgcn_ubfe(ww[m >> 2], 8 * (m & 3), 8);
+        for (int m = 0; m < 8; ++m) pr[m] = (y >> m) & 0x00010001u;
+    } else if constexpr (P == 2) {
+#pragma unroll
+        for (int m = 0; m < 8; ++m) pr[m] = (f[0] >> (2 * m)) & 0x00030003u;
+    } else if constexpr (P == 4) {
+        const uint32_t y01 = perm(f[1], f[0], 0x05040100u), y23 = perm(f[1], f[0], 0x07060302u);
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+            pr[m] = (y01 >> (4 * m)) & 0x000f000fu;
+            pr[m + 4] = (y23 >> (4 * m)) & 0x000f000fu;
+        }
     } else {
 #pragma unroll
-        for (int m = 0; m < 16; ++m) c[m] = 0u;
-#pragma unroll
-        for (int k = 0; k < n_planes(B); ++k) {
-            const int P = plane_w(B, k), SH = plane_sh(B, k), OFF = plane_off(B, k);
-            const uint8_t* base = tile + 8 * r * OFF + P * (128 * g + 2 * t);
-            uint32_t f[2] = {0u, 0u};
-            if (P == 1) f[0] = *reinterpret_cast<const uint16_t*>(base);
-            else if (P == 2) f[0] = *reinterpret_cast<const uint32_t*>(base);
-            else { const uint2 v2 = *reinterpret_cast<const uint2*>(base); f[0] = v2.x; f[1] = v2.y; }
-#pragma unroll
-            for (int m = 0; m < 16; ++m) {
-                const uint32_t v = __builtin_amdgcn_ubfe(f[(P * m) >> 5], (P * m) & 31, P);
-                c[m] = k == 0 ? (v << SH) : (c[m] | (v << SH));
+        for (int m = 0; m < 8; ++m)  // byte m % 4 of dwords m / 4 and m / 4 + 2, zero bytes between
+            pr[m] = perm(f[(m >> 2) + 2], f[m >> 2], 0x0c040c00u + 0x00010001u * (uint32_t)(m & 3));
+    }
+}
+
+// The fields of group g of token t of a K tile, aligned: a whole group's field of a plane of width p is
+// 16 p bits at bit p (1024 g + 16 t) of the plane; the tail group's (rho = r % 16 codes) starts at
+// bit p (1024 g16 + t rho) and is aligned with funnel shifts over five words (codes past rho are other
+// tokens' codes: finite, and they meet zero basis entries).
+template <int P>
+__device__ __forceinline__ void group_field(const uint8_t* __restrict__ plane, bool tail, int g, int g16, int rho, int t,
+                                            uint32_t (&f)[4]) {
+    if (!tail) {
+        const uint8_t* base = plane + P * (128 * g + 2 * t);
+        if constexpr (P == 1) {
+            f[0] = *reinterpret_cast<const uint16_t*>(base);
+        } else if constexpr (P == 2) {
+            f[0] = *reinterpret_cast<const uint32_t*>(base);
+        } else if constexpr (P == 4) {
+            const uint2 v2 = *reinterpret_cast<const uint2*>(base);
+            f[0] = v2.x; f[1] = v2.y;
+        } else {
+            const uint4 v4 = *reinterpret_cast<const uint4*>(base);
+            f[0] = v4.x; f[1] = v4.y; f[2] = v4.z; f[3] = v4.w;
+        }
+    } else {
+        const uint32_t bit0 = (uint32_t)(P * (1024 * g16 + t * rho));
+        const uint32_t* w = reinterpret_cast<const uint32_t*>(plane) + (bit0 >> 5);
+        const uint32_t d0 = w[0], d1 = w[1];
+        f[0] = funnel(d1, d0, bit0);
+        if constexpr (P >= 4) {
+            const uint32_t d2 = w[2];
+            f[1] = funnel(d2, d1, bit0);
+            if constexpr (P == 8) {
+                const uint32_t d3 = w[3], d4 = w[4];
+                f[2] = funnel(d3, d2, bit0);
+                f[3] = funnel(d4, d3, bit0);
             }
         }
     }
 }
 
-// Codes of the tail group (rho = r % 16 coordinates after the 16 g16 of the whole groups) of token t: the
-// rho p bits of a plane start at bit p (1024 g16 + t rho); five words around them are aligned with
-// funnel shifts, so that every code sits at a fixed bit of the aligned value.
-template <int B>
-__device__ __forceinline__ void k_tail_codes(const uint8_t* __restrict__ tile, int r, int g16, int rho, int t,
-                                             uint32_t (&c)[16]) {
-#pragma unroll
-    for (int m = 0; m < 16; ++m) c[m] = 0u;
-#pragma unroll
-    for (int k = 0; k < n_planes(B); ++k) {
-        const int P = plane_w(B, k), SH = plane_sh(B, k), OFF = plane_off(B, k);
-        const uint32_t bit0 = (uint32_t)(P * (1024 * g16 + t * rho));
-        const uint32_t* w = reinterpret_cast<const uint32_t*>(tile + 8 * r * OFF) + (bit0 >> 5);
-        const uint32_t d0 = w[0], d1 = w[1], d2 = w[2], d3 = w[3], d4 = w[4];
-        const uint32_t x[4] = {funnel(d1, d0, bit0), funnel(d2, d1, bit0), funnel(d3, d2, bit0), funnel(d4, d3, bit0)};
-#pragma unroll
-        for (int m = 0; m < 16; ++m) {
-            if (P * m >= 128) break;
-            const uint32_t v = __builtin_amdgcn_ubfe(x[(P * m) >> 5], (P * m) & 31, P);
-            c[m] |= v << SH;
-        }
-    }
-}
-
 // Stage the centred K codes (c - 2^(b-1) + 1/2, exact in fp16) of token t for the lane's two groups
-// 2 kq, 2 kq + 1 into its row of ZT (zero past the rank).
+// 2 kq, 2 kq + 1 into its row of ZT, in zpos order: per code pair, the planes' bits are combined one
+// bit up, under the fp16 exponent of 512 (512 + c, exact: the spacing there is 1/2), and moved by one
+// packed add of -512 - 2^(b-1) + 1/2 (also exact).
 template <int B>
 __device__ __forceinline__ void rope_stage_codes(const uint8_t* __restrict__ ktile, int rk, int g16, int rho, int kq,
                                                  int t, uint16_t* __restrict__ zrow) {
-    const _Float16 hk = (_Float16)((float)(1 << (B - 1)) - 0.5f);
+    typedef _Float16 h2v __attribute__((ext_vector_type(2)));
+    const _Float16 sh = (_Float16)(-512.f - ((float)(1 << (B - 1)) - 0.5f));
+    const h2v sh2 = h2v{sh, sh};
 #pragma unroll
     for (int gg = 0; gg < 2; ++gg) {
         const int g = 2 * kq + gg;
-        uint32_t c[16];
-        if (g < g16) k_group_codes<B>(ktile, rk, g, t, c);
-        else k_tail_codes<B>(ktile, rk, g16, rho, t, c);
-        rp_h8 h0, h1;
+        const bool tail = g >= g16;
+        uint32_t pc[8];
 #pragma unroll
-        for (int m = 0; m < 8; ++m) {
-            const bool in0 = g < g16 || (g == g16 && m < rho), in1 = g < g16 || (g == g16 && m + 8 < rho);
-            h0[m] = in0 ? (_Float16)(uint16_t)c[m] - hk : (_Float16)0.f;
-            h1[m] = in1 ? (_Float16)(uint16_t)c[8 + m] - hk : (_Float16)0.f;
+        for (int m = 0; m < 8; ++m) pc[m] = 0u;
+#pragma unroll
+        for (int k = 0; k < n_planes(B); ++k) {
+            const int P = plane_w(B, k), SH = plane_sh(B, k), OFF = plane_off(B, k);
+            uint32_t f[4] = {0u, 0u, 0u, 0u}, pr[8];
+            const uint8_t* plane = ktile + 8 * rk * OFF;
+            if (P == 1) { group_field<1>(plane, tail, g, g16, rho, t, f); plane_pairs<1>(f, pr); }
+            else if (P == 2) { group_field<2>(plane, tail, g, g16, rho, t, f); plane_pairs<2>(f, pr); }
+            else if (P == 4) { group_field<4>(plane, tail, g, g16, rho, t, f); plane_pairs<4>(f, pr); }
+            else { group_field<8>(plane, tail, g, g16, rho, t, f); plane_pairs<8>(f, pr); }
+#pragma unroll
+            for (int m = 0; m < 8; ++m) pc[m] |= pr[m] << (SH + 1);
         }
-        *reinterpret_cast<rp_h8*>(zrow + 16 * g) = h0;
-        *reinterpret_cast<rp_h8*>(zrow + 16 * g + 8) = h1;
+        uint32_t hw[8];
+#pragma unroll
+        for (int m = 0; m < 8; ++m)
+            hw[m] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(h2v, pc[m] | 0x60006000u) + sh2);
+        *reinterpret_cast<uint4*>(zrow + 16 * g) = uint4{hw[0], hw[1], hw[2], hw[3]};
+        *reinterpret_cast<uint4*>(zrow + 16 * g + 8) = uint4{hw[4], hw[5], hw[6], hw[7]};
     }
 }
 
@@ -1131,7 +1160,7 @@ __global__ __launch_bounds__(64 * kRopeWaves) void decode_rope_kernel(
             const uint4 w = reinterpret_cast<const uint4*>(P + (int64_t)i * kD)[f0 / 8];
             const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
-            for (int k = 0; k < 8; ++k) PT[(f0 + k) * kPtPitch + i] = (uint16_t)(ww[k >> 1] >> (16 * (k & 1)));
+            for (int k = 0; k < 8; ++k) PT[(f0 + k) * kPtPitch + zpos(i)] = (uint16_t)(ww[k >> 1] >> (16 * (k & 1)));
         }
         __syncthreads();
     }
