@@ -615,7 +615,9 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2, 2)))
 // same stream, read the appended codes.
 constexpr int kStepPrepThreads = 128;
 static_assert(kStepPrepThreads == kAppThreads, "the append uses one thread per coordinate");
-__global__ __launch_bounds__(kStepPrepThreads) void step_prep_kernel(
+// Three wavefronts per SIMD (166 registers, none spilled): 1.5 times the resident blocks of the
+// unconstrained allocation, so the 3 x units blocks run in fewer rounds.
+__global__ __launch_bounds__(kStepPrepThreads) __attribute__((amdgpu_waves_per_eu(3, 3))) void step_prep_kernel(
     DevSide K, DevSide V, const uint16_t* __restrict__ q, int G, int LM, v4i* __restrict__ qa, float4* __restrict__ qk,
     const uint16_t* __restrict__ xk, int64_t xk_stride, const uint16_t* __restrict__ xv, int64_t xv_stride, int t_new) {
     if (blockIdx.y == 0) qprep_unit<2>(K, q, G, LM, qa, qk, blockIdx.x);
