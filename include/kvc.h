@@ -27,18 +27,24 @@
  *  - a b-bit code is split into planes (b = 8: one 8-bit plane; otherwise the
  *    binary expansion of b, widest first, widest = most significant bits);
  *    the plane of width p is 8*r*p bytes, planes in that order;
- *  - inside a plane, slot phi holds its p bits at bits [p*phi, p*phi + p) of
- *    the plane (a little-endian bit stream);
- *  - slot of (token t in the tile, coordinate i), g16 = r/16, rho = r%16:
- *      K side: i < 16*g16: phi = (i/16)*1024 + t*16 + i%16 (token-major in
- *              groups of 16 coordinates); else phi = 1024*g16 + t*rho + (i - 16*g16);
- *      V side: phi = i*64 + 16*(t/16) + pos_b(t%16), with pos_b(m) = m (b = 8),
- *              8*(m/8) + 2*(m%4) + (m/4)%2 (b = 4), 4*(m%4) + m/4 (other b):
- *              coordinate-major, each quarter of 16 tokens in a fixed order;
- *    so a token's codes of a group of 16 coordinates (K) and a quarter of 16
+ *  - K side: inside a plane of width p, slot phi holds its p bits at bits
+ *    [p*phi, p*phi + p) of the plane (a little-endian bit stream); slot of
+ *    (token t in the tile, coordinate i), g16 = r/16, rho = r%16:
+ *      i < 16*g16: phi = (i/16)*1024 + t*16 + i%16 (token-major in groups of
+ *      16 coordinates); else phi = 1024*g16 + t*rho + (i - 16*g16);
+ *  - V side: field (n, c, q) holds coordinate 16n + c for the 16 tokens of
+ *    quarter q = t/16 of the tile, token t at position pos_b(t%16), p bits
+ *    each (2p bytes), with pos_b(m) = m (b = 8), 8*(m/8) + 2*(m%4) + (m/4)%2
+ *    (b = 4), 4*(m%4) + m/4 (other b). In a plane of width p the N-tiles n
+ *    form groups of g = 8/p (1 for p = 8), and the fields of coordinates
+ *    below r follow one another in the order (n/g, 4c + q, n), so the
+ *    fields of one (c, q) in a group are 16 consecutive bytes (fewer in a
+ *    short last group);
+ *  - so a token's codes of a group of 16 coordinates (K) and a quarter of 16
  *    tokens of one coordinate (V) are one bit field of 16p bits, unpacked by
- *    the decode kernels straight into matrix-core operands;
- *  - kvc_encode writes only the slots of the tokens it encodes; slots of
+ *    the decode kernels straight into matrix-core operands, and a lane of the
+ *    decode reads a V group of one plane with one 16-byte load;
+ *  - kvc_encode writes only the bits of the tokens it encodes; bits of
  *    tokens never encoded keep the arena's contents (zero if the caller
  *    zeroed the arena, which the reference packing assumes).
  */

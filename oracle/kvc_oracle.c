@@ -93,22 +93,37 @@ static int pos_b(int b, int m) {
     return 4 * (m % 4) + m / 4;
 }
 
-static int slot_of(int side, int t, int i, int r, int b) {
-    if (side == 0) {
-        int g16 = r / 16, rho = r % 16;
-        if (i < 16 * g16) return (i / 16) * 1024 + t * 16 + i % 16;
-        return 1024 * g16 + t * rho + (i - 16 * g16);
-    }
-    return i * 64 + 16 * (t / 16) + pos_b(b, t % 16);
+static int slot_k(int t, int i, int r) {
+    int g16 = r / 16, rho = r % 16;
+    if (i < 16 * g16) return (i / 16) * 1024 + t * 16 + i % 16;
+    return 1024 * g16 + t * rho + (i - 16 * g16);
 }
 
-/* codes[t*r+i] (t < n) -> stream of ceil(n/64) tiles (zero-filled by this function).
- * Slot phi of a plane of width p holds its bits at [p*phi, p*phi + p) of the plane. */
+/* Byte offset of every V field (n, c, q) inside a plane of width p, by enumeration in the layout's
+ * order: group n / g (g = 8 / p, 1 for p = 8), then L = 4 c + q, then n; fields of coordinates >= r
+ * are absent. off[64 n + 4 c + q]. */
+static void v_field_table(int r, int p, int *off) {
+    int g = p == 8 ? 1 : 8 / p, nvt = (r + 15) / 16, k = 0;
+    for (int n0 = 0; n0 < nvt; n0 += g)
+        for (int L = 0; L < 64; ++L)
+            for (int n = n0; n < n0 + g && n < nvt; ++n)
+                if (16 * n + L / 4 < r) off[64 * n + L] = 2 * p * k++;
+}
+
+/* Bit of the code of (token t in tile, coordinate i) inside its plane of width p (vtab: the plane's
+ * v_field_table on the V side). */
+static int64_t plane_bit(int side, int t, int i, int r, int b, int p, const int *vtab) {
+    if (side == 0) return (int64_t)p * slot_k(t, i, r);
+    return 8LL * vtab[64 * (i / 16) + 4 * (i % 16) + t / 16] + (int64_t)p * pos_b(b, t % 16);
+}
+
+/* codes[t*r+i] (t < n) -> stream of ceil(n/64) tiles (zero-filled by this function). */
 void oracle_pack(const uint8_t *codes, int n, int r, int b, int side, uint8_t *out) {
     int w[3];
     int np = n_planes(b, w);
     int n_tiles = (n + 63) / 64;
     int64_t tb = 8LL * r * b;
+    int vtab[512];
     memset(out, 0, (size_t)(n_tiles * tb));
     for (int tile = 0; tile < n_tiles; ++tile) {
         uint8_t *base = out + tile * tb;
@@ -117,12 +132,13 @@ void oracle_pack(const uint8_t *codes, int n, int r, int b, int side, uint8_t *o
             int p = w[k];
             int sh = 0;
             for (int k2 = k + 1; k2 < np; ++k2) sh += w[k2];
+            if (side != 0) v_field_table(r, p, vtab);
             for (int t = 0; t < 64; ++t) {
                 int tok = tile * 64 + t;
                 if (tok >= n) continue;
                 for (int i = 0; i < r; ++i) {
                     uint32_t v = (codes[(int64_t)tok * r + i] >> sh) & ((1u << p) - 1);
-                    int64_t bitpos = (int64_t)p * slot_of(side, t, i, r, b);
+                    int64_t bitpos = plane_bit(side, t, i, r, b, p, vtab);
                     base[plane_off + bitpos / 8] |= (uint8_t)(v << (bitpos % 8));
                 }
             }
@@ -136,6 +152,9 @@ void oracle_unpack(const uint8_t *stream, int n, int r, int b, int side, uint8_t
     int w[3];
     int np = n_planes(b, w);
     int64_t tb = 8LL * r * b;
+    int vtab[3][512];
+    if (side != 0)
+        for (int k = 0; k < np; ++k) v_field_table(r, w[k], vtab[k]);
     for (int tok = 0; tok < n; ++tok) {
         int tile = tok / 64, t = tok % 64;
         const uint8_t *base = stream + tile * tb;
@@ -146,7 +165,7 @@ void oracle_unpack(const uint8_t *stream, int n, int r, int b, int side, uint8_t
                 int p = w[k];
                 int sh = 0;
                 for (int k2 = k + 1; k2 < np; ++k2) sh += w[k2];
-                int64_t bitpos = (int64_t)p * slot_of(side, t, i, r, b);
+                int64_t bitpos = plane_bit(side, t, i, r, b, p, vtab[k]);
                 c |= ((uint32_t)(base[plane_off + bitpos / 8] >> (bitpos % 8)) & ((1u << p) - 1)) << sh;
                 plane_off += 8LL * r * p;
             }

@@ -221,8 +221,8 @@ __device__ __forceinline__ void append_unit(const DevSide& s, int side, const ui
     // Merge, per new token and plane. K: a token's 16 codes of a full coordinate group are 16
     // consecutive slots, i.e. whole 16-bit (p = 1) or 32-bit words that belong to this token alone:
     // the group's lanes OR their fields together and one lane per word stores it. The tail group's
-    // fields, and every V field (one slot of a coordinate row shared with other tokens), are written
-    // in place with an atomic clear and set of the field's bits (a field never straddles a word).
+    // fields, and every V code (p bits of a field of 16 tokens shared with other tokens), are written
+    // in place with an atomic clear and set of its bits (they never straddle a word).
     // One thread owns each coordinate, so the new tokens of a call are written in order.
     uint8_t* __restrict__ stream = s.codes + s.code_off[u];
     const int g16 = r >> 4, rho = r & 15;
@@ -248,8 +248,7 @@ __device__ __forceinline__ void append_unit(const DevSide& s, int side, const ui
                     else *reinterpret_cast<uint32_t*>(w) = v;
                 }
             } else {
-                const int phi = side == KVC_SIDE_K ? 1024 * g16 + tt * rho + (i - 16 * g16) : slot_v(tt, i, b);
-                const int bit = p * phi;
+                const int bit = side == KVC_SIDE_K ? p * (1024 * g16 + tt * rho + (i - 16 * g16)) : v_plane_bit(tt, i, r, b, p);
                 if (p == 8) {
                     base[bit >> 3] = (uint8_t)pb;
                 } else {

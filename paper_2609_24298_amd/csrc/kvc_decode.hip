@@ -159,15 +159,36 @@ __device__ __forceinline__ v4i unpack16(const Fld (&f)[3], bool hi1) {
 __host__ __device__ constexpr int k_step_words(int b) { return 2 * b; }
 __host__ __device__ constexpr int plane_stage_off(int b, int k) { return 512 * plane_off(b, k); }  // LDS bytes
 constexpr int kKBufWords = 16;  // prefetch registers per side
-__host__ __device__ constexpr bool k_prefetch_both(int b) { return 2 * k_step_words(b) <= kKBufWords; }
-// words of one value N-tile field per lane, and N-tiles prefetched
-__host__ __device__ constexpr int v_words(int b) {
-    return b == 8 ? 4 : ((b & 4 ? 2 : 0) + (b & 2 ? 1 : 0) + (b & 1 ? 1 : 0));
+// K-steps' words kept in the prefetch registers: both K-steps of the widths where they fit, also for the
+// structure taken at run time (KM < 0); the one K-step of ranks <= 64 (KM >= 2) for every width.
+__host__ __device__ constexpr bool k_prefetch_on(int b, int km) {
+    return 2 * k_step_words(b) <= kKBufWords || (km >= 2 && k_step_words(b) <= kKBufWords);
 }
+// The second K-step's load is issued (absent K-steps read past the stream and return zero) wherever
+// its words fit the registers, so that every tile issues the same loads.
+__host__ __device__ constexpr bool k_second_load(int b) { return 2 * k_step_words(b) <= kKBufWords; }
 constexpr int kVBufWords = 16;  // value prefetch registers
 constexpr int kPrefetchDepth = 2;  // tiles of K and V loads in flight ahead of the one being processed (the
                                     // general path keeps one: its per-tile width switches need the registers)
-__host__ __device__ constexpr int v_prefetch_tiles(int b) { return kVBufWords / v_words(b) < 8 ? kVBufWords / v_words(b) : 8; }
+
+// Value groups (v_field_off): a plane of width p keeps the fields of v_group(p) = 8 / p consecutive
+// N-tiles of a lane together (16 bytes), so a lane reads a group of one plane with one 16-byte load.
+__host__ __device__ constexpr int v_group(int p) { return v_group_ntiles(p); }
+__host__ __device__ constexpr int cdiv(int a, int b) { return (a + b - 1) / b; }
+// Prefetch registers taken by the groups of the first n N-tiles, plane k's groups starting at word
+// v_pf_base(b, k, n), and the N-tiles prefetched for a rank bound of NV N-tiles (whole groups that
+// fit kVBufWords; the groups past them are loaded while the tile is processed).
+__host__ __device__ constexpr int v_pf_base(int b, int k, int n) {
+    int w = 0;
+    for (int j = 0; j < k; ++j) w += 4 * cdiv(n, v_group(plane_w(b, j)));
+    return w;
+}
+__host__ __device__ constexpr int v_pf_words(int b, int n) { return v_pf_base(b, n_planes(b), n); }
+__host__ __device__ constexpr int v_pf_tiles(int b, int nv) {
+    int n = nv;
+    while (n > 0 && v_pf_words(b, n) > kVBufWords) --n;
+    return n;
+}
 
 // Direct loads of one K-step's fields into w[0 .. 2B).
 template <int B>
@@ -270,14 +291,14 @@ __device__ __forceinline__ void k_fetch(uint32_t* w, const __amdgpu_buffer_rsrc_
 
 // Prefetch of a unit's first tile (both K-steps, for the widths whose two K-steps fit the prefetch
 // registers; wider codes are loaded when their tile is processed).
-template <int B>
+template <int B, int KM>
 __device__ __forceinline__ void k_prefetch(uint32_t (&kb)[kKBufWords], const __amdgpu_buffer_rsrc_t rs, int rk, int nk,
                                            int ks_t, const uint32_t (&LK)[2], int lane) {
     constexpr int W0 = k_step_words(B);
     (void)nk;
-    if constexpr (k_prefetch_both(B)) {
+    if constexpr (k_prefetch_on(B, KM)) {
         k_fetch<B>(kb, rs, rk, LK[0]);
-        k_fetch<B>(kb + W0, rs, rk, LK[1]);
+        if constexpr (k_second_load(B)) k_fetch<B>(kb + W0, rs, rk, LK[1]);
     }
 }
 
@@ -309,20 +330,25 @@ __device__ __forceinline__ void k_tile(uint32_t (&kb)[kKBufWords], uint32_t (&kb
     // K-step structure fixed at compile time when KM >= 0 (see k_mode), else taken at run time
     const int nk = KM >= 0 ? (KM < 2 ? 2 : 1) : nk_rt;
     const int ks_t = KM >= 0 ? (KM == 1 ? 1 : (KM == 3 ? 0 : 2)) : ks_t_rt;
-    if constexpr (k_prefetch_both(B)) {
+    if constexpr (k_prefetch_on(B, KM)) {
         // The staged K-step goes to LDS first (constant indices into kb: a runtime one would move the
         // array to scratch memory). Every load below is issued unconditionally, in the same order on
         // every tile (absent K-steps read past the stream and return zero), so that the wait for a
         // tile's data counts exactly the younger loads still in flight.
         // The staged K-step of this tile is already in LDS when the caller staged it one tile ahead
         // (stage_next on the previous tile); otherwise it is written now.
+        // Widths whose second K-step does not fit are prefetched only with one K-step (KM >= 2), and
+        // their code below never forms the second K-step's registers.
+        constexpr bool kTwo = k_second_load(B);
         if (!stage_next) {
             if (ks_t == 0) {
                 k_write_stage<B>(kb, stage, lane);
                 wave_lds_sync();
-            } else if (ks_t == 1 && nk > 1) {
-                k_write_stage<B>(kb + W0, stage, lane);
-                wave_lds_sync();
+            } else if constexpr (kTwo) {
+                if (ks_t == 1 && nk > 1) {
+                    k_write_stage<B>(kb + W0, stage, lane);
+                    wave_lds_sync();
+                }
             }
         }
 #pragma unroll
@@ -333,21 +359,25 @@ __device__ __forceinline__ void k_tile(uint32_t (&kb)[kKBufWords], uint32_t (&kb
 #pragma unroll
                 for (int lm = 0; lm < LM; ++lm) acc[lm] = mfma_i8(qa[0][lm], bk, v4i{0, 0, 0, 0});
             }
-            if (nk > 1) {
-                const v4i bk = ks_t == 1 ? k_frag_staged<B>(stage, xb + st * xs) : k_frag_direct<B>(kb + W0, st);
+            if constexpr (kTwo) {
+                if (nk > 1) {
+                    const v4i bk = ks_t == 1 ? k_frag_staged<B>(stage, xb + st * xs) : k_frag_direct<B>(kb + W0, st);
 #pragma unroll
-                for (int lm = 0; lm < LM; ++lm) acc[lm] = mfma_i8(qa[1][lm], bk, acc[lm]);
+                    for (int lm = 0; lm < LM; ++lm) acc[lm] = mfma_i8(qa[1][lm], bk, acc[lm]);
+                }
             }
             logit_of<LM>(acc, k0, k1, k2, off, s, st);
         }
         k_load_direct<B>(rs_n, rk, LK[0], kb);
-        k_load_direct<B>(rs_n, rk, LK[1], kb + W0);
+        if constexpr (kTwo) k_load_direct<B>(rs_n, rk, LK[1], kb + W0);
         // stage the next tile's K-step (loaded into the other register set one tile ago) now, away from
         // the loop head
         if (stage_next) {
             wave_lds_sync();
             if (ks_t == 0) k_write_stage<B>(kb_next, stage, lane);
-            else if (ks_t == 1 && nk > 1) k_write_stage<B>(kb_next + W0, stage, lane);
+            else if constexpr (kTwo) {
+                if (ks_t == 1 && nk > 1) k_write_stage<B>(kb_next + W0, stage, lane);
+            }
             wave_lds_sync();
         }
     } else {
@@ -382,84 +412,116 @@ __device__ __forceinline__ void k_tile(uint32_t (&kb)[kKBufWords], uint32_t (&kb
     }
 }
 
-// Value field words of N-tile nt for this lane (coordinate 16 nt + col, tokens 16 grp + ...).
+// Group Q of plane k for this lane: field index L = 4 col + grp of every N-tile in the group, the
+// lane's fields in N-tile order. Groups before the last hold g N-tiles (16 bytes per lane, lanes in
+// order); the last holds the remaining m N-tiles, the lanes of coordinates col >= ct (the coordinates
+// of a partial last N-tile) one field fewer, so lane L starts A = 4 max(0, col - ct) + [col >= ct] grp
+// fields before L m. Groups past the rank read beyond it (bounded by the stream) into accumulator
+// columns that are never output.
 template <int B>
-__device__ __forceinline__ void v_load(const __amdgpu_buffer_rsrc_t rs, int r, uint32_t lv, int nt, uint32_t* w) {
-    int o = 0;
-#pragma unroll
-    for (int k = 0; k < n_planes(B); ++k) {
-        const int P = plane_w(B, k);
-        const int voff = (int)(P * lv) + 8 * r * plane_off(B, k) + 128 * P * nt;
-        if (P == 1) {
-            w[o++] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(rs, voff, 0, 0);
-        } else if (P == 2) {
-            w[o++] = __builtin_amdgcn_raw_buffer_load_b32(rs, voff, 0, 0);
-        } else if (P == 4) {
-            const v2u v = __builtin_amdgcn_raw_buffer_load_b64(rs, voff, 0, 0);
-            w[o++] = v[0];
-            w[o++] = v[1];
-        } else {
-            const v4u v = __builtin_amdgcn_raw_buffer_load_b128(rs, voff, 0, 0);
-            w[o++] = v[0];
-            w[o++] = v[1];
-            w[o++] = v[2];
-            w[o++] = v[3];
-        }
-    }
+__device__ __forceinline__ v4u v_group_load(const __amdgpu_buffer_rsrc_t rs, int k, int Q, int r, uint32_t L,
+                                            uint32_t A) {
+    const int P = plane_w(B, k), g = v_group(P);
+    const int nvt = (r + 15) >> 4;
+    const int ql = (nvt - 1) / g, m = nvt - g * ql;
+    const uint32_t in = Q == ql ? (uint32_t)(2 * P) * (L * (uint32_t)m - A) : 16u * L;
+    const int voff = 8 * r * plane_off(B, k) + 1024 * Q + (int)in;
+    // A multiple of 4 bytes, except for 1-bit planes, whose last group (the only one, r <= 128) may start
+    // a lane's fields at 2 mod 4 bytes: the load takes the dword-aligned 16 bytes below (the lane's
+    // fields, at most 14 bytes in that case, stay inside them) and v_tile shifts them into place.
+    return __builtin_amdgcn_raw_buffer_load_b128(rs, voff & ~3, 0, 0);
 }
 
-template <int B>
-__device__ __forceinline__ v4i v_frag(const uint32_t* w) {
-    Fld f[3];
-    int o = 0;
+// A of the lane (col, grp) for rank r.
+__device__ __forceinline__ uint32_t v_lane_adj(int r, int col, int grp) {
+    const int ct = r - 16 * (((r + 15) >> 4) - 1);
+    return col >= ct ? (uint32_t)(4 * (col - ct) + grp) : 0u;
+}
+
+// Loads of the prefetched groups whose last N-tile (below NV) is nt, plane by plane: the prefetch of a
+// tile issues them for nt = 0, 1, .. in the same order as the processing of a tile refills them.
+template <int B, int NV>
+__device__ __forceinline__ void v_refill(uint32_t* vb, const __amdgpu_buffer_rsrc_t rs, int r, uint32_t L, uint32_t A,
+                                         int nt) {
+    constexpr int NPF = v_pf_tiles(B, NV);
 #pragma unroll
-    for (int k = 0; k < 3; ++k) {
-        if (k < n_planes(B)) {
-            const int P = plane_w(B, k);
-            if (P <= 2) f[k] = Fld{w[o], 0u, 0u, 0u};
-            else if (P == 4) f[k] = Fld{w[o], w[o + 1], 0u, 0u};
-            else f[k] = Fld{w[o], w[o + 1], w[o + 2], w[o + 3]};
-            o += P <= 2 ? 1 : P / 2;
-        } else {
-            f[k] = Fld{0u, 0u, 0u, 0u};
+    for (int k = 0; k < n_planes(B); ++k) {
+        const int g = v_group(plane_w(B, k)), Q = nt / g;
+        const int last = (Q + 1) * g < NV ? (Q + 1) * g - 1 : NV - 1;
+        if (Q < cdiv(NPF, g) && nt == last) {
+            const v4u v = v_group_load<B>(rs, k, Q, r, L, A);
+            uint32_t* w = vb + v_pf_base(B, k, NPF) + 4 * Q;
+            w[0] = v[0];
+            w[1] = v[1];
+            w[2] = v[2];
+            w[3] = v[3];
         }
     }
-    return unpack16<B>(f, false);
 }
 
 template <int B, int NV>
 __device__ __forceinline__ void v_prefetch(uint32_t (&vb)[kVBufWords], const __amdgpu_buffer_rsrc_t rs, int r,
-                                           uint32_t lv, int nv) {
-    constexpr int VW = v_words(B), NPF = v_prefetch_tiles(B) < NV ? v_prefetch_tiles(B) : NV;
-    (void)nv;
+                                           uint32_t L, uint32_t A) {
 #pragma unroll
-    for (int nt = 0; nt < NPF; ++nt) v_load<B>(rs, r, lv, nt, vb + nt * VW);
+    for (int nt = 0; nt < NV; ++nt) v_refill<B, NV>(vb, rs, r, L, A, nt);
 }
 
-// PV MFMAs of one tile (N-tiles nt < NV, a compile-time bound on the rank's N-tiles; the first
-// v_prefetch_tiles come from the prefetched words, the rest are loaded here), then the next tile's
+// PV MFMAs of one tile (N-tiles nt < NV, a compile-time bound on the rank's N-tiles; the prefetched
+// groups come from vb, the rest are loaded here as their first N-tile comes), then the next tile's
 // prefetch (rs_next; a zero-sized descriptor when there is none).
 template <int B, int LM, int NV>
 __device__ __forceinline__ void v_tile(uint32_t* vb, const __amdgpu_buffer_rsrc_t rs, const __amdgpu_buffer_rsrc_t rs_next,
-                                       int r, uint32_t lv, int nv, const v4i (&ap)[LM], v4i (&C)[LM][9]) {
-    constexpr int VW = v_words(B), NPF = v_prefetch_tiles(B) < NV ? v_prefetch_tiles(B) : NV;
-    // Every N-tile below NV is processed, also those past the rank (their loads read beyond the plane,
-    // bounded by the stream, into accumulator columns that are never output): no branches, and every
-    // tile issues the same loads in the same order, so the waits for a tile's data stay exact.
-    (void)nv;
+                                       int r, uint32_t L, uint32_t A, const v4i (&ap)[LM], v4i (&C)[LM][9]) {
+    constexpr int NPF = v_pf_tiles(B, NV);
+    // Every N-tile below NV is processed, also those past the rank: no branches, and every tile issues
+    // the same loads in the same order, so the waits for a tile's data stay exact.
+    uint32_t gw[3][4], w1[4];
 #pragma unroll
     for (int nt = 0; nt < NV; ++nt) {
-        uint32_t w[4];
-        if (nt < NPF) {
+        Fld f[3];
+        bool hi = false;
 #pragma unroll
-            for (int q = 0; q < VW; ++q) w[q] = vb[nt * VW + q];
-        } else {
-            v_load<B>(rs, r, lv, nt, w);
+        for (int k = 0; k < 3; ++k) {
+            if (k < n_planes(B)) {
+                const int P = plane_w(B, k), g = v_group(P), Q = nt / g, j = nt % g;
+                const bool pf = Q < cdiv(NPF, g);
+                if (!pf && j == 0) {
+                    const v4u v = v_group_load<B>(rs, k, Q, r, L, A);
+                    gw[k][0] = v[0];
+                    gw[k][1] = v[1];
+                    gw[k][2] = v[2];
+                    gw[k][3] = v[3];
+                }
+                const uint32_t* w = pf ? vb + v_pf_base(B, k, NPF) + 4 * Q : gw[k];
+                if (P == 1) {
+                    // one group of m = ceil(r / 16) N-tiles: the lane's fields start at bit 16 (m L - A)
+                    // mod 32 of the dword-aligned words; they are shifted down once, on the group's
+                    // first N-tile, where the words are used (a shift right after the load would wait
+                    // for it)
+                    if (j == 0) {
+                        const uint32_t sh = ((L * (uint32_t)((r + 15) >> 4) - A) & 1u) << 4;
+                        w1[0] = funnel(w[1], w[0], sh);
+                        w1[1] = funnel(w[2], w[1], sh);
+                        w1[2] = funnel(w[3], w[2], sh);
+                        w1[3] = w[3] >> sh;
+                    }
+                    f[k] = Fld{w1[j >> 1], 0u, 0u, 0u};
+                    hi = (j & 1) != 0;
+                } else if (P == 2) {
+                    f[k] = Fld{w[j], 0u, 0u, 0u};
+                } else if (P == 4) {
+                    f[k] = Fld{w[2 * j], w[2 * j + 1], 0u, 0u};
+                } else {
+                    f[k] = Fld{w[0], w[1], w[2], w[3]};
+                }
+            } else {
+                f[k] = Fld{0u, 0u, 0u, 0u};
+            }
         }
-        const v4i bv = v_frag<B>(w);
+        const v4i bv = unpack16<B>(f, hi);
 #pragma unroll
         for (int pm = 0; pm < LM; ++pm) C[pm][nt] = mfma_i8(ap[pm], bv, C[pm][nt]);
-        if (nt < NPF) v_load<B>(rs_next, r, lv, nt, vb + nt * VW);
+        v_refill<B, NV>(vb, rs_next, r, L, A, nt);
     }
 }
 
@@ -651,7 +713,7 @@ template <int G> struct Shape {
     }
 
 // One work item (unit u, context chunk [start, end)) with the K and V bit widths fixed at compile
-// time (BKc, BVc in 1..4), or switched per tile (0: the general path for widths above 4).
+// time (BKc in 1..8, BVc in 1..4), or switched per tile (0: the general path for values wider than 4).
 extern __shared__ __attribute__((aligned(16))) uint8_t kvc_dsm[];
 
 // K-step structure of a rank: 0: two K-steps, no tail group; 1: two K-steps, the tail group in the
@@ -713,7 +775,7 @@ __device__ __attribute__((always_inline)) void run_item(const DevSide& K, const 
         const int cg = 4 * ks + grp;
         LK[ks] = ks == ks_t ? (uint32_t)(512 * ks + 8 * lane) : (cg < g16 ? (uint32_t)(128 * cg + 8 * col) : kLaneOOB);
     }
-    const uint32_t LV = (uint32_t)(8 * col + 2 * grp);
+    const uint32_t LV = (uint32_t)(4 * col + grp), VA = v_lane_adj(rv, col, grp);
     uint32_t XB = 0, XS = 0;  // staged token fields start at plane-width units XB + st XS
     {
         const int nf = g16 - 4 * (ks_t < 2 ? ks_t : 0);  // full groups in the staged K-step
@@ -759,15 +821,15 @@ __device__ __attribute__((always_inline)) void run_item(const DevSide& K, const 
         // issued in the loop's own order (K-steps, then value N-tiles, per set), so that the waits at
         // the loop head count the same younger loads on entry as on the back edge
         const auto krs = k_rs(tile0), vrs = v_rs(tile0);
-        KVC_SW_K(k_prefetch<B_>(kbA, krs, rk, nk, ks_t, LK, lane));
+        KVC_SW_K((k_prefetch<B_, KM>(kbA, krs, rk, nk, ks_t, LK, lane)));
         __builtin_amdgcn_sched_barrier(0);
-        KVC_SW_V((v_prefetch<B_, NVc>(vbA, vrs, rv, LV, nv)));
+        KVC_SW_V((v_prefetch<B_, NVc>(vbA, vrs, rv, LV, VA)));
         __builtin_amdgcn_sched_barrier(0);
         if constexpr (kDepth == 2) {
             const auto krs1 = k_rs(tile0 + 1), vrs1 = v_rs(tile0 + 1);
-            KVC_SW_K(k_prefetch<B_>(kbB, krs1, rk, nk, ks_t, LK, lane));
+            KVC_SW_K((k_prefetch<B_, KM>(kbB, krs1, rk, nk, ks_t, LK, lane)));
             __builtin_amdgcn_sched_barrier(0);
-            KVC_SW_V((v_prefetch<B_, NVc>(vbB, vrs1, rv, LV, nv)));
+            KVC_SW_V((v_prefetch<B_, NVc>(vbB, vrs1, rv, LV, VA)));
             __builtin_amdgcn_sched_barrier(0);
         }
     }
@@ -781,13 +843,13 @@ __device__ __attribute__((always_inline)) void run_item(const DevSide& K, const 
         // Opaque per-tile copies of the lane and rank constants: the offsets every bit width derives
         // from them are recomputed inside the loop instead of being hoisted and kept live across it
         // for all eight widths at once.
-        uint32_t LKt[2] = {LK[0], LK[1]}, XBt = XB, XSt = XS, LVt = LV;
+        uint32_t LKt[2] = {LK[0], LK[1]}, XBt = XB, XSt = XS, LVt = LV, VAt = VA;
         int rkt = rk, rvt = rv;
         if constexpr (BKc == 0 || BVc == 0) {
-            asm volatile("" : "+v"(LKt[0]), "+v"(LKt[1]), "+v"(LVt), "+v"(XBt), "+v"(XSt));
+            asm volatile("" : "+v"(LKt[0]), "+v"(LKt[1]), "+v"(LVt), "+v"(VAt), "+v"(XBt), "+v"(XSt));
             asm volatile("" : "+s"(rkt), "+s"(rvt));
         }
-        const int nkt = nk, nvt = nv, kst = ks_t;
+        const int nkt = nk, kst = ks_t;
 
         // ---- logits, log2 domain, less the running max (the raw logits on the first tile)
         float s[LM][4];
@@ -890,7 +952,7 @@ __device__ __attribute__((always_inline)) void run_item(const DevSide& K, const 
             ap[pm] = *reinterpret_cast<const v4i*>(pmat + (16 * pm + col) * kPRowBytes + 16 * grp);
 
         // ---- PV (value N-tiles, then the all-ones column)
-        KVC_SW_V((v_tile<B_, LM, NVc>(vb, vrs, vrs_n, rvt, LVt, nvt, ap, C)));
+        KVC_SW_V((v_tile<B_, LM, NVc>(vb, vrs, vrs_n, rvt, LVt, VAt, ap, C)));
 #pragma unroll
         for (int pm = 0; pm < LM; ++pm) C[pm][8] = mfma_i8(ap[pm], ones, C[pm][8]);
         wave_lds_sync();  // pmat is rewritten by the next tile
@@ -899,10 +961,12 @@ __device__ __attribute__((always_inline)) void run_item(const DevSide& K, const 
         // pairs of tiles in a straight-line body (the load-wait counts stay exact across the back edge)
         // The staged (tail) K-step of tile t + 1 goes to LDS at the end of tile t's logits (the first
         // tile's before the loop); the general path stages each tile itself.
-        constexpr bool kAhead = KM >= 0;
+        constexpr bool kAhead = KM >= 0 && k_prefetch_on(BKc, KM);
         if constexpr (kAhead) {
             if (ks_t == 0) k_write_stage<BKc>(kbA, stage, lane);
-            else if (ks_t == 1) k_write_stage<BKc>(kbA + k_step_words(BKc), stage, lane);
+            else if constexpr (k_second_load(BKc)) {
+                if (ks_t == 1) k_write_stage<BKc>(kbA + k_step_words(BKc), stage, lane);
+            }
             wave_lds_sync();
         }
         int tile = tile0;
@@ -966,10 +1030,10 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(Shape<G>::W,
         return;
     }
     const int bk = K.b[u], bv = V.b[u];
-    // Compiled per (b_K, b_V, K-step structure) for the common widths and group sizes; the general
-    // path switches on the widths per tile.
+    // Compiled per (b_K, b_V, K-step structure) for value widths up to 4 and the common group sizes;
+    // the general path switches on the widths per tile.
     if constexpr (G == 4 || G == 8) {
-        if (bk <= 4 && bv <= 4) {
+        if (bv <= 4) {
             // 3-bit values at rank <= 96 (six N-tiles) have their own instantiations
             const int vm = bv == 3 && V.r[u] <= 96 ? 1 : 0;
             switch ((((bk - 1) * 4 + (bv - 1)) * 4 + k_mode(K.r[u])) * 2 + vm) {
@@ -983,6 +1047,10 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(Shape<G>::W,
                 KVC_ITEM4(2, 1) KVC_ITEM4(2, 2) KVC_ITEM4S(2) KVC_ITEM4(2, 4)
                 KVC_ITEM4(3, 1) KVC_ITEM4(3, 2) KVC_ITEM4S(3) KVC_ITEM4(3, 4)
                 KVC_ITEM4(4, 1) KVC_ITEM4(4, 2) KVC_ITEM4S(4) KVC_ITEM4(4, 4)
+                KVC_ITEM4(5, 1) KVC_ITEM4(5, 2) KVC_ITEM4S(5) KVC_ITEM4(5, 4)
+                KVC_ITEM4(6, 1) KVC_ITEM4(6, 2) KVC_ITEM4S(6) KVC_ITEM4(6, 4)
+                KVC_ITEM4(7, 1) KVC_ITEM4(7, 2) KVC_ITEM4S(7) KVC_ITEM4(7, 4)
+                KVC_ITEM4(8, 1) KVC_ITEM4(8, 2) KVC_ITEM4S(8) KVC_ITEM4(8, 4)
 #undef KVC_ITEM4S
 #undef KVC_ITEM4
 #undef KVC_ITEM
@@ -1244,10 +1312,10 @@ __global__ __launch_bounds__(64 * kRopeWaves) void decode_rope_kernel(
     uint32_t vb[kVBufWords];
 #pragma unroll
     for (int k = 0; k < kVBufWords; ++k) vb[k] = 0u;
-    const uint32_t LV = (uint32_t)(8 * col + 2 * grp);
+    const uint32_t LV = (uint32_t)(4 * col + grp), VA = v_lane_adj(rv, col, grp);
     {
         const auto vrs = v_rs(tile0);
-        KVC_SWITCH_B(bv, (v_prefetch<B_, 8>(vb, vrs, rv, LV, nv)));
+        KVC_SWITCH_B(bv, (v_prefetch<B_, 8>(vb, vrs, rv, LV, VA)));
     }
     k_fetch(tile0);
 
@@ -1261,9 +1329,9 @@ __global__ __launch_bounds__(64 * kRopeWaves) void decode_rope_kernel(
         // Opaque per-tile copies of the widths, ranks and lane offsets: the addresses every width's branch
         // derives from them are recomputed inside the loop, not hoisted and kept live for all widths.
         int rkt = rk, bkt = bk, rvt = rv, bvt = bv, nvt = nv, g16t = g16, rhot = rho, nkst = nks;
-        uint32_t LVt = LV;
+        uint32_t LVt = LV, VAt = VA;
         int colt = col, kqt = kq;
-        asm volatile("" : "+v"(LVt), "+v"(colt), "+v"(kqt));
+        asm volatile("" : "+v"(LVt), "+v"(VAt), "+v"(colt), "+v"(kqt));
         asm volatile("" : "+s"(rkt), "+s"(bkt), "+s"(rvt), "+s"(bvt), "+s"(nvt), "+s"(g16t), "+s"(rhot), "+s"(nkst));
         const uint8_t* ktile = KS;
         {
@@ -1430,7 +1498,7 @@ __global__ __launch_bounds__(64 * kRopeWaves) void decode_rope_kernel(
             ap[pm] = *reinterpret_cast<const v4i*>(pmat + (16 * pm + col) * kPRowBytes + 16 * grp);
         {
             const auto vrs = v_rs(tile), vrs_n = v_rs(tile + 1);
-            KVC_SWITCH_B(bvt, (v_tile<B_, LM, 8>(vb, vrs, vrs_n, rvt, LVt, nvt, ap, C)));
+            KVC_SWITCH_B(bvt, (v_tile<B_, LM, 8>(vb, vrs, vrs_n, rvt, LVt, VAt, ap, C)));
         }
 #pragma unroll
         for (int pm = 0; pm < LM; ++pm) C[pm][8] = mfma_i8(ap[pm], ones, C[pm][8]);

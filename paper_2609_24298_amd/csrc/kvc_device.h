@@ -33,10 +33,9 @@ __host__ __device__ constexpr int kidx_b(int b, int j) {
     return b == 8 ? j : (b == 4 ? 8 * (j >> 3) + 4 * (j & 1) + ((j & 7) >> 1) : 4 * (j & 3) + (j >> 2));
 }
 
-// Slot of (token t in tile, coordinate i). K: token-major inside groups of 16
-// coordinates (a token's 16 codes of a group are 16 consecutive slots), the
-// r % 16 tail group token-major after them. V: coordinate-major, each quarter
-// of 16 tokens in the order pos_b.
+// Slot of (token t in tile, coordinate i) on the K side: token-major inside groups of 16
+// coordinates (a token's 16 codes of a group are 16 consecutive slots), the r % 16 tail group
+// token-major after them; slot phi of a plane of width p holds bits [p phi, p phi + p).
 __device__ __forceinline__ int slot_k(int t, int i, int r) {
     const int g16 = r >> 4;
     if (i < 16 * g16) return ((i >> 4) << 10) + (t << 4) + (i & 15);
@@ -50,13 +49,29 @@ __device__ __forceinline__ void unslot_k(int phi, int r, int& t, int& i) {
     t = q / rho;
     i = 16 * g16 + (q - t * rho);
 }
-__device__ __forceinline__ int slot_v(int t, int i, int b) { return i * 64 + (t & 48) + pos_b(b, t & 15); }
-__device__ __forceinline__ void unslot_v(int phi, int b, int& t, int& i) {
-    i = phi >> 6;
-    t = (phi & 48) + kidx_b(b, phi & 15);
+// V fields: the 16 codes of coordinate 16 n + c (N-tile n, column c) for the tokens of quarter q of
+// the tile, token t at position pos_b(t % 16), p bits each: 2p bytes. In a plane of width p the
+// N-tiles form groups of g = 8 / p (g = 1 for p = 8), group Q at byte 1024 Q of the plane, and a
+// group stores its fields ordered by L = 4 c + q, then n (the fields of coordinates below r only):
+// a lane's fields of a whole group are 16 consecutive bytes. Byte offset of field (n, c, q) in the
+// plane: 2p (g L + j), j = n - g Q, in a group of g N-tiles; in the last group, of m N-tiles whose
+// last holds ct coordinates, 2p (m L - A + j) with A = 4 max(0, c - ct) + [c >= ct] q fields of
+// the coordinates c' >= ct (one field fewer each) ahead of L.
+__host__ __device__ constexpr int v_group_ntiles(int p) { return p == 8 ? 1 : 8 / p; }
+__host__ __device__ inline int v_field_off(int p, int r, int n, int c, int q) {
+    const int g = v_group_ntiles(p), nvt = (r + 15) >> 4;
+    const int Q = n / g, j = n - g * Q, ql = (nvt - 1) / g, L = 4 * c + q;
+    if (Q < ql) return 1024 * Q + 2 * p * (g * L + j);
+    const int m = nvt - g * ql, ct = r - 16 * (nvt - 1);
+    const int A = c >= ct ? 4 * (c - ct) + q : 0;
+    return 1024 * Q + 2 * p * (m * L - A + j);
+}
+// Bit of the code of (token t in tile, coordinate i) in the V plane of width p.
+__host__ __device__ inline int v_plane_bit(int t, int i, int r, int b, int p) {
+    return 8 * v_field_off(p, r, i >> 4, i & 15, t >> 4) + p * pos_b(b, t & 15);
 }
 
-// Code stored in slot phi of the tile starting at `tile`: the p bits of each plane
+// Code stored in K slot phi of the tile starting at `tile`: the p bits of each plane
 // (widest first) sit at bits [p phi, p phi + p) of the plane.
 __device__ __forceinline__ uint32_t load_code(const uint8_t* __restrict__ tile, int r, int b, int phi) {
     if (b == 8) return tile[phi];
@@ -67,6 +82,24 @@ __device__ __forceinline__ uint32_t load_code(const uint8_t* __restrict__ tile, 
     for (int p = 4; p >= 1; p >>= 1) {
         if (b & p) {
             const int bit = p * phi;
+            rem -= p;
+            c |= ((uint32_t)(tile[off + (bit >> 3)] >> (bit & 7)) & ((1u << p) - 1u)) << rem;
+            off += 8 * r * p;
+        }
+    }
+    return c;
+}
+
+// Code of (token t in tile, coordinate i) on the V side.
+__device__ __forceinline__ uint32_t load_code_v(const uint8_t* __restrict__ tile, int r, int b, int t, int i) {
+    if (b == 8) return tile[v_plane_bit(t, i, r, 8, 8) >> 3];
+    uint32_t c = 0;
+    int rem = b;
+    int off = 0;
+#pragma unroll
+    for (int p = 4; p >= 1; p >>= 1) {
+        if (b & p) {
+            const int bit = v_plane_bit(t, i, r, b, p);
             rem -= p;
             c |= ((uint32_t)(tile[off + (bit >> 3)] >> (bit & 7)) & ((1u << p) - 1u)) << rem;
             off += 8 * r * p;

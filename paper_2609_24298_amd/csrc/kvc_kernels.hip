@@ -120,6 +120,39 @@ __device__ __forceinline__ void pack_plane(const uint8_t* __restrict__ sb, uint8
     }
 }
 
+// One plane of the V field of this lane (see v_field_off): its 16 codes, in position order, as four
+// dwords of four bytes -> 2p bytes at the field's offset.
+template <int B, int K>
+__device__ __forceinline__ void pack_vfield_plane(const uint32_t (&src)[4], uint8_t* __restrict__ tbase, int r, int n,
+                                                  int c, int q) {
+    if constexpr (K < n_planes(B)) {
+        constexpr int P = plane_w(B, K), SH = plane_sh(B, K);
+        constexpr uint32_t PM = (P == 8 ? 0xffu : ((1u << P) - 1u)) * 0x01010101u;
+        uint8_t* __restrict__ dst = tbase + 8 * r * plane_off(B, K) + v_field_off(P, r, n, c, q);
+        uint32_t w[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int m = 0; m < 4; ++m) w[(4 * P * m) >> 5] |= compact4<P>((src[m] >> SH) & PM) << ((4 * P * m) & 31);
+        if constexpr (P == 1) *reinterpret_cast<uint16_t*>(dst) = (uint16_t)w[0];
+        else if constexpr (P == 2) *reinterpret_cast<uint32_t*>(dst) = w[0];
+        else if constexpr (P == 4) *reinterpret_cast<uint2*>(dst) = uint2{w[0], w[1]};
+        else *reinterpret_cast<uint4*>(dst) = uint4{w[0], w[1], w[2], w[3]};
+    }
+}
+
+// Packs the V fields of N-tile n (its codes in sb: coordinate row c at kVRow c, quarter q at 16 q,
+// in position order) into every plane: lane 4 c + q writes field (n, c, q).
+template <int B>
+__device__ __forceinline__ void pack_vfields(const uint8_t* __restrict__ sb, uint8_t* __restrict__ tbase, int r, int n,
+                                             int lane) {
+    const int c = lane >> 2, q = lane & 3;
+    if (16 * n + c >= r) return;
+    const uint4 a = *reinterpret_cast<const uint4*>(sb + kVRow * c + 16 * q);
+    const uint32_t src[4] = {a.x, a.y, a.z, a.w};
+    pack_vfield_plane<B, 0>(src, tbase, r, n, c, q);
+    pack_vfield_plane<B, 1>(src, tbase, r, n, c, q);
+    pack_vfield_plane<B, 2>(src, tbase, r, n, c, q);
+}
+
 template <int side, int B>
 __device__ __forceinline__ void pack_group(const uint8_t* __restrict__ sb, uint8_t* __restrict__ tbase, int r, int sl0,
                                            int n_sl, int lane) {
@@ -325,10 +358,35 @@ __global__ __launch_bounds__(kEncMmaThreads) __attribute__((amdgpu_waves_per_eu(
                 }
             }
             __builtin_amdgcn_wave_barrier();
-            // pack the group's slots [1024 mc, 1024 mc + n_sl) into every plane
-            const int n_sl = (rho && mc == n_mc - 1) ? 64 * rho : 1024;  // K tail group / V last coordinate rows
+            // pack the group's slots [1024 mc, 1024 mc + n_sl) (K) or fields of N-tile mc (V) into every plane
+            const int n_sl = (rho && mc == n_mc - 1) ? 64 * rho : 1024;  // K tail group
             const int sl0 = 1024 * mc;
-            if (full) {
+            if constexpr (side == KVC_SIDE_V) {
+                if (full) {
+                    KVC_SWITCH_B(b, (pack_vfields<B_>(sb, tbase, r, mc, lane)));
+                } else {
+                    // partial tile: rewrite only the codes of tokens in [lo, hi), byte by byte (a code
+                    // never straddles a byte); lane 4 c + q owns field (mc, c, q)
+                    const int c = lane >> 2, q = lane & 3;
+                    if (16 * mc + c < r) {
+                        for (int p = 8, off = 0; p >= 1; p >>= 1) {
+                            if (b == 8 ? p != 8 : (p == 8 || !(b & p))) continue;
+                            const int sh = b == 8 ? 0 : (b & (p - 1));
+                            const uint32_t vm = p == 8 ? 0xffu : ((1u << p) - 1u);
+                            uint8_t* __restrict__ dst = tbase + 8 * r * off + v_field_off(p, r, mc, c, q);
+                            for (int m = 0; m < 16; ++m) {
+                                const int tk = tok0 + 16 * q + kidx_b(b, m);
+                                if (tk >= lo && tk < hi) {
+                                    const uint32_t v = ((uint32_t)sb[kVRow * c + 16 * q + m] >> sh) & vm;
+                                    const int bit = p * m;
+                                    dst[bit >> 3] = (uint8_t)((dst[bit >> 3] & ~(vm << (bit & 7))) | (v << (bit & 7)));
+                                }
+                            }
+                            off += p;
+                        }
+                    }
+                }
+            } else if (full) {
                 KVC_SWITCH_B(b, (pack_group<side, B_>(sb, tbase, r, sl0, n_sl, lane)));
             } else {
                 // partial tile: rewrite only the slots of tokens in [lo, hi)
@@ -343,8 +401,7 @@ __global__ __launch_bounds__(kEncMmaThreads) __attribute__((amdgpu_waves_per_eu(
                         for (int io = 0; io < ppw; ++io) {
                             const int ph = sl0 + wi * ppw + io;
                             int t2, i2;
-                            if constexpr (side == KVC_SIDE_K) unslot_k(ph, r, t2, i2);
-                            else unslot_v(ph, b, t2, i2);
+                            unslot_k(ph, r, t2, i2);
                             const int tk = tok0 + t2;
                             if (tk >= lo && tk < hi) {
                                 const int bit = p * io;
@@ -402,8 +459,8 @@ __global__ __launch_bounds__(kRecThreads) void reconstruct_kernel(DevSide s, int
         if (tok < t0 + n_tok) {
             const uint8_t* tile = stream + (int64_t)(tok / kTile) * 8 * r * b;
             const int tl = tok % kTile;
-            const int phi = side == KVC_SIDE_K ? slot_k(tl, i, r) : slot_v(tl, i, b);
-            z = ((float)load_code(tile, r, b, phi) - half) * step;
+            const uint32_t code = side == KVC_SIDE_K ? load_code(tile, r, b, slot_k(tl, i, r)) : load_code_v(tile, r, b, tl, i);
+            z = ((float)code - half) * step;
         }
         zh[tt * zs + i] = z;
     }

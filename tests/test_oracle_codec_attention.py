@@ -130,6 +130,76 @@ def test_layout_hand_derived_bit_positions():
     assert s.size == 48 and s[0] == 0b11 and np.count_nonzero(s) == 1
 
 
+def test_layout_v_groups_hand_derived():
+    # V side, r = 40: N-tiles 0, 1 full and 2 holding coordinates 32..39 (ct = 8). For p = 1 and 2 the
+    # three N-tiles are one group (g = 8 and 4), stored by L = 4 c + q, then N-tile; columns c < 8
+    # have three fields, columns 8..15 two.
+    # b = 2, coordinate 17 (n = 1, c = 1), token 0 (q = 0, position 0): L = 4; 4 lanes x 3 fields
+    # before it, then n = 0 -> field 13 -> byte 4 * 13 = 52, bits 0..1
+    c = np.zeros((64, 40), dtype=np.uint8)
+    c[0, 17] = 3
+    s = onat.pack(c, 40, 2, ol.SIDE_V)
+    assert s.size == 8 * 40 * 2 and list(np.nonzero(s)[0]) == [52] and s[52] == 3
+    # b = 2, coordinate 9 (n = 0, c = 9), token 16 (q = 1, position 0): L = 37. Before it: L < 32 (c < 8)
+    # 32 x 3 = 96 fields, L = 32..35 (c = 8) 4 x 2, L = 36 (c = 9, q = 0) 2 -> field 106 -> byte 424
+    c[:] = 0
+    c[16, 9] = 2
+    s = onat.pack(c, 40, 2, ol.SIDE_V)
+    assert list(np.nonzero(s)[0]) == [424] and s[424] == 2
+    # b = 1, the same code position: 2-byte fields -> byte 212
+    c[:] = 0
+    c[16, 9] = 1
+    s = onat.pack(c, 40, 1, ol.SIDE_V)
+    assert s.size == 8 * 40 and list(np.nonzero(s)[0]) == [212] and s[212] == 1
+    # b = 3 = planes (2, 1) at r = 40: the 2-bit plane (640 bytes) then the 1-bit plane; coordinate 33
+    # (n = 2, c = 1), token 5 (q = 0, position 4 * 1 + 1 = 5): L = 4, field 4 * 3 + 2 = 14 ->
+    # 2-bit plane byte 56 + 10 // 8 = 57, bits 2..3; 1-bit plane byte 640 + 28 + 5 // 8 = 668, bit 5
+    c[:] = 0
+    c[5, 33] = 0b111
+    s = onat.pack(c, 40, 3, ol.SIDE_V)
+    assert list(np.nonzero(s)[0]) == [57, 668] and s[57] == 0b1100 and s[668] == 1 << 5
+    # r = 128, b = 2: groups of four N-tiles, 1024 bytes each. Coordinate 80 (n = 5, c = 0) token 0:
+    # group 1, L = 0, j = 1 -> byte 1024 + 4 = 1028
+    c128 = np.zeros((64, 128), dtype=np.uint8)
+    c128[0, 80] = 1
+    s = onat.pack(c128, 128, 2, ol.SIDE_V)
+    assert list(np.nonzero(s)[0]) == [1028] and s[1028] == 1
+    # r = 100, b = 2: N-tiles 4..6 form the last group (m = 3, ct = 4). Coordinate 99 (n = 6, c = 3),
+    # token 63 (q = 3, position 4 * 3 + 3 = 15): L = 15, field 15 * 3 + 2 = 47 ->
+    # byte 1024 + 4 * 47 + 30 // 8 = 1215, bits 6..7
+    c100 = np.zeros((64, 100), dtype=np.uint8)
+    c100[63, 99] = 2
+    s = onat.pack(c100, 100, 2, ol.SIDE_V)
+    assert list(np.nonzero(s)[0]) == [1215] and s[1215] == 2 << 6
+    # r = 100, b = 4 (g = 2): N-tile 6 alone in the last group (m = 1, ct = 4); coordinate 97
+    # (n = 6, c = 1), token 20 (q = 1, item 4: position 8 * 0 + 2 * 0 + 1 = 1): L = 5, field 5 ->
+    # byte 3 * 1024 + 8 * 5 = 3112, bits 4..7
+    c100[:] = 0
+    c100[20, 97] = 0x9
+    s = onat.pack(c100, 100, 4, ol.SIDE_V)
+    assert list(np.nonzero(s)[0]) == [3112] and s[3112] == 0x90
+    # r = 24, b = 8 (g = 1): coordinate-major fields; coordinate 20 (n = 1, c = 4), token 50 (q = 3,
+    # position 2): field 64 + 4 * 4 + 3 = 83 -> byte 16 * 83 + 2 = 1330
+    c24 = np.zeros((64, 24), dtype=np.uint8)
+    c24[50, 20] = 77
+    s = onat.pack(c24, 24, 8, ol.SIDE_V)
+    assert list(np.nonzero(s)[0]) == [1330] and s[1330] == 77
+
+
+@pytest.mark.parametrize("r", [2, 16, 18, 40, 64, 84, 100, 126, 128])
+@pytest.mark.parametrize("b", [1, 2, 3, 4, 5, 7, 8])
+def test_layout_v_fields_tile_the_plane(r, b):
+    # every V code of a tile has its own bits and together they fill every plane exactly
+    for p in ol.plane_widths(b):
+        tab = ol.v_field_bytes(r, p)
+        seen = np.zeros(8 * r * p * 8, dtype=np.int32)
+        for t in range(64):
+            for i in range(r):
+                bit = ol.plane_bit(ol.SIDE_V, t, i, r, b, p, tab)
+                seen[bit:bit + p] += 1
+        assert seen.min() == 1 and seen.max() == 1
+
+
 @pytest.mark.parametrize("b", range(1, 9))
 def test_v_token_order_is_a_permutation_of_each_quarter(b):
     pos = [ol.pos_b(b, m) for m in range(16)]
