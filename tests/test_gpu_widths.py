@@ -8,6 +8,11 @@ orthonormal rows rounded to fp16, steps scaled to each width. 512 units of 4133 
 multi-tile context chunks with a ragged last tile. One cache is decoded with every query-group size
 G in {1, 2, 4, 8, 16} (the streams do not depend on G) and checked unit by unit against the oracle's
 fp64 decode from its own codes; reconstruction of a token range is checked for every unit.
+
+Queries of scale 1.5 against these keys give logits of about 1 nat standard deviation (at full key
+rank): nearly flat attention, whose output (about the mean value) hardly moves when some value
+fields are read from the wrong place. Every other unit therefore gets queries of scale 6 (about 4
+nats): a few tokens then take most of the attention and their value fields show in the output.
 """
 import sys
 
@@ -87,7 +92,8 @@ def test_decode_every_width_pair(width_cache, G):
     rows, K, V, Pk, dk, Pv, dv, codes = width_cache
     U = len(rows)
     rng = np.random.default_rng(100 + G)
-    q = (rng.standard_normal((U, G, 128)) * 1.5).astype(np.float16)
+    scale = np.where(np.arange(U) % 2 == 0, 1.5, 6.0)[:, None, None]
+    q = (rng.standard_normal((U, G, 128)) * scale).astype(np.float16)
     qt = torch.as_tensor(q.view(np.int16), device="cuda").view(torch.float16)
     # lengths: most units attend over everything, some over ragged prefixes
     seq = np.full(U, T, dtype=np.int32)
