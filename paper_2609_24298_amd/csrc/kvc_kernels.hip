@@ -139,18 +139,67 @@ __device__ __forceinline__ void pack_vfield_plane(const uint32_t (&src)[4], uint
     }
 }
 
+// The wavefront's LDS accesses execute in program order: between a write and a read of the same
+// bytes by other lanes only the compiler's reordering has to be stopped.
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+}
+
+// Value fields of a plane narrower than 8 bits are gathered per group in LDS (kVGroupBytes per plane
+// and wavefront) and the finished group goes out as whole 16-byte rows of the plane, instead of one
+// scattered 2p-byte store per field.
+constexpr int kVGroupBytes = 1024;
+constexpr int kVStageBytes = 3 * kVGroupBytes;
+
+template <int B, int K>
+__device__ __forceinline__ void pack_vfield_staged(const uint32_t (&src)[4], bool has, uint8_t* __restrict__ vst,
+                                                   uint8_t* __restrict__ tbase, int r, int n, int n_last, int c, int q,
+                                                   int lane) {
+    if constexpr (K < n_planes(B)) {
+        constexpr int P = plane_w(B, K), SH = plane_sh(B, K), G = v_group_ntiles(P);
+        if constexpr (P == 8) {
+            if (has) pack_vfield_plane<B, K>(src, tbase, r, n, c, q);
+        } else {
+            constexpr uint32_t PM = ((1u << P) - 1u) * 0x01010101u;
+            const int Q = n / G;
+            uint8_t* __restrict__ gst = vst + K * kVGroupBytes;
+            if (has) {
+                uint32_t w[2] = {0u, 0u};
+#pragma unroll
+                for (int m = 0; m < 4; ++m) w[(4 * P * m) >> 5] |= compact4<P>((src[m] >> SH) & PM) << ((4 * P * m) & 31);
+                uint8_t* dst = gst + (v_field_off(P, r, n, c, q) - 1024 * Q);
+                if constexpr (P == 1) *reinterpret_cast<uint16_t*>(dst) = (uint16_t)w[0];
+                else if constexpr (P == 2) *reinterpret_cast<uint32_t*>(dst) = w[0];
+                else *reinterpret_cast<uint2*>(dst) = uint2{w[0], w[1]};
+            }
+            if (n - G * Q == G - 1 || n == n_last) {  // the group is complete: 8 p bytes per coordinate
+                const int gbytes = 8 * P * min(16 * G, r - 16 * G * Q);  // a multiple of 16 (r even)
+                wave_lds_sync();
+                uint8_t* __restrict__ pbase = tbase + 8 * r * plane_off(B, K) + 1024 * Q;
+                if (16 * lane < gbytes)
+                    *reinterpret_cast<uint4*>(pbase + 16 * lane) = *reinterpret_cast<const uint4*>(gst + 16 * lane);
+                wave_lds_sync();
+            }
+        }
+    }
+}
+
 // Packs the V fields of N-tile n (its codes in sb: coordinate row c at kVRow c, quarter q at 16 q,
-// in position order) into every plane: lane 4 c + q writes field (n, c, q).
+// in position order) into every plane: lane 4 c + q owns field (n, c, q).
 template <int B>
-__device__ __forceinline__ void pack_vfields(const uint8_t* __restrict__ sb, uint8_t* __restrict__ tbase, int r, int n,
-                                             int lane) {
+__device__ __forceinline__ void pack_vfields(const uint8_t* __restrict__ sb, uint8_t* __restrict__ vst,
+                                             uint8_t* __restrict__ tbase, int r, int n, int n_last, int lane) {
     const int c = lane >> 2, q = lane & 3;
-    if (16 * n + c >= r) return;
-    const uint4 a = *reinterpret_cast<const uint4*>(sb + kVRow * c + 16 * q);
-    const uint32_t src[4] = {a.x, a.y, a.z, a.w};
-    pack_vfield_plane<B, 0>(src, tbase, r, n, c, q);
-    pack_vfield_plane<B, 1>(src, tbase, r, n, c, q);
-    pack_vfield_plane<B, 2>(src, tbase, r, n, c, q);
+    const bool has = 16 * n + c < r;
+    uint32_t src[4] = {0u, 0u, 0u, 0u};
+    if (has) {
+        const uint4 a = *reinterpret_cast<const uint4*>(sb + kVRow * c + 16 * q);
+        src[0] = a.x; src[1] = a.y; src[2] = a.z; src[3] = a.w;
+    }
+    pack_vfield_staged<B, 0>(src, has, vst, tbase, r, n, n_last, c, q, lane);
+    pack_vfield_staged<B, 1>(src, has, vst, tbase, r, n, n_last, c, q, lane);
+    pack_vfield_staged<B, 2>(src, has, vst, tbase, r, n, n_last, c, q, lane);
 }
 
 template <int side, int B>
@@ -195,6 +244,8 @@ __global__ __launch_bounds__(kEncMmaThreads) __attribute__((amdgpu_waves_per_eu(
 
     const int wv = tid >> 6, lane = tid & 63, col = lane & 15, grp = lane >> 4;
     uint8_t* __restrict__ sb = slots + wv * kSlotBufBytes;
+    // [4 waves][kVStageBytes] value groups being gathered (value side only)
+    uint8_t* __restrict__ vst = slots + (kEncMmaThreads / 64) * kSlotBufBytes + wv * kVStageBytes;
     float* __restrict__ etok = etoks + wv * kTile;
     const int h = 1 << (b - 1);
     const float fh = (float)h, fmax_code = (float)(2 * h - 1), inv = 1.f / step;
@@ -363,7 +414,7 @@ __global__ __launch_bounds__(kEncMmaThreads) __attribute__((amdgpu_waves_per_eu(
             const int sl0 = 1024 * mc;
             if constexpr (side == KVC_SIDE_V) {
                 if (full) {
-                    KVC_SWITCH_B(b, (pack_vfields<B_>(sb, tbase, r, mc, lane)));
+                    KVC_SWITCH_B(b, (pack_vfields<B_>(sb, vst, tbase, r, mc, n_mc - 1, lane)));
                 } else {
                     // partial tile: rewrite only the codes of tokens in [lo, hi), byte by byte (a code
                     // never straddles a byte); lane 4 c + q owns field (mc, c, q)
@@ -512,7 +563,8 @@ extern "C" int kvc_encode(const kvc_stream_desc* s, const uint16_t* x, int64_t x
     }
     const int tile_first = t0 / kTile;
     const int n_tiles = (t0 + n_tok - 1) / kTile - tile_first + 1;
-    const size_t smem = (size_t)kD * kPRow * 2 + 2 * kD * 4 + (kEncMmaThreads / 64) * (kTile * 4 + kSlotBufBytes);
+    const size_t smem = (size_t)kD * kPRow * 2 + 2 * kD * 4 + (kEncMmaThreads / 64) * (kTile * 4 + kSlotBufBytes) +
+                        (s->side == KVC_SIDE_V ? (kEncMmaThreads / 64) * kVStageBytes : 0);
     dim3 grid((n_tiles + kEncMmaTilesPerBlock - 1) / kEncMmaTilesPerBlock, s->n_units);
     if (s->side == KVC_SIDE_K)
         hipLaunchKernelGGL(encode_mfma_kernel<KVC_SIDE_K>, grid, dim3(kEncMmaThreads), smem, (hipStream_t)stream,
