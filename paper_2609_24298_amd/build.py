@@ -38,12 +38,19 @@ def build(verbose: bool = True) -> str:
     _run(["g++", "-std=c++17", "-O2", "-fPIC", "-ffp-contract=off", "-fno-fast-math", "-Wall",
           "-I", INCLUDE, "-c", os.path.join(CSRC, "kvc_host.cpp"), "-o", host_o])
     objs = [host_o]
-    for src in ("kvc_kernels.hip", "kvc_decode.hip", "kvc_calib.hip"):
+    # the HIP sources compile in parallel (the two decode partials units take most of the time)
+    procs = []
+    for src in ("kvc_decode_g4.hip", "kvc_decode_g8.hip", "kvc_decode.hip", "kvc_kernels.hip", "kvc_calib.hip"):
         o = os.path.join(BUILD, src.replace(".hip", ".o"))
-        _run([hipcc, "-std=c++17", "-O3", "-fPIC", f"--offload-arch={ARCH}", "-ffp-contract=fast",
-              "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-              "-I", INCLUDE, "-I", CSRC, "-c", os.path.join(CSRC, src), "-o", o])
+        cmd = [hipcc, "-std=c++17", "-O3", "-fPIC", f"--offload-arch={ARCH}", "-ffp-contract=fast",
+               "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+               "-I", INCLUDE, "-I", CSRC, "-c", os.path.join(CSRC, src), "-o", o]
+        print("+", " ".join(cmd), flush=True)
+        procs.append((cmd, subprocess.Popen(cmd)))
         objs.append(o)
+    failed = [cmd for cmd, p in procs if p.wait() != 0]
+    if failed:
+        raise subprocess.CalledProcessError(1, failed[0])
     tmp = LIB + ".tmp%d" % os.getpid()
     _run([hipcc, "-shared", f"--offload-arch={ARCH}", "-o", tmp] + objs)
     os.replace(tmp, LIB)

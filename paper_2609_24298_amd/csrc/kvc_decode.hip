@@ -679,6 +679,7 @@ constexpr int kStepPrepThreads = 128;
 static_assert(kStepPrepThreads == kAppThreads, "the append uses one thread per coordinate");
 // Three wavefronts per SIMD (166 registers, none spilled): 1.5 times the resident blocks of the
 // unconstrained allocation, so the 3 x units blocks run in fewer rounds.
+#ifndef KVC_DECODE_PARTIALS_UNIT
 __global__ __launch_bounds__(kStepPrepThreads) __attribute__((amdgpu_waves_per_eu(3, 3))) void step_prep_kernel(
     DevSide K, DevSide V, const uint16_t* __restrict__ q, int G, int LM, v4i* __restrict__ qa, float4* __restrict__ qk,
     const uint16_t* __restrict__ xk, int64_t xk_stride, const uint16_t* __restrict__ xv, int64_t xv_stride, int t_new) {
@@ -686,6 +687,7 @@ __global__ __launch_bounds__(kStepPrepThreads) __attribute__((amdgpu_waves_per_e
     else if (blockIdx.y == 1) append_unit(K, KVC_SIDE_K, xk, xk_stride, t_new, 1, blockIdx.x);
     else append_unit(V, KVC_SIDE_V, xv, xv_stride, t_new, 1, blockIdx.x);
 }
+#endif
 
 // ---------------------------------------------------------------- partials
 
@@ -1034,23 +1036,29 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(Shape<G>::W,
     // the general path switches on the widths per tile.
     if constexpr (G == 4 || G == 8) {
         if (bv <= 4) {
-            // 3-bit values at rank <= 96 (six N-tiles) have their own instantiations
-            const int vm = bv == 3 && V.r[u] <= 96 ? 1 : 0;
-            switch ((((bk - 1) * 4 + (bv - 1)) * 4 + k_mode(K.r[u])) * 2 + vm) {
+            // Value ranks <= 64 (four N-tiles) at 1-3 bits with keys up to 4 bits, and 3-bit values at
+            // rank <= 96 (six N-tiles), have instantiations of their own.
+            const int rv = V.r[u];
+            const int nvc = rv <= 64 && bk <= 4 && bv <= 3 ? 2 : (bv == 3 && rv <= 96 ? 1 : 0);
+            switch ((((bk - 1) * 4 + (bv - 1)) * 4 + k_mode(K.r[u])) * 3 + nvc) {
 #define KVC_ITEM(BK, BV, KM, NV)                                                                                  \
-    case (((BK - 1) * 4 + (BV - 1)) * 4 + KM) * 2 + (NV == 6):                                                  \
+    case (((BK - 1) * 4 + (BV - 1)) * 4 + KM) * 3 + (NV == 6 ? 1 : (NV == 4 ? 2 : 0)):                          \
         run_item<G, BK, BV, KM, NV>(K, V, qa_ws, qk_ws, k_cap_tiles, v_cap_tiles, u, start, end, out, lane);    \
         return;
 #define KVC_ITEM4(BK, BV) KVC_ITEM(BK, BV, 0, 8) KVC_ITEM(BK, BV, 1, 8) KVC_ITEM(BK, BV, 2, 8) KVC_ITEM(BK, BV, 3, 8)
-#define KVC_ITEM4S(BK) KVC_ITEM4(BK, 3) KVC_ITEM(BK, 3, 0, 6) KVC_ITEM(BK, 3, 1, 6) KVC_ITEM(BK, 3, 2, 6) KVC_ITEM(BK, 3, 3, 6)
-                KVC_ITEM4(1, 1) KVC_ITEM4(1, 2) KVC_ITEM4S(1) KVC_ITEM4(1, 4)
-                KVC_ITEM4(2, 1) KVC_ITEM4(2, 2) KVC_ITEM4S(2) KVC_ITEM4(2, 4)
-                KVC_ITEM4(3, 1) KVC_ITEM4(3, 2) KVC_ITEM4S(3) KVC_ITEM4(3, 4)
-                KVC_ITEM4(4, 1) KVC_ITEM4(4, 2) KVC_ITEM4S(4) KVC_ITEM4(4, 4)
+#define KVC_ITEM4N(BK, BV, NV) KVC_ITEM(BK, BV, 0, NV) KVC_ITEM(BK, BV, 1, NV) KVC_ITEM(BK, BV, 2, NV) KVC_ITEM(BK, BV, 3, NV)
+#define KVC_ITEM4S(BK) KVC_ITEM4(BK, 3) KVC_ITEM4N(BK, 3, 6)
+#define KVC_ITEMN4(BK) KVC_ITEM4N(BK, 1, 4) KVC_ITEM4N(BK, 2, 4) KVC_ITEM4N(BK, 3, 4)
+                KVC_ITEM4(1, 1) KVC_ITEM4(1, 2) KVC_ITEM4S(1) KVC_ITEM4(1, 4) KVC_ITEMN4(1)
+                KVC_ITEM4(2, 1) KVC_ITEM4(2, 2) KVC_ITEM4S(2) KVC_ITEM4(2, 4) KVC_ITEMN4(2)
+                KVC_ITEM4(3, 1) KVC_ITEM4(3, 2) KVC_ITEM4S(3) KVC_ITEM4(3, 4) KVC_ITEMN4(3)
+                KVC_ITEM4(4, 1) KVC_ITEM4(4, 2) KVC_ITEM4S(4) KVC_ITEM4(4, 4) KVC_ITEMN4(4)
                 KVC_ITEM4(5, 1) KVC_ITEM4(5, 2) KVC_ITEM4S(5) KVC_ITEM4(5, 4)
                 KVC_ITEM4(6, 1) KVC_ITEM4(6, 2) KVC_ITEM4S(6) KVC_ITEM4(6, 4)
                 KVC_ITEM4(7, 1) KVC_ITEM4(7, 2) KVC_ITEM4S(7) KVC_ITEM4(7, 4)
                 KVC_ITEM4(8, 1) KVC_ITEM4(8, 2) KVC_ITEM4S(8) KVC_ITEM4(8, 4)
+#undef KVC_ITEMN4
+#undef KVC_ITEM4N
 #undef KVC_ITEM4S
 #undef KVC_ITEM4
 #undef KVC_ITEM
@@ -1060,6 +1068,15 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(Shape<G>::W,
     }
     run_item<G, 0, 0, -1, 8>(K, V, qa_ws, qk_ws, k_cap_tiles, v_cap_tiles, u, start, end, out, lane);
 }
+
+// The instantiations for 4 and 8 query heads per KV head are compiled in translation units of their
+// own (kvc_decode_g4.hip, kvc_decode_g8.hip), in parallel with this one.
+#ifndef KVC_DECODE_PARTIALS_UNIT
+extern template __global__ void decode_partial_kernel<4>(DevSide, DevSide, const v4i*, const float4*, const int32_t*, int,
+                                                         int, int, int, int, float*);
+extern template __global__ void decode_partial_kernel<8>(DevSide, DevSide, const v4i*, const float4*, const int32_t*, int,
+                                                         int, int, int, int, float*);
+#endif
 
 // ---------------------------------------------------------------- RoPE-aware partials
 
@@ -1697,6 +1714,7 @@ void launch_combine(int cw, dim3 grid, dim3 blk, size_t smem, hipStream_t st, co
     hipLaunchKernelGGL((combine_kernel<G, 1>), grid, dim3(64), (size_t)G * kPartStride * 4, st, V, n_chunks, part, out);
 }
 
+#ifndef KVC_DECODE_PARTIALS_UNIT
 // ---------------------------------------------------------------- read probe
 
 // Streaming read of n16 16-byte words (non-temporal loads, grid-stride). The words fold into one
@@ -2071,3 +2089,6 @@ extern "C" int kvc_read_probe(const void* buf, size_t bytes, uint32_t* sink, voi
                        reinterpret_cast<const v4u*>(buf), n16, sink);
     return check_launch("kvc_read_probe");
 }
+#else
+}  // namespace kvc
+#endif  // KVC_DECODE_PARTIALS_UNIT
