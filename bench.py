@@ -52,7 +52,8 @@ def decode_alg_bytes(cache, n_tok: int) -> int:
 
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
-    for f in ("kvc_kernels.hip", "kvc_decode.hip", "kvc_device.h", "kvc_append.h"):
+    for f in ("kvc_kernels.hip", "kvc_decode.hip", "kvc_decode_g4.hip", "kvc_decode_g8.hip", "kvc_device.h",
+              "kvc_append.h"):
         with open(os.path.join(ROOT, "paper_2609_24298_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
