@@ -446,8 +446,11 @@ def main():
     log(f"{args.steps} steps: {ms_step:.3f} ms/step fused (kvc_decode_step), {ms_two:.3f} ms as two calls")
 
     # decode call alone, events on the launch stream, for the roofline entry: back to back, and with the
-    # 256 MB MALL flushed (a 512 MB write) before each call, outside the events; the roofline takes the
-    # mean of the flushed calls
+    # 256 MB MALL flushed before each call, outside the events; the roofline takes the mean of the
+    # flushed calls. The flush reads a 512 MB buffer (a reduction), then the device idles: the MALL then
+    # holds other, clean lines, so the call reads its codes from HBM. A flush by writing the buffer leaves
+    # the MALL full of dirty lines whose write-back overlaps the next call and takes HBM time from it
+    # (about 55 us per call on the 8B-shaped 32k workload); that variant is reported as well.
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
     for a, b in evs:
         a.record()
@@ -456,25 +459,29 @@ def main():
     torch.cuda.synchronize()
     t_b2b = float(np.mean([a.elapsed_time(b) for a, b in evs])) / 1e3
     flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
-    for i, (a, b) in enumerate(evs):
-        flush.fill_(i & 0xFF)
-        a.record()
-        cache.decode(q, seq, n_att, out, ws)
-        b.record()
-    torch.cuda.synchronize()
-    t_dec = float(np.mean([a.elapsed_time(b) for a, b in evs])) / 1e3
+    flush.fill_(1)
+    flush_words = flush.view(torch.int32)
+
+    def flushed(call, write=False):
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+        for i, (a, b) in enumerate(evs):
+            if write:
+                flush.fill_(i & 0xFF)
+            else:
+                flush_words.sum()
+            torch.cuda.synchronize()
+            a.record()
+            call()
+            b.record()
+        torch.cuda.synchronize()
+        return float(np.mean([a.elapsed_time(b) for a, b in evs])) / 1e3
+
+    t_dec = flushed(lambda: cache.decode(q, seq, n_att, out, ws))
+    t_dec_wflush = flushed(lambda: cache.decode(q, seq, n_att, out, ws), write=True)
     # the same decode with rotary position embeddings (keys cached pre-RoPE, rotated after reconstruction):
     # same bytes, plus the reconstruction of every key on the matrix cores
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
-    for i, (a, b) in enumerate(evs):
-        flush.fill_(i & 0xFF)
-        a.record()
-        kvc.kvc_decode_attn_rope(cache.K, cache.V, q, w.group, seq, n_att, 500000.0, out, ws)
-        b.record()
-    torch.cuda.synchronize()
-    t_rope = float(np.mean([a.elapsed_time(b) for a, b in evs])) / 1e3
-    del flush
+    t_rope = flushed(lambda: kvc.kvc_decode_attn_rope(cache.K, cache.V, q, w.group, seq, n_att, 500000.0, out, ws))
+    del flush, flush_words
     assert torch.isfinite(out).all().item()
 
     # achievable HBM read rate on this device: the library's streaming-read probe over 2 GiB (best of 5)
@@ -502,7 +509,8 @@ def main():
     value = step_bytes / (ms_step / 1e3) / 1e9
     achieved = dec_bytes / t_dec / 1e9
     log(f"decode call {t_dec * 1e3:.3f} ms, {achieved:.1f} GB/s algorithmic ({dec_bytes / 1e9:.3f} GB); "
-        f"back to back {t_b2b * 1e3:.3f} ms; read probe {read_gbs:.1f} GB/s")
+        f"back to back {t_b2b * 1e3:.3f} ms; after a write flush {t_dec_wflush * 1e3:.3f} ms; "
+        f"read probe {read_gbs:.1f} GB/s")
 
     res_workload = w.name + ("" if args.uniform is None else "@uniform_k{}_{}_v{}_{}".format(*args.uniform))
     res = {
@@ -516,7 +524,10 @@ def main():
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(dec_bytes, res_workload),
                      "kernel": "kvc_decode_attn (qproj + decode_partial + combine)",
                      "alg_bytes_per_launch": dec_bytes, "avg_launch_ms": round(t_dec * 1e3, 4),
-                     "launch_ms_back_to_back": round(t_b2b * 1e3, 4), "achievable_read_GBs": round(read_gbs, 1),
+                     "launch_ms_back_to_back": round(t_b2b * 1e3, 4),
+                     "launch_ms_after_write_flush": round(t_dec_wflush * 1e3, 4),
+                     "flush": "512 MB read, then the device idles, before each timed call",
+                     "achievable_read_GBs": round(read_gbs, 1),
                      "frac_of_achievable": round(achieved / read_gbs, 4)},
         "step": {"fused_ms": round(ms_step, 4), "two_calls_ms": round(ms_two, 4),
                  "bytes": step_bytes, "note": "append of the new token + decode attention over T + 1 tokens"},
