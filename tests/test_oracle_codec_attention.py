@@ -186,6 +186,29 @@ def test_layout_v_groups_hand_derived():
     assert list(np.nonzero(s)[0]) == [1330] and s[1330] == 77
 
 
+def test_layout_v_group_closed_form():
+    # The kernels address a value field by a closed form instead of the enumeration: for lane
+    # L = 4 c + q and N-tile n = g Q + j, byte 2p (g L + j) of group Q (at 1024 Q) in a full group, and
+    # 2p (m L - A + j) in the last one (m N-tiles, its last holding ct coordinates, A = 4 (c - ct) + q
+    # for c >= ct, else 0). A lane's run of fields in a group starts at a multiple of 4 bytes except in
+    # a 1-bit plane, where the fields still lie in the 16 bytes from the dword boundary below the start.
+    for r in range(2, 129, 2):
+        nvt = (r + 15) // 16
+        ct = r - 16 * (nvt - 1)
+        for p in (1, 2, 4, 8):
+            tab = ol.v_field_bytes(r, p)
+            g = 1 if p == 8 else 8 // p
+            ql = (nvt - 1) // g
+            m = nvt - g * ql
+            for (n, c, q), off in tab.items():
+                Q, j, L = n // g, n % g, 4 * c + q
+                A = 4 * (c - ct) + q if c >= ct else 0
+                start = 1024 * Q + (2 * p * (m * L - A) if Q == ql else 16 * L)
+                assert off == start + 2 * p * j, (r, p, n, c, q)
+                assert start % 4 == 0 or p == 1, (r, p, n, c, q)
+                assert off + 2 * p <= (start & ~3) + 16, (r, p, n, c, q)
+
+
 @pytest.mark.parametrize("r", [2, 16, 18, 40, 64, 84, 100, 126, 128])
 @pytest.mark.parametrize("b", [1, 2, 3, 4, 5, 7, 8])
 def test_layout_v_fields_tile_the_plane(r, b):
