@@ -447,10 +447,12 @@ def main():
 
     # decode call alone, events on the launch stream, for the roofline entry: back to back, and with the
     # 256 MB MALL flushed before each call, outside the events; the roofline takes the mean of the
-    # flushed calls. The flush reads a 512 MB buffer (a reduction), then the device idles: the MALL then
-    # holds other, clean lines, so the call reads its codes from HBM. A flush by writing the buffer leaves
-    # the MALL full of dirty lines whose write-back overlaps the next call and takes HBM time from it
-    # (about 55 us per call on the 8B-shaped 32k workload); that variant is reported as well.
+    # flushed calls. The flush reads a 512 MB buffer (a reduction on the same stream, which ends before
+    # the first event): the MALL then holds other, clean lines, so the call reads its codes from HBM. A
+    # flush by writing the buffer leaves the MALL full of dirty lines whose write-back overlaps the next
+    # call and takes HBM time from it (about 55 us per call on the 8B-shaped 32k workload); that variant
+    # is reported as well, with the device idle before each call (an idle device also starts the call
+    # at lower clocks, which the issue-bound workloads feel).
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
     for a, b in evs:
         a.record()
@@ -467,9 +469,9 @@ def main():
         for i, (a, b) in enumerate(evs):
             if write:
                 flush.fill_(i & 0xFF)
+                torch.cuda.synchronize()
             else:
                 flush_words.sum()
-            torch.cuda.synchronize()
             a.record()
             call()
             b.record()
@@ -526,7 +528,7 @@ def main():
                      "alg_bytes_per_launch": dec_bytes, "avg_launch_ms": round(t_dec * 1e3, 4),
                      "launch_ms_back_to_back": round(t_b2b * 1e3, 4),
                      "launch_ms_after_write_flush": round(t_dec_wflush * 1e3, 4),
-                     "flush": "512 MB read, then the device idles, before each timed call",
+                     "flush": "512 MB read on the same stream before each timed call",
                      "achievable_read_GBs": round(read_gbs, 1),
                      "frac_of_achievable": round(achieved / read_gbs, 4)},
         "step": {"fused_ms": round(ms_step, 4), "two_calls_ms": round(ms_two, 4),
